@@ -1,0 +1,457 @@
+// Host side of libsx: argument validation, plan construction (segment metadata, probe and base
+// row sets, cos/sin tables) and dispatch of the HIP kernels.  See include/sx.h for the ABI.
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <new>
+
+#include "sx_internal.h"
+
+namespace {
+
+thread_local std::string g_err;
+
+sx_status fail(sx_status st, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof(buf), fmt, ap);
+  va_end(ap);
+  g_err = buf;
+  return st;
+}
+
+sx_status ok() { return SX_OK; }
+
+sx_status hip_fail(hipError_t e, const char* what) {
+  return fail(SX_EHIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+// Checks a launch: the launcher's own status, then the runtime's sticky launch error.
+sx_status check_launch(hipError_t e, const char* what) {
+  if (e != hipSuccess) return hip_fail(e, what);
+  e = hipGetLastError();
+  if (e != hipSuccess) return hip_fail(e, what);
+  return SX_OK;
+}
+
+sx_status validate_desc(const sx_layer_desc* d) {
+  if (!d) return fail(SX_EINVAL, "desc is NULL");
+  if (d->n_q_heads < 1 || d->n_kv_heads < 1) return fail(SX_ESHAPE, "head counts must be >= 1");
+  if (d->n_q_heads % d->n_kv_heads != 0)
+    return fail(SX_ESHAPE, "n_q_heads (%d) must be a multiple of n_kv_heads (%d)", d->n_q_heads, d->n_kv_heads);
+  if (d->n_q_heads / d->n_kv_heads > 128) return fail(SX_EUNSUPPORTED, "more than 128 query heads per KV head");
+  if (d->head_dim != 64 && d->head_dim != 128)
+    return fail(SX_EUNSUPPORTED, "head_dim %d unsupported (64 or 128)", d->head_dim);
+  if (d->block_size != sx::kBlock) return fail(SX_EUNSUPPORTED, "block_size %d unsupported (16)", d->block_size);
+  if (d->dtype != SX_F32 && d->dtype != SX_BF16) return fail(SX_EUNSUPPORTED, "dtype %d unsupported", d->dtype);
+  if (d->rope_style != SX_ROPE_NEOX && d->rope_style != SX_ROPE_GPTJ)
+    return fail(SX_EINVAL, "rope_style %d unknown", d->rope_style);
+  if (!(d->rope_base > 0.0) || !std::isfinite(d->rope_base)) return fail(SX_EINVAL, "rope_base must be > 0");
+  if (!(d->softmax_scale >= 0.0f) || !std::isfinite(d->softmax_scale))
+    return fail(SX_EINVAL, "softmax_scale must be finite and >= 0");
+  if (d->reserved != 0) return fail(SX_EINVAL, "reserved field must be 0");
+  return SX_OK;
+}
+
+float effective_scale(const sx_layer_desc* d) {
+  return d->softmax_scale > 0.0f ? d->softmax_scale : (float)(1.0 / std::sqrt((double)d->head_dim));
+}
+
+template <typename T>
+sx_status dev_alloc(sx_plan* p, T** ptr, size_t count) {
+  *ptr = nullptr;
+  if (count == 0) count = 1;
+  hipError_t e = hipMalloc((void**)ptr, count * sizeof(T));
+  if (e != hipSuccess) {
+    *ptr = nullptr;
+    return fail(SX_ENOMEM, "hipMalloc of %zu bytes failed: %s", count * sizeof(T), hipGetErrorString(e));
+  }
+  p->device_bytes += (int64_t)(count * sizeof(T));
+  return SX_OK;
+}
+
+template <typename T>
+sx_status dev_upload(sx_plan* p, T** ptr, const std::vector<T>& host) {
+  sx_status st = dev_alloc(p, ptr, host.size());
+  if (st != SX_OK) return st;
+  if (!host.empty()) {
+    hipError_t e = hipMemcpy(*ptr, host.data(), host.size() * sizeof(T), hipMemcpyHostToDevice);
+    if (e != hipSuccess) return hip_fail(e, "hipMemcpy (plan upload)");
+  }
+  return SX_OK;
+}
+
+void free_plan(sx_plan* p) {
+  if (!p) return;
+  void* bufs[] = {p->d_req, p->d_bt, p->d_ra, p->d_cs, p->d_probe, p->d_nr,
+                  p->d_n_nr, p->d_n_probe, p->d_flags, p->d_lse, p->d_colsum};
+  for (void* b : bufs)
+    if (b) (void)hipFree(b);
+  delete p;
+}
+
+// k_r = min(n, floor(ratio * n + 1/2)), each float64 operation rounded on its own.
+int64_t budget_of(int64_t n, double ratio) {
+#pragma clang fp contract(off)
+  volatile double prod = ratio * (double)n;
+  double k = std::floor(prod + 0.5);
+  if (k > (double)n) k = (double)n;
+  if (k < 0) k = 0;
+  return (int64_t)k;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* sx_last_error(void) { return g_err.c_str(); }
+
+const char* sx_version(void) { return "libsx 0.1 (gfx950)"; }
+
+sx_status sx_plan_create(const sx_layer_desc* desc, const sx_request* requests, int32_t n_requests,
+                         int64_t n_dst_blocks, int64_t n_src_blocks, sx_plan** out) {
+  if (!out) return fail(SX_EINVAL, "out is NULL");
+  sx_status st = validate_desc(desc);
+  if (st != SX_OK) return st;
+  if (!requests || n_requests < 1) return fail(SX_EINVAL, "need at least one request");
+  if (n_dst_blocks < 1 || n_src_blocks < 0) return fail(SX_ESHAPE, "bad pool sizes");
+  if (n_dst_blocks > (INT32_MAX / sx::kBlock) || n_src_blocks > (INT32_MAX / sx::kBlock))
+    return fail(SX_EUNSUPPORTED, "pool larger than 2^31 slots");
+  const int b = desc->block_size;
+  const int d = desc->head_dim;
+
+  // ---- validate every request before allocating anything ----
+  int64_t total = 0;
+  std::vector<uint8_t> dst_seen((size_t)n_dst_blocks, 0);
+  for (int r = 0; r < n_requests; ++r) {
+    const sx_request& q = requests[r];
+    if (q.n_tokens < 1) return fail(SX_EINVAL, "request %d: n_tokens must be >= 1", r);
+    if (q.n_segments < 1 || !q.segments) return fail(SX_EINVAL, "request %d: no segments", r);
+    if (!q.block_table) return fail(SX_EINVAL, "request %d: block_table is NULL", r);
+    int64_t t = 0;
+    for (int m = 0; m < q.n_segments; ++m) {
+      const sx_segment& s = q.segments[m];
+      if (s.seq_start != t) return fail(SX_EINVAL, "request %d segment %d: starts at %d, expected %lld", r, m,
+                                        s.seq_start, (long long)t);
+      if (s.length < 1) return fail(SX_EINVAL, "request %d segment %d: length must be >= 1", r, m);
+      if (s.cached != 0 && s.cached != 1) return fail(SX_EINVAL, "request %d segment %d: cached must be 0/1", r, m);
+      if (s.new_pos < 0 || (int64_t)s.new_pos + s.length > INT32_MAX)
+        return fail(SX_EINVAL, "request %d segment %d: bad new_pos", r, m);
+      if (s.cached) {
+        if (s.old_pos < 0 || (int64_t)s.old_pos + s.length > INT32_MAX)
+          return fail(SX_EINVAL, "request %d segment %d: bad old_pos", r, m);
+        const int64_t nb = (s.length + b - 1) / b;
+        if (!q.src_block_ids || s.src_block_start < 0 || s.src_block_start + nb > q.n_src_block_ids)
+          return fail(SX_ESHAPE, "request %d segment %d: source blocks out of range", r, m);
+        for (int64_t i = 0; i < nb; ++i) {
+          const int32_t id = q.src_block_ids[s.src_block_start + i];
+          if (id < 0 || id >= n_src_blocks)
+            return fail(SX_ESHAPE, "request %d segment %d: source block id %d out of range", r, m, id);
+        }
+      }
+      t += s.length;
+    }
+    if (t != q.n_tokens) return fail(SX_EINVAL, "request %d: segments cover %lld tokens, n_tokens is %d", r,
+                                     (long long)t, q.n_tokens);
+    const int64_t nblk = (q.n_tokens + b - 1) / b;
+    for (int64_t i = 0; i < nblk; ++i) {
+      const int32_t id = q.block_table[i];
+      if (id < 0 || id >= n_dst_blocks)
+        return fail(SX_ESHAPE, "request %d: destination block id %d out of range", r, id);
+      if (dst_seen[id]) return fail(SX_EINVAL, "destination block %d used twice", id);
+      dst_seen[id] = 1;
+    }
+    total += q.n_tokens;
+    if (total > INT32_MAX) return fail(SX_EUNSUPPORTED, "more than 2^31 tokens in one plan");
+  }
+
+  sx_plan* p = new (std::nothrow) sx_plan();
+  if (!p) return fail(SX_ENOMEM, "host allocation failed");
+  p->desc = *desc;
+  p->scale = effective_scale(desc);
+  p->n_req = n_requests;
+  p->total = total;
+  p->n_dst_blocks = n_dst_blocks;
+  p->n_src_blocks = n_src_blocks;
+  (void)hipGetDevice(&p->device);
+
+  // ---- derive the per-token sets (Sections 3.2-3.3, Algorithm 1 steps 15-16) ----
+  std::vector<sx::ReqDev> rdev(n_requests);
+  std::vector<int32_t> bt_all;
+  std::vector<sx::RealignRow> ra;
+  std::vector<float2> cs;
+  std::vector<int32_t> probe((size_t)total, 0), nr((size_t)total, 0);
+  std::vector<int32_t> n_nr(n_requests), n_probe(n_requests);
+  std::vector<uint8_t> flags((size_t)total, 0);
+  std::vector<double> theta(d / 2);
+  for (int i = 0; i < d / 2; ++i) theta[i] = std::pow(desc->rope_base, -2.0 * i / d);
+  int64_t off = 0;
+  int32_t cs_rows = 0;
+  for (int r = 0; r < n_requests; ++r) {
+    const sx_request& q = requests[r];
+    const int T = q.n_tokens;
+    sx::HostReq h{};
+    h.T = T;
+    h.tok_off = (int32_t)off;
+    h.bt_off = (int32_t)bt_all.size();
+    const int nblk = (T + b - 1) / b;
+    bt_all.insert(bt_all.end(), q.block_table, q.block_table + nblk);
+    uint8_t* fl = flags.data() + off;
+    const sx_segment* last = nullptr;
+    for (int m = 0; m < q.n_segments; ++m) {
+      const sx_segment& s = q.segments[m];
+      if (s.seq_start <= T - 1 && T - 1 < s.seq_start + s.length) last = &s;
+      if (!s.cached) continue;
+      const double delta = (double)s.new_pos - (double)s.old_pos;
+      for (int i = 0; i < d / 2; ++i) {
+        const double phi = delta * theta[i];
+        cs.push_back(make_float2((float)std::cos(phi), (float)std::sin(phi)));
+      }
+      for (int j = 0; j < s.length; ++j) {
+        const int tok = s.seq_start + j;
+        fl[tok] |= sx::kFlagCandidate;
+        sx::RealignRow row;
+        row.src_slot = q.src_block_ids[s.src_block_start + j / b] * b + (j % b);
+        row.dst_slot = q.block_table[tok / b] * b + (tok % b);
+        row.cs_row = cs_rows;
+        row.pad = 0;
+        ra.push_back(row);
+      }
+      ++cs_rows;
+    }
+    // I_nr, overflow blocks around each maximal uncached run, tail fallback
+    int cnt_nr = 0;
+    for (int t = 0; t < T; ++t)
+      if (!(fl[t] & sx::kFlagCandidate)) nr[off + cnt_nr++] = t;
+    std::vector<uint8_t> base(T, 0);
+    for (int t = 0; t < T;) {
+      if (fl[t] & sx::kFlagCandidate) { ++t; continue; }
+      const int a = t;
+      while (t < T && !(fl[t] & sx::kFlagCandidate)) base[t++] = 1;
+      const int e = t;
+      for (int x = (a - b > 0 ? a - b : 0); x < a; ++x) base[x] = 1;
+      for (int x = e; x < T && x < e + b; ++x) base[x] = 1;
+    }
+    int tail_lo = T;  // tail-fallback rows [tail_lo, T) when the final segment is reused
+    if (last && last->cached) tail_lo = (T - sx::kTail > last->seq_start) ? T - sx::kTail : last->seq_start;
+    for (int t = tail_lo; t < T; ++t) base[t] = 1;
+    int cnt_probe = 0, cnt_base = 0, cnt_reuse = 0;
+    for (int t = 0; t < T; ++t) {
+      const bool cand = fl[t] & sx::kFlagCandidate;
+      cnt_reuse += cand;
+      if (!cand || t >= tail_lo) probe[off + cnt_probe++] = t;
+      if (base[t]) { fl[t] |= sx::kFlagBase; ++cnt_base; }
+    }
+    h.n_reuse = cnt_reuse;
+    h.n_probe = cnt_probe;
+    h.n_nr = cnt_nr;
+    h.n_base = cnt_base;
+    p->reqs.push_back(h);
+    rdev[r] = sx::ReqDev{h.T, h.tok_off, h.bt_off, h.n_reuse, h.n_probe, h.n_nr, h.n_base, 0};
+    n_nr[r] = cnt_nr;
+    n_probe[r] = cnt_probe;
+    p->n_reuse += cnt_reuse;
+    p->n_nr += cnt_nr;
+    p->n_probe += cnt_probe;
+    p->n_base += cnt_base;
+    if (cnt_nr > p->max_nr) p->max_nr = cnt_nr;
+    if (cnt_probe > p->max_probe) p->max_probe = cnt_probe;
+    if (T > p->max_T) p->max_T = T;
+    off += T;
+  }
+  p->n_realign = (int64_t)ra.size();
+
+  st = SX_OK;
+  if (st == SX_OK) st = dev_upload(p, &p->d_req, rdev);
+  if (st == SX_OK) st = dev_upload(p, &p->d_bt, bt_all);
+  if (st == SX_OK) st = dev_upload(p, &p->d_ra, ra);
+  if (st == SX_OK) st = dev_upload(p, &p->d_cs, cs);
+  if (st == SX_OK) st = dev_upload(p, &p->d_probe, probe);
+  if (st == SX_OK) st = dev_upload(p, &p->d_nr, nr);
+  if (st == SX_OK) st = dev_upload(p, &p->d_n_nr, n_nr);
+  if (st == SX_OK) st = dev_upload(p, &p->d_n_probe, n_probe);
+  if (st == SX_OK) st = dev_upload(p, &p->d_flags, flags);
+  if (st == SX_OK) st = dev_alloc(p, &p->d_lse, (size_t)total * desc->n_q_heads);
+  if (st == SX_OK) st = dev_alloc(p, &p->d_colsum, (size_t)total * desc->n_kv_heads);
+  if (st != SX_OK) {
+    std::string keep = g_err;
+    free_plan(p);
+    g_err = keep;
+    return st;
+  }
+  *out = p;
+  return ok();
+}
+
+sx_status sx_plan_destroy(sx_plan* plan) {
+  if (!plan) return SX_OK;
+  hipError_t e = hipDeviceSynchronize();
+  free_plan(plan);
+  if (e != hipSuccess) return hip_fail(e, "hipDeviceSynchronize before freeing the plan");
+  return SX_OK;
+}
+
+sx_status sx_plan_get_info(const sx_plan* p, sx_plan_info* info) {
+  if (!p || !info) return fail(SX_EINVAL, "NULL argument");
+  info->total_tokens = p->total;
+  info->n_requests = p->n_req;
+  info->max_tokens = p->max_T;
+  info->n_reused = p->n_reuse;
+  info->n_nonreused = p->n_nr;
+  info->n_probes = p->n_probe;
+  info->n_base = p->n_base;
+  info->max_nonreused = p->max_nr;
+  info->max_probes = p->max_probe;
+  info->device_bytes = p->device_bytes;
+  return SX_OK;
+}
+
+sx_status sx_plan_budget(const sx_plan* p, double ratio, int64_t* k_total, int32_t* max_rows) {
+  if (!p) return fail(SX_EINVAL, "plan is NULL");
+  if (!(ratio >= 0.0 && ratio <= 1.0)) return fail(SX_EINVAL, "ratio must lie in [0, 1]");
+  int64_t kt = 0;
+  int64_t mr = 0;
+  for (const auto& h : p->reqs) {
+    const int64_t k = budget_of(h.n_reuse, ratio);
+    kt += k;
+    int64_t bound = h.n_base + k;
+    if (bound > h.T) bound = h.T;
+    if (bound > mr) mr = bound;
+  }
+  if (k_total) *k_total = kt;
+  if (max_rows) *max_rows = (int32_t)mr;
+  return SX_OK;
+}
+
+sx_status sx_plan_nonreused_rows(const sx_plan* p, const int32_t** rows, const int32_t** n_rows,
+                                 int32_t* max_rows) {
+  if (!p) return fail(SX_EINVAL, "plan is NULL");
+  if (rows) *rows = p->d_nr;
+  if (n_rows) *n_rows = p->d_n_nr;
+  if (max_rows) *max_rows = p->max_nr;
+  return SX_OK;
+}
+
+sx_status sx_rope_realign(const sx_plan* p, const void* src_k, const void* src_v, void* k_cache,
+                          void* v_cache, void* stream) {
+  if (!p) return fail(SX_EINVAL, "plan is NULL");
+  if (p->n_realign == 0) return SX_OK;
+  if (!src_k || !src_v || !k_cache || !v_cache) return fail(SX_EINVAL, "NULL tensor argument");
+  return check_launch(sx::launch_realign(p, src_k, src_v, k_cache, v_cache, (hipStream_t)stream),
+                      "sx_rope_realign launch");
+}
+
+sx_status sx_kv_scatter(const sx_plan* p, const void* k_new, const void* v_new, const int32_t* rows,
+                        const int32_t* n_rows, int32_t max_rows, void* k_cache, void* v_cache, void* stream) {
+  if (!p) return fail(SX_EINVAL, "plan is NULL");
+  if (!k_new || !v_new || !k_cache || !v_cache) return fail(SX_EINVAL, "NULL tensor argument");
+  if (rows) {
+    if (!n_rows) return fail(SX_EINVAL, "n_rows is NULL while rows is not");
+    if (max_rows < 0) return fail(SX_EINVAL, "max_rows must be >= 0");
+    if (max_rows == 0) return SX_OK;
+  }
+  return check_launch(sx::launch_scatter(p, k_new, v_new, rows, n_rows, rows ? max_rows : p->max_T, k_cache,
+                                         v_cache, (hipStream_t)stream),
+                      "sx_kv_scatter launch");
+}
+
+sx_status sx_sparseq_score(const sx_plan* p, const void* q, const void* k_cache, float* scores, void* stream) {
+  if (!p) return fail(SX_EINVAL, "plan is NULL");
+  if (!q || !k_cache || !scores) return fail(SX_EINVAL, "NULL tensor argument");
+  hipStream_t s = (hipStream_t)stream;
+  // pass 1: log-sum-exp of every (probe row, query head)
+  sx::AttnLaunch a{};
+  a.Hq = p->desc.n_q_heads;
+  a.Hkv = p->desc.n_kv_heads;
+  a.D = p->desc.head_dim;
+  a.n_req = p->n_req;
+  a.grid_rows = p->max_probe;
+  a.dtype = p->desc.dtype;
+  a.scale = p->scale;
+  a.q = q;
+  a.k = k_cache;
+  a.v = nullptr;
+  a.out = nullptr;
+  a.lse = p->d_lse;
+  a.lse_base2 = 1;
+  a.reqs = p->d_req;
+  a.bt = p->d_bt;
+  a.rows = p->d_probe;
+  a.n_rows = p->d_n_probe;
+  sx_status st = SX_OK;
+  if (p->max_probe > 0) {
+    st = check_launch(sx::launch_attn_paged(a, s), "sx_sparseq_score pass 1 launch");
+    if (st != SX_OK) return st;
+  }
+  // pass 2: per-key column sums of the probabilities, per KV head
+  st = check_launch(sx::launch_colsum(p, q, k_cache, s), "sx_sparseq_score pass 2 launch");
+  if (st != SX_OK) return st;
+  // pass 3: fixed-order sum over KV heads
+  return check_launch(sx::launch_head_reduce(p, scores, s), "sx_sparseq_score pass 3 launch");
+}
+
+sx_status sx_topk_select(const sx_plan* p, const float* scores, double ratio, int32_t* rows, int32_t* n_rows,
+                         void* stream) {
+  if (!p) return fail(SX_EINVAL, "plan is NULL");
+  if (!scores || !rows || !n_rows) return fail(SX_EINVAL, "NULL argument");
+  if (!(ratio >= 0.0 && ratio <= 1.0)) return fail(SX_EINVAL, "ratio must lie in [0, 1]");
+  return check_launch(sx::launch_topk(p, scores, ratio, rows, n_rows, (hipStream_t)stream),
+                      "sx_topk_select launch");
+}
+
+sx_status sx_sparse_attn(const sx_plan* p, const void* q, const int32_t* rows, const int32_t* n_rows,
+                         int32_t max_rows, const void* k_cache, const void* v_cache, void* out, void* stream) {
+  if (!p) return fail(SX_EINVAL, "plan is NULL");
+  if (!q || !rows || !n_rows || !k_cache || !v_cache || !out) return fail(SX_EINVAL, "NULL argument");
+  if (max_rows < 0) return fail(SX_EINVAL, "max_rows must be >= 0");
+  if (max_rows == 0) return SX_OK;
+  sx::AttnLaunch a{};
+  a.Hq = p->desc.n_q_heads;
+  a.Hkv = p->desc.n_kv_heads;
+  a.D = p->desc.head_dim;
+  a.n_req = p->n_req;
+  a.grid_rows = max_rows;
+  a.dtype = p->desc.dtype;
+  a.scale = p->scale;
+  a.q = q;
+  a.k = k_cache;
+  a.v = v_cache;
+  a.out = out;
+  a.lse = nullptr;
+  a.reqs = p->d_req;
+  a.bt = p->d_bt;
+  a.rows = rows;
+  a.n_rows = n_rows;
+  return check_launch(sx::launch_attn_paged(a, (hipStream_t)stream), "sx_sparse_attn launch");
+}
+
+sx_status sx_full_attn(const sx_layer_desc* desc, const void* q, const void* k, const void* v,
+                       const int32_t* cu_seqlens, int32_t n_requests, int32_t max_seqlen, void* out, float* lse,
+                       void* stream) {
+  sx_status st = validate_desc(desc);
+  if (st != SX_OK) return st;
+  if (!q || !k || !v || !out || !cu_seqlens) return fail(SX_EINVAL, "NULL argument");
+  if (n_requests < 1) return fail(SX_EINVAL, "n_requests must be >= 1");
+  if (max_seqlen < 0) return fail(SX_EINVAL, "max_seqlen must be >= 0");
+  if (max_seqlen == 0) return SX_OK;
+  sx::AttnLaunch a{};
+  a.Hq = desc->n_q_heads;
+  a.Hkv = desc->n_kv_heads;
+  a.D = desc->head_dim;
+  a.n_req = n_requests;
+  a.grid_rows = max_seqlen;
+  a.dtype = desc->dtype;
+  a.scale = effective_scale(desc);
+  a.q = q;
+  a.k = k;
+  a.v = v;
+  a.out = out;
+  a.lse = lse;
+  a.lse_base2 = 0;
+  a.cu = cu_seqlens;
+  return check_launch(sx::launch_attn_dense(a, (hipStream_t)stream), "sx_full_attn launch");
+}
+
+}  // extern "C"

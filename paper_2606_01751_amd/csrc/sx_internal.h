@@ -1,0 +1,107 @@
+// Internal declarations shared by the host library and the HIP kernels of libsx.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+#include <string>
+#include <vector>
+
+#include "sx.h"
+
+namespace sx {
+
+constexpr int kBlock = 16;     // paged-cache block size supported by the kernels
+constexpr int kTail = 64;      // tail-fallback rows (Section 3.2)
+
+// Per-request device metadata.
+struct ReqDev {
+  int32_t T;        // tokens of the request
+  int32_t tok_off;  // first token in the concatenation of all requests
+  int32_t bt_off;   // first entry of its block table in the concatenated tables
+  int32_t n_reuse;  // |I_reuse|: top-k candidates
+  int32_t n_probe;  // |I_nr U S_tail|: Sparse-Q rows
+  int32_t n_nr;     // |I_nr|
+  int32_t n_base;   // |I_nr U S_ov U S_tail|
+  int32_t pad;
+};
+
+// One reused token of the re-alignment pass.  Slots are pool-wide: block * kBlock + slot.
+struct RealignRow {
+  int32_t src_slot;
+  int32_t dst_slot;
+  int32_t cs_row;   // row of the cos/sin table (one row per cached segment)
+  int32_t pad;
+};
+
+// Token flags used by the selection kernel.
+enum : uint8_t { kFlagCandidate = 1, kFlagBase = 2 };
+
+struct HostReq {
+  int32_t T, tok_off, bt_off, n_reuse, n_probe, n_nr, n_base;
+};
+
+}  // namespace sx
+
+struct sx_plan {
+  sx_layer_desc desc;
+  float scale;                    // softmax scale actually used
+  int32_t n_req = 0;
+  int64_t total = 0;              // sum T
+  int32_t max_T = 0;
+  int64_t n_dst_blocks = 0, n_src_blocks = 0;
+  int32_t device = 0;
+  std::vector<sx::HostReq> reqs;
+  int64_t n_reuse = 0, n_nr = 0, n_probe = 0, n_base = 0;
+  int32_t max_nr = 0, max_probe = 0;
+  int64_t n_realign = 0;
+  int64_t device_bytes = 0;
+  // device memory owned by the plan
+  sx::ReqDev* d_req = nullptr;
+  int32_t* d_bt = nullptr;
+  sx::RealignRow* d_ra = nullptr;
+  float2* d_cs = nullptr;         // [cached segments][d/2] (cos, sin)
+  int32_t* d_probe = nullptr;     // row-list layout
+  int32_t* d_nr = nullptr;        // row-list layout
+  int32_t* d_n_nr = nullptr;      // [n_req]
+  int32_t* d_n_probe = nullptr;   // [n_req]
+  uint8_t* d_flags = nullptr;     // [sum T]
+  float* d_lse = nullptr;         // scratch [sum T][Hq]
+  double* d_colsum = nullptr;     // scratch [Hkv][sum T]
+};
+
+namespace sx {
+
+// Kernel launchers (defined in the .hip files).  Each returns the launch status.
+hipError_t launch_realign(const sx_plan* p, const void* src_k, const void* src_v, void* kc, void* vc,
+                          hipStream_t s);
+hipError_t launch_scatter(const sx_plan* p, const void* k_new, const void* v_new, const int32_t* rows,
+                          const int32_t* n_rows, int32_t max_rows, void* kc, void* vc, hipStream_t s);
+hipError_t launch_head_reduce(const sx_plan* p, float* scores, hipStream_t s);
+hipError_t launch_topk(const sx_plan* p, const float* scores, double ratio, int32_t* rows, int32_t* n_rows,
+                       hipStream_t s);
+
+// Attention family.  Mode selects the query rows and the key source.
+struct AttnLaunch {
+  int Hq, Hkv, D, n_req, grid_rows;   // grid_rows: max query rows of any request
+  int dtype;
+  float scale;
+  const void* q;
+  const void* k;
+  const void* v;
+  void* out;          // null in LSE-only mode
+  float* lse;         // optional
+  int lse_base2;      // 1: base-2 LSE of scale*q.k (score pass); 0: natural log
+  // paged mode
+  const ReqDev* reqs;
+  const int32_t* bt;
+  const int32_t* rows;
+  const int32_t* n_rows;
+  // dense mode
+  const int32_t* cu;
+};
+hipError_t launch_attn_paged(const AttnLaunch& a, hipStream_t s);   // rows over a paged cache
+hipError_t launch_attn_dense(const AttnLaunch& a, hipStream_t s);   // all rows, dense K/V
+hipError_t launch_colsum(const sx_plan* p, const void* q, const void* kc, hipStream_t s);
+
+}  // namespace sx
