@@ -1,0 +1,305 @@
+"""Throughput of the sparse-KV recomputation step on one MI355X.
+
+Default workload: the 32-layer hybrid chat stack (T = 32768 tokens, 32 query / 8 KV heads,
+head_dim 128, bf16, recompute ratio 15 %).  One step is one pass of the whole path over the
+stack:
+    layers 0-3   KV write of every row + full causal attention
+    boundary     Sparse-Q scoring + top-k selection on layer 3 (fresh keys of every token)
+    layers 4-31  RoPE re-alignment + KV write of R + sparse attention of R
+Inputs (per-layer Q/K/V and source pools, seeded N(0,1)) are resident in HBM before timing.
+
+value = effective prefill tokens/s per layer = T * L / (seconds per step).
+
+Prints one JSON line with the metric, per-kernel timings (HIP events on the launch stream),
+the roofline of the dominant kernel and the CPU oracle timed on a bounded sample.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_BF16_TFLOPS = 2500.0     # MI355X dense bf16 matrix peak
+PEAK_F32_TFLOPS = 157.3       # MI355X fp32 vector peak
+PEAK_HBM_GBS = 8000.0         # MI355X HBM3E
+METRIC = "effective prefill tokens/s per layer at 15% recompute; MFMA util + HBM GB/s"
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=5)
+    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--config", type=int, default=3, help="named workload c1..c5")
+    ap.add_argument("--ratio", type=float, default=None)
+    ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--layers", type=int, default=None, help="override the number of layers (profiling)")
+    return ap.parse_args()
+
+
+class Timers:
+    """HIP events around each launch, recorded on the stream the library launches on."""
+
+    def __init__(self, torch):
+        self.torch = torch
+        self.ev = {}
+        self.on = False
+
+    def run(self, name, fn):
+        if not self.on:
+            fn()
+            return
+        s = self.torch.cuda.Event(enable_timing=True)
+        e = self.torch.cuda.Event(enable_timing=True)
+        s.record()
+        fn()
+        e.record()
+        self.ev.setdefault(name, []).append((s, e))
+
+    def summary(self):
+        out = {}
+        for k, lst in self.ev.items():
+            ms = [s.elapsed_time(e) for s, e in lst]
+            out[k] = {"launches": len(ms), "avg_ms": float(np.mean(ms)), "total_ms": float(np.sum(ms))}
+        return out
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported (the step is not sharded).",
+              file=sys.stderr)
+        sys.exit(2)
+    import torch
+
+    import paper_2606_01751_amd as sx
+    import workloads as W
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    torch.cuda.set_device(0)
+    w = W.config(args.config, seed=args.seed)
+    ratio = args.ratio if args.ratio is not None else (0.15 if 0.15 in w.ratios else w.ratios[0])
+    L = args.layers if args.layers else w.n_layers
+    nfull = min(w.n_full_layers, L)
+    T = w.total_tokens
+    Hq, Hkv, d = w.n_q_heads, w.n_kv_heads, w.head_dim
+    esz = 2 if w.dtype == "bf16" else 4
+    dt = torch.bfloat16 if w.dtype == "bf16" else torch.float32
+    desc = sx.make_desc(Hq, Hkv, d, w.dtype, w.rope_base, w.rope_style)
+    plan = sx.Plan(desc, w.requests, w.n_dst_blocks, w.n_src_blocks)
+    info = plan.info()
+    k_total, max_rows = plan.budget(ratio)
+    log(f"workload {w.name}: T={T} layers={L} (full {nfull}) ratio={ratio} k={k_total} max_rows={max_rows}")
+
+    t0 = time.time()
+    layers = []
+    pool = (w.n_dst_blocks, Hkv, w.block_size, d)
+    for l in range(L):
+        need = ("q", "k", "v") + (("k_src", "v_src") if l >= nfull else ())
+        tl = W.layer_tensors_torch(w, l, args.seed, which=need)
+        tl["kc"] = torch.zeros(pool, dtype=dt, device="cuda")
+        tl["vc"] = torch.zeros(pool, dtype=dt, device="cuda")
+        layers.append(tl)
+    out = torch.empty((T, Hq, d), dtype=dt, device="cuda")
+    scores = torch.zeros(T, dtype=torch.float32, device="cuda")
+    rows = torch.zeros(T, dtype=torch.int32, device="cuda")
+    n_rows = torch.zeros(len(w.requests), dtype=torch.int32, device="cuda")
+    cu = torch.tensor(w.token_offsets, dtype=torch.int32, device="cuda")
+    max_T = max(r.n_tokens for r in w.requests)
+    nr_rows, nr_n, nr_max = plan.nonreused_rows()
+    torch.cuda.synchronize()
+    log(f"inputs resident in HBM ({torch.cuda.memory_allocated() / 2**30:.1f} GiB) in {time.time() - t0:.1f}s")
+
+    tm = Timers(torch)
+
+    def step():
+        for l in range(nfull):
+            tl = layers[l]
+            tm.run("sx_kv_scatter", lambda: sx.kv_scatter(plan, tl["k"], tl["v"], tl["kc"], tl["vc"]))
+            tm.run("sx_full_attn", lambda: sx.full_attn(desc, tl["q"], tl["k"], tl["v"], cu, len(w.requests), max_T,
+                                                        out))
+        if nfull == 0:
+            # single selecting layer: mixed keys (re-aligned cached + fresh uncached)
+            tl = layers[0]
+            tm.run("sx_rope_realign", lambda: sx.rope_realign(plan, tl["k_src"], tl["v_src"], tl["kc"], tl["vc"]))
+            tm.run("sx_kv_scatter", lambda: sx.kv_scatter(plan, tl["k"], tl["v"], tl["kc"], tl["vc"], rows=nr_rows,
+                                                          n_rows=nr_n, max_rows=nr_max))
+            sel = tl
+        else:
+            sel = layers[nfull - 1]
+        tm.run("sx_sparseq_score", lambda: sx.sparseq_score(plan, sel["q"], sel["kc"], scores))
+        tm.run("sx_topk_select", lambda: sx.topk_select(plan, scores, ratio, rows, n_rows))
+        for l in range(max(nfull, 0), L):
+            tl = layers[l]
+            if not (nfull == 0 and l == 0):
+                tm.run("sx_rope_realign",
+                       lambda: sx.rope_realign(plan, tl["k_src"], tl["v_src"], tl["kc"], tl["vc"]))
+            tm.run("sx_kv_scatter", lambda: sx.kv_scatter(plan, tl["k"], tl["v"], tl["kc"], tl["vc"], rows=rows,
+                                                          n_rows=n_rows, max_rows=max_rows))
+            tm.run("sx_sparse_attn", lambda: sx.sparse_attn(plan, tl["q"], rows, n_rows, max_rows, tl["kc"], tl["vc"],
+                                                            out))
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    # the recompute set is a function of the fixed inputs: read it once for the work counts
+    offs = w.token_offsets
+    R = [rows[offs[r]:offs[r] + int(n_rows[r])].cpu().numpy().astype(np.int64) for r in range(len(w.requests))]
+
+    tm.on = True
+    torch.cuda.synchronize()
+    t_start = time.perf_counter()
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t_start
+    ms_per_step = elapsed * 1e3 / args.steps
+    kern = tm.summary()
+
+    # ---- algorithmic work per launch ----
+    def probe_rows(req):
+        cached = req.cached_mask()
+        last = [sg for sg in req.segments if sg.seq_start <= req.n_tokens - 1 < sg.seq_start + sg.length][0]
+        p = ~cached
+        if last.cached:
+            p[max(last.seq_start, req.n_tokens - 64):] = True
+        return np.flatnonzero(p)
+
+    pairs_R = float(sum(np.sum(Rr + 1) for Rr in R))
+    pairs_P = float(sum(np.sum(probe_rows(req) + 1) for req in w.requests))
+    pairs_full = float(sum(req.n_tokens * (req.n_tokens + 1) / 2 for req in w.requests))
+    n_R = int(sum(len(Rr) for Rr in R))
+    row_bytes = Hkv * d * esz
+    work = {
+        "sx_sparse_attn": ("mfma", 4.0 * Hq * d * pairs_R),
+        "sx_full_attn": ("mfma", 4.0 * Hq * d * pairs_full),
+        "sx_sparseq_score": ("mfma", 2.0 * Hq * d * pairs_P),
+        "sx_rope_realign": ("hbm", 4.0 * info["n_reused"] * row_bytes),
+        "sx_topk_select": ("latency", 5.0 * T),
+    }
+    # KV write: all rows in the full layers, R in the sparse layers (and I_nr in a selecting layer)
+    n_scatter_rows = nfull * T + (L - nfull) * n_R + (info["n_nonreused"] if nfull == 0 else 0)
+    n_scatter_launches = nfull + (L - nfull) + (1 if nfull == 0 else 0)
+    work["sx_kv_scatter"] = ("hbm", 4.0 * row_bytes * n_scatter_rows / n_scatter_launches)
+    peak = PEAK_BF16_TFLOPS if w.dtype == "bf16" else PEAK_F32_TFLOPS
+    kernels = {}
+    for name, k in kern.items():
+        kind, amount = work[name]
+        sec = k["avg_ms"] / 1e3
+        e = {"launches_per_step": k["launches"] // args.steps, "avg_us": round(k["avg_ms"] * 1e3, 2),
+             "share_of_step": round(k["total_ms"] / args.steps / ms_per_step, 4)}
+        if kind == "mfma":
+            e["tflops"] = round(amount / sec / 1e12, 2)
+            e["frac_of_peak"] = round(amount / sec / 1e12 / peak, 4)
+        elif kind == "hbm":
+            e["gbps"] = round(amount / sec / 1e9, 1)
+            e["frac_of_peak"] = round(amount / sec / 1e9 / PEAK_HBM_GBS, 4)
+        kernels[name] = e
+    dom = max(kern, key=lambda n: kern[n]["total_ms"])
+    kind, amount = work[dom]
+    sec = kern[dom]["avg_ms"] / 1e3
+    if kind == "hbm":
+        roof = {"kernel": dom, "bound": "hbm", "achieved": round(amount / sec / 1e9, 1), "peak": PEAK_HBM_GBS,
+                "unit": "GB/s", "frac": round(amount / sec / 1e9 / PEAK_HBM_GBS, 4), "traffic": None}
+    else:
+        roof = {"kernel": dom, "bound": "mfma", "achieved": round(amount / sec / 1e12, 2), "peak": peak,
+                "unit": "TFLOP/s", "frac": round(amount / sec / 1e12 / peak, 4), "traffic": None,
+                "algorithmic_per_launch": amount}
+
+    value = T * L / (ms_per_step / 1e3)
+    cpu = None
+    if not args.no_cpu_baseline:
+        cpu = cpu_baseline(w, layers, R, nfull, L, ratio, torch)
+    res = {
+        "metric": METRIC, "value": round(value, 1), "unit": "tokens/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": round(ms_per_step, 3), "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": w.dtype, "data": "synthetic (seeded N(0,1) inputs, layout rules of the workload)",
+        "config": {"workload": f"{w.name}: {w.description}", "tokens": T, "layers": L, "full_layers": nfull,
+                   "ratio": ratio, "recompute_rows": n_R, "k": int(k_total), "q_heads": Hq, "kv_heads": Hkv,
+                   "head_dim": d, "requests": len(w.requests)},
+        "kernels": kernels, "roofline": roof, "cpu_baseline": cpu,
+    }
+    print(json.dumps(res), flush=True)
+    plan.close()
+
+
+def cpu_baseline(w, layers, R, nfull, L, ratio, torch):
+    """The CPU oracle timed on a bounded sample of one step, scaled to the metric.
+
+    Timed on the host: one layer's full re-alignment, KV writes and top-k selection; the
+    attention and scoring rows of the oracle on samples of rows, scaled by the oracle's own cost
+    model (the matrix form costs the same per row; the per-row full attention costs i + 1)."""
+    import threadpoolctl
+
+    import oracle as O
+
+    rng = np.random.default_rng(0)
+    b = w.block_size
+    scale = O.softmax_scale(w.head_dim)
+    req = w.requests[0]
+    lay = layers[min(nfull, L - 1)]
+    h = {k: lay[k].float().cpu().numpy() for k in ("q", "k", "v", "k_src", "v_src") if k in lay}
+    threads = max(x.get("num_threads", 1) for x in threadpoolctl.threadpool_info()) if threadpoolctl.threadpool_info() else 1
+    T = req.n_tokens
+    kp = np.zeros((w.n_dst_blocks, w.n_kv_heads, b, w.head_dim), np.float32)
+    vp = np.zeros_like(kp)
+    t = {}
+    s0 = time.perf_counter()
+    for r in w.requests:
+        O.realign_request(r, w, h["k_src"], h["v_src"], kp, vp)
+    t["realign"] = time.perf_counter() - s0
+    s0 = time.perf_counter()
+    O.scatter_rows(req, w, R[0], h["k"], h["v"], kp, vp)
+    t["scatter_R"] = (time.perf_counter() - s0) * len(w.requests)
+    s0 = time.perf_counter()
+    O.scatter_rows(req, w, np.arange(T), h["k"], h["v"], kp, vp)
+    t["scatter_all"] = (time.perf_counter() - s0) * len(w.requests)
+    kt, vt = O.gather_tokens(req, w, kp), O.gather_tokens(req, w, vp)
+    ns = 32
+    samp = np.sort(rng.choice(len(R[0]), size=min(ns, len(R[0])), replace=False))
+    s0 = time.perf_counter()
+    O.attention_rows(h["q"][:T], kt, vt, R[0][samp], scale)
+    t["sparse_attn"] = (time.perf_counter() - s0) * sum(len(x) for x in R) / len(samp)
+    probes = np.flatnonzero(~req.cached_mask())
+    ps = np.sort(rng.choice(probes, size=min(ns, len(probes)), replace=False))
+    s0 = time.perf_counter()
+    sc = O.sparseq_scores(h["q"][:T], kt, ps, scale)
+    t["score"] = (time.perf_counter() - s0) * sum(int((~r.cached_mask()).sum()) for r in w.requests) / len(ps)
+    s0 = time.perf_counter()
+    O.recompute_set(T, req.segments, sc, ratio, b)
+    t["topk"] = (time.perf_counter() - s0) * len(w.requests)
+    full_rows = np.sort(rng.choice(T, size=ns, replace=False))
+    s0 = time.perf_counter()
+    O.full_attention(h["q"][:T], h["k"][:T], h["v"][:T], scale, rows=full_rows)
+    frac = float(np.sum(full_rows + 1)) / (T * (T + 1) / 2)
+    t["full_attn"] = (time.perf_counter() - s0) / frac * sum(
+        r.n_tokens * (r.n_tokens + 1) / 2 for r in w.requests) / (T * (T + 1) / 2)
+    if nfull > 0:
+        t_step = nfull * (t["scatter_all"] + t["full_attn"]) + t["score"] + t["topk"] + (L - nfull) * (
+            t["realign"] + t["scatter_R"] + t["sparse_attn"])
+    else:
+        t_step = t["realign"] + 2 * t["scatter_R"] + t["score"] + t["topk"] + t["sparse_attn"]
+    value = w.total_tokens * L / t_step
+    return {"value": round(value, 2), "unit": "tokens/s", "cores": int(threads), "kind": "oracle",
+            "sample": (f"one layer of request 0: full re-alignment, KV writes and top-k; attention of {len(samp)} "
+                       f"rows of R, {len(ps)} Sparse-Q probe rows and {ns} full-attention rows, scaled to the "
+                       f"whole {L}-layer step by the oracle's cost per row"),
+            "seconds_estimated_per_step": round(t_step, 2),
+            "step_seconds": {k: round(v, 4) for k, v in t.items()}}
+
+
+if __name__ == "__main__":
+    main()
