@@ -14,8 +14,13 @@
 //   * K tiles sit in LDS row-major (padded rows, conflict-free 16-byte reads).  V tiles sit in
 //     LDS as [key run of 4][d][4 keys], so the V^T A operand of a lane is two contiguous 8-byte
 //     reads and each loader thread writes 64 contiguous bytes.
-//   * Global loads of the next K/V tile are issued before the current tile is computed.
-//   * Query-row tiles are launched heaviest-first (latest rows see the most keys).
+//   * K/V tiles are double-buffered in LDS (one barrier per tile); global loads of tile j+2 are
+//     in flight while tile j is computed.
+//   * The 1-D grid is decoded KV head fastest, then request, then query-row tile from the latest
+//     rows (most keys) to the earliest: the heaviest tiles of every head start first, and with 8 KV
+//     heads the round-robin dispatch keeps all tiles of one head on one XCD (one L2).
+//   * Softmax: the running max is only raised when it grows by more than 8 (log2 units), so the
+//     O^T rescale is rare; probabilities then stay below 2^8, safe in float32 and bfloat16.
 #include "sx_device.h"
 #include "sx_internal.h"
 
@@ -36,7 +41,7 @@ struct AttnK {
   const int32_t* rows;
   const int32_t* n_rows;
   const int32_t* cu;
-  int Hq, Hkv, G, rpw;
+  int Hq, Hkv, G, rpw, n_req;
   float scale_log2;
   int lse_base2;
 };
@@ -55,16 +60,20 @@ __global__ __launch_bounds__(256, 2) void attn_mfma_kernel(AttnK a) {
   constexpr int KSTRIDE = D + 8;                 // padded K row (elements)
   constexpr int KVEC = KT * D / 8 / 256;         // 16-byte K vectors per loader thread
   constexpr int DV = D / 16;                     // V dims per loader thread (4 keys each)
-  __shared__ __attribute__((aligned(16))) uint16_t Ks[KT * KSTRIDE];
-  __shared__ __attribute__((aligned(16))) uint16_t Vs[PV ? KT * D : 8];
+  constexpr int KBUF = KT * KSTRIDE;
+  constexpr int VBUF = PV ? KT * D : 8;
+  __shared__ __attribute__((aligned(16))) uint16_t Ks[2 * KBUF];
+  __shared__ __attribute__((aligned(16))) uint16_t Vs[2 * VBUF];
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int w = tid >> 6;
   const int l32 = lane & 31;
   const int hg = lane >> 5;
-  const int kvh = blockIdx.y;
-  const int r = blockIdx.z;
+  const int kvh = (int)(blockIdx.x % (unsigned)a.Hkv);
+  const int rest = (int)(blockIdx.x / (unsigned)a.Hkv);
+  const int r = rest % a.n_req;
+  const int rank = rest / a.n_req;
 
   int T, tok_off, bt_off = 0, nrows;
   if constexpr (PAGED) {
@@ -80,8 +89,8 @@ __global__ __launch_bounds__(256, 2) void attn_mfma_kernel(AttnK a) {
   }
   const int rpw = a.rpw;
   const int ntiles = (nrows + rpw - 1) / rpw;
-  if ((int)blockIdx.x >= ntiles) return;
-  const int tile = ntiles - 1 - (int)blockIdx.x;
+  if (rank >= ntiles) return;
+  const int tile = ntiles - 1 - rank;
   const int row0 = tile * rpw;
   const int col = w * 32 + l32;
   const int lrow = col / a.G;
@@ -135,7 +144,8 @@ __global__ __launch_bounds__(256, 2) void attn_mfma_kernel(AttnK a) {
       const int key = vid / (D / 8);
       const int dc = vid - key * (D / 8);
       const int j = kbase + key;
-      kreg[e] = j < T ? *(const uint4*)(key_row(a.k, j) + dc * 8) : make_uint4(0, 0, 0, 0);
+      const uint4 t = *(const uint4*)(key_row(a.k, min(j, T - 1)) + dc * 8);   // clamped, branch-free
+      kreg[e] = j < T ? t : make_uint4(0, 0, 0, 0);
     }
     if constexpr (PV) {
       const int run = tid >> 4;
@@ -143,27 +153,29 @@ __global__ __launch_bounds__(256, 2) void attn_mfma_kernel(AttnK a) {
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         const int j = kbase + run * 4 + i;
+        const uint16_t* vp = key_row(a.v, min(j, T - 1));
         if constexpr (DV == 8) {
-          vreg[i] = j < T ? *(const uint4*)(key_row(a.v, j) + dc * 8) : make_uint4(0, 0, 0, 0);
+          const uint4 t = *(const uint4*)(vp + dc * 8);
+          vreg[i] = j < T ? t : make_uint4(0, 0, 0, 0);
         } else {
-          uint2 t2 = j < T ? *(const uint2*)(key_row(a.v, j) + dc * 4) : make_uint2(0, 0);
-          vreg[i] = make_uint4(t2.x, t2.y, 0, 0);
+          const uint2 t2 = *(const uint2*)(vp + dc * 4);
+          vreg[i] = j < T ? make_uint4(t2.x, t2.y, 0, 0) : make_uint4(0, 0, 0, 0);
         }
       }
     }
   };
-  auto lstore = [&]() {
+  auto lstore = [&](int buf) {
 #pragma unroll
     for (int e = 0; e < KVEC; ++e) {
       const int vid = tid + 256 * e;
       const int key = vid / (D / 8);
       const int dc = vid - key * (D / 8);
-      *(uint4*)(&Ks[key * KSTRIDE + dc * 8]) = kreg[e];
+      *(uint4*)(&Ks[buf * KBUF + key * KSTRIDE + dc * 8]) = kreg[e];
     }
     if constexpr (PV) {
       const int run = tid >> 4;
       const int dc = tid & 15;
-      uint16_t* dst = &Vs[(run * D + dc * DV) * 4];
+      uint16_t* dst = &Vs[buf * VBUF + (run * D + dc * DV) * 4];
 #pragma unroll
       for (int c = 0; c < DV; c += 2) {
         uint4 t;
@@ -177,85 +189,101 @@ __global__ __launch_bounds__(256, 2) void attn_mfma_kernel(AttnK a) {
   };
 
   gload(0);
+  lstore(0);
+  if (nkt > 1) gload(1);
+  __syncthreads();
+  const float c2 = a.scale_log2;
   for (int kt = 0; kt < nkt; ++kt) {
-    if (kt > 0) __syncthreads();
-    lstore();
-    __syncthreads();
-    if (kt + 1 < nkt) gload(kt + 1);
+    const int buf = kt & 1;
     const int kbase = kt * KT;
-    if (kbase > wave_max) continue;   // every column of this wave is before the tile
-
-    // S^T = K Q^T for the 64 keys of the tile: two 32-key M tiles
-    f32x16_t sacc[2];
+    if (kbase <= wave_max) {   // otherwise every column of this wave is before the tile
+      const uint16_t* Kb = Ks + buf * KBUF;
+      // S^T = K Q^T for the 64 keys of the tile: two 32-key M tiles
+      f32x16_t sacc[2];
 #pragma unroll
-    for (int mt = 0; mt < 2; ++mt) {
+      for (int mt = 0; mt < 2; ++mt) {
 #pragma unroll
-      for (int e = 0; e < 16; ++e) sacc[mt][e] = 0.f;
+        for (int e = 0; e < 16; ++e) sacc[mt][e] = 0.f;
 #pragma unroll
-      for (int s = 0; s < D / 16; ++s) {
-        const bf16x8_t ka = *(const bf16x8_t*)(&Ks[(mt * 32 + l32) * KSTRIDE + s * 16 + hg * 8]);
-        sacc[mt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka, qb[s], sacc[mt], 0, 0, 0);
-      }
-    }
-    // online softmax in the log2 domain; lane value e of M tile mt is key
-    // kbase + 32 mt + 8 (e / 4) + 4 hg + e % 4 of the lane's query column
-    float x[32];
-    float mx = -INFINITY;
-    const bool need_mask = kbase + KT - 1 > wave_min;
-#pragma unroll
-    for (int mt = 0; mt < 2; ++mt)
-#pragma unroll
-      for (int e = 0; e < 16; ++e) {
-        float v = sacc[mt][e] * a.scale_log2;
-        if (need_mask) {
-          const int key = kbase + mt * 32 + (e >> 2) * 8 + hg * 4 + (e & 3);
-          if (key > pos) v = -INFINITY;
+        for (int s = 0; s < D / 16; ++s) {
+          const bf16x8_t ka = *(const bf16x8_t*)(&Kb[(mt * 32 + l32) * KSTRIDE + s * 16 + hg * 8]);
+          sacc[mt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka, qb[s], sacc[mt], 0, 0, 0);
         }
-        x[mt * 16 + e] = v;
-        mx = fmaxf(mx, v);
       }
-    mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
-    const float m_new = fmaxf(m_run, mx);
-    const float m_use = m_new == -INFINITY ? 0.f : m_new;
-    const float alpha = __builtin_amdgcn_exp2f(m_run - m_use);
-    float psum = 0.f;
+      // lane value e of M tile mt is key kbase + 32 mt + 8 (e / 4) + 4 hg + e % 4 of the lane's column
+      float x[32];
 #pragma unroll
-    for (int i = 0; i < 32; ++i) {
-      x[i] = __builtin_amdgcn_exp2f(x[i] - m_use);
-      psum += x[i];
-    }
-    l_run = l_run * alpha + psum;
-    m_run = m_new;
-    if constexpr (PV) {
-      if (__builtin_expect(alpha != 1.f, 1)) {
+      for (int mt = 0; mt < 2; ++mt)
 #pragma unroll
-        for (int dt = 0; dt < D / 32; ++dt)
+        for (int e = 0; e < 16; ++e) x[mt * 16 + e] = sacc[mt][e];
+      if (kbase + KT - 1 > wave_min) {
+        const int lim = pos - kbase - hg * 4;   // mask keys with offset > lim
 #pragma unroll
-          for (int e = 0; e < 16; ++e) o[dt][e] *= alpha;
+        for (int i = 0; i < 32; ++i) {
+          const int koff = (i >> 4) * 32 + ((i & 15) >> 2) * 8 + (i & 3);
+          if (koff > lim) x[i] = -INFINITY;
+        }
       }
-      // P^T operand of k-step kk (16 keys) = lane values x[8kk .. 8kk+7]
-      bf16x8_t pb[4];
+      float mx = x[0];
 #pragma unroll
-      for (int kk = 0; kk < 4; ++kk) {
-        uint4 t;
-        t.x = pack_bf16x2(x[8 * kk + 0], x[8 * kk + 1]);
-        t.y = pack_bf16x2(x[8 * kk + 2], x[8 * kk + 3]);
-        t.z = pack_bf16x2(x[8 * kk + 4], x[8 * kk + 5]);
-        t.w = pack_bf16x2(x[8 * kk + 6], x[8 * kk + 7]);
-        pb[kk] = __builtin_bit_cast(bf16x8_t, t);
+      for (int i = 1; i < 32; ++i) mx = fmaxf(mx, x[i]);
+      mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+      const float m_tile = mx * c2;             // scaled, log2 domain (c2 > 0)
+      // raise the running max only when it grows by more than 8
+      const bool grow = m_tile > m_run + 8.f;
+      if (__ballot(grow)) {
+        const float m_new = grow ? m_tile : m_run;
+        const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);   // m_run = -inf -> 0
+        l_run *= alpha;
+        if constexpr (PV) {
+#pragma unroll
+          for (int dt = 0; dt < D / 32; ++dt)
+#pragma unroll
+            for (int e = 0; e < 16; ++e) o[dt][e] *= alpha;
+        }
+        m_run = m_new;
       }
+      const float m_use = m_run == -INFINITY ? 0.f : m_run;
+      float psum = 0.f;
 #pragma unroll
-      for (int dt = 0; dt < D / 32; ++dt) {
-        const int d = dt * 32 + l32;
+      for (int i = 0; i < 32; ++i) {
+        x[i] = __builtin_amdgcn_exp2f(__builtin_fmaf(x[i], c2, -m_use));
+        psum += x[i];
+      }
+      l_run += psum;
+      if constexpr (PV) {
+        const uint16_t* Vb = Vs + buf * VBUF;
+        // P^T operand of k-step kk (16 keys) = lane values x[8kk .. 8kk+7]
+        bf16x8_t pb[4];
 #pragma unroll
         for (int kk = 0; kk < 4; ++kk) {
-          const uint2 lo = *(const uint2*)(&Vs[((4 * kk + hg) * D + d) * 4]);
-          const uint2 hi = *(const uint2*)(&Vs[((4 * kk + 2 + hg) * D + d) * 4]);
-          const bf16x8_t va = __builtin_bit_cast(bf16x8_t, make_uint4(lo.x, lo.y, hi.x, hi.y));
-          o[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, pb[kk], o[dt], 0, 0, 0);
+          uint4 t;
+          t.x = pack_bf16x2(x[8 * kk + 0], x[8 * kk + 1]);
+          t.y = pack_bf16x2(x[8 * kk + 2], x[8 * kk + 3]);
+          t.z = pack_bf16x2(x[8 * kk + 4], x[8 * kk + 5]);
+          t.w = pack_bf16x2(x[8 * kk + 6], x[8 * kk + 7]);
+          pb[kk] = __builtin_bit_cast(bf16x8_t, t);
+        }
+#pragma unroll
+        for (int dt = 0; dt < D / 32; ++dt) {
+          const int d = dt * 32 + l32;
+#pragma unroll
+          for (int kk = 0; kk < 4; ++kk) {
+            const uint2 lo = *(const uint2*)(&Vb[((4 * kk + hg) * D + d) * 4]);
+            const uint2 hi = *(const uint2*)(&Vb[((4 * kk + 2 + hg) * D + d) * 4]);
+            const bf16x8_t va = __builtin_bit_cast(bf16x8_t, make_uint4(lo.x, lo.y, hi.x, hi.y));
+            o[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, pb[kk], o[dt], 0, 0, 0);
+          }
         }
       }
     }
+    // stage tile kt+1 (its loads were issued one iteration ago) and start loading tile kt+2;
+    // the buffer written here was last read in iteration kt-1, which every wave has left
+    if (kt + 1 < nkt) {
+      lstore(buf ^ 1);
+      if (kt + 2 < nkt) gload(kt + 2);
+    }
+    __syncthreads();
   }
 
   const float l_tot = l_run + __shfl_xor(l_run, 32, 64);
@@ -295,7 +323,7 @@ struct ColsumK {
   const int32_t* probe;
   double* colsum;
   int64_t total;
-  int Hq, Hkv, G;
+  int Hq, Hkv, G, n_req;
   float scale_log2;
 };
 
@@ -306,10 +334,12 @@ __global__ __launch_bounds__(256, 2) void colsum_mfma_kernel(ColsumK a) {
   const int w = tid >> 6;
   const int l32 = lane & 31;
   const int hg = lane >> 5;
-  const int kvh = blockIdx.y;
-  const ReqDev rq = a.reqs[blockIdx.z];
+  // 1-D grid: KV head fastest, then request, then key tile from the first keys (most probe rows)
+  const int kvh = (int)(blockIdx.x % (unsigned)a.Hkv);
+  const int rest = (int)(blockIdx.x / (unsigned)a.Hkv);
+  const ReqDev rq = a.reqs[rest % a.n_req];
   const int T = rq.T;
-  const int j0 = blockIdx.x * 128;
+  const int j0 = (rest / a.n_req) * 128;
   if (j0 >= T) return;
   const int jw = j0 + w * 32;
   // K rows of the wave's 32 keys as the A operand
@@ -414,7 +444,9 @@ hipError_t launch_mfma(const AttnLaunch& L, hipStream_t s) {
   a.rpw = COLS / a.G;
   a.scale_log2 = L.scale * 1.4426950408889634f;
   a.lse_base2 = L.lse_base2;
-  const dim3 grid((unsigned)((L.grid_rows + a.rpw - 1) / a.rpw), (unsigned)L.Hkv, (unsigned)L.n_req);
+  a.n_req = L.n_req;
+  const int64_t ntiles = (L.grid_rows + a.rpw - 1) / a.rpw;
+  const dim3 grid((unsigned)(ntiles * L.Hkv * L.n_req));
   hipLaunchKernelGGL((attn_mfma_kernel<D, PAGED, PV>), grid, dim3(256), 0, s, a);
   return hipGetLastError();
 }
@@ -453,7 +485,8 @@ hipError_t launch_colsum(const sx_plan* p, const void* q, const void* kc, hipStr
   a.Hkv = p->desc.n_kv_heads;
   a.G = a.Hq / a.Hkv;
   a.scale_log2 = p->scale * 1.4426950408889634f;
-  const dim3 grid((unsigned)((p->max_T + 127) / 128), (unsigned)a.Hkv, (unsigned)p->n_req);
+  a.n_req = p->n_req;
+  const dim3 grid((unsigned)(((p->max_T + 127) / 128) * a.Hkv * p->n_req));
   if (p->desc.head_dim == 128)
     hipLaunchKernelGGL(colsum_mfma_kernel<128>, grid, dim3(256), 0, s, a);
   else
