@@ -46,24 +46,29 @@ struct AttnK {
   int lse_base2;
 };
 
-__device__ __forceinline__ uint32_t lo16(uint32_t w) { return w & 0xffffu; }
-__device__ __forceinline__ uint32_t hi16(uint32_t w) { return w >> 16; }
+typedef short shortx4_t __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) shortx4_t lds_shortx4_t;
 
-// Element c (0..7) of a 16-byte bf16 vector.
-__device__ __forceinline__ uint32_t elem8(const uint4& v, int c) {
-  const uint32_t w = c < 2 ? v.x : c < 4 ? v.y : c < 6 ? v.z : v.w;
-  return (c & 1) ? hi16(w) : lo16(w);
-}
+// s_waitcnt with vmcnt <= n (n < 16), expcnt and lgkmcnt left unconstrained (gfx9 encoding).
+#define SX_WAIT_VMCNT(n) __builtin_amdgcn_s_waitcnt(((n) & 0xF) | (0x7 << 4) | (0xF << 8))
 
 template <int D, bool PAGED, bool PV>
 __global__ __launch_bounds__(256, 2) void attn_mfma_kernel(AttnK a) {
-  constexpr int KSTRIDE = D + 8;                 // padded K row (elements)
-  constexpr int KVEC = KT * D / 8 / 256;         // 16-byte K vectors per loader thread
-  constexpr int DV = D / 16;                     // V dims per loader thread (4 keys each)
-  constexpr int KBUF = KT * KSTRIDE;
-  constexpr int VBUF = PV ? KT * D : 8;
-  __shared__ __attribute__((aligned(16))) uint16_t Ks[2 * KBUF];
-  __shared__ __attribute__((aligned(16))) uint16_t Vs[2 * VBUF];
+  constexpr int ROWB = D * 2;                 // bytes of one key row
+  constexpr int NCH = ROWB / 16;              // 16-byte chunks per row
+  constexpr int TILEB = KT * ROWB;            // bytes of one K (or V) tile
+  constexpr int RPK = 1024 / ROWB;            // rows per 1 KB direct-load instruction
+  constexpr int IPW = TILEB / 1024 / 4;       // direct-load instructions per wave per matrix
+  constexpr int NMAT = PV ? 2 : 1;
+  // LDS: two buffers of K and V tiles, rows row-major; chunk c of row r of K sits at chunk
+  // c ^ (r mod NCH) (conflict-free 16-byte row reads), of V at c ^ 2 (r mod NCH/2)
+  // (32-byte pairs kept together: conflict-free transposed 8-byte reads).  Each buffer is its
+  // own array so the compiler can tell the in-flight loads into one buffer from the reads of
+  // the other (no false waits).
+  __shared__ __attribute__((aligned(1024))) char K0[TILEB];
+  __shared__ __attribute__((aligned(1024))) char K1[TILEB];
+  __shared__ __attribute__((aligned(1024))) char V0[PV ? TILEB : 16];
+  __shared__ __attribute__((aligned(1024))) char V1[PV ? TILEB : 16];
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -116,6 +121,9 @@ __global__ __launch_bounds__(256, 2) void attn_mfma_kernel(AttnK a) {
       qb[s] = __builtin_bit_cast(bf16x8_t, v);
     }
   }
+  // Q must be complete before any tile transfer is issued: the compiler does not see those
+  // transfers, so a later wait of its own for Q would also wait for them.
+  SX_WAIT_VMCNT(0);
 
   f32x16_t o[PV ? D / 32 : 1];
 #pragma unroll
@@ -125,89 +133,91 @@ __global__ __launch_bounds__(256, 2) void attn_mfma_kernel(AttnK a) {
   float m_run = -INFINITY;
   float l_run = 0.f;
 
-  // ---- tile loaders ----
-  uint4 kreg[KVEC];
-  uint4 vreg[4];      // 4 keys x DV dims (DV*2 bytes each, low part used when DV == 4)
-  auto key_row = [&](const uint16_t* base, int key) -> const uint16_t* {
+  // ---- direct global -> LDS tile loads.  Instruction q (1 KB) of a tile holds rows
+  // RPK*q .. RPK*q + RPK - 1, all inside one 16-key block; keys past the end read row T-1 (they
+  // are masked: every query row is < T). ----
+  const int last_key = T - 1;
+  const int lrow_in = lane / NCH;     // row of this lane inside its 1 KB chunk
+  const int pchunk = lane % NCH;      // physical chunk this lane fills
+  const int wu = __builtin_amdgcn_readfirstlane(w);
+  // base of (block, head) for the wave's 16-key block, and for the block holding key T-1
+  auto block_base = [&](const uint16_t* base, int key16) -> const uint16_t* {
     if constexpr (PAGED) {
-      const int32_t blk = a.bt[bt_off + (key >> 4)];
-      return base + (((int64_t)blk * a.Hkv + kvh) * 16 + (key & 15)) * D;
+      // the block table is read-only here: read it through the constant address space (scalar loads)
+      const __attribute__((address_space(4))) int32_t* btc = (const __attribute__((address_space(4))) int32_t*)a.bt;
+      const int32_t blk = btc[__builtin_amdgcn_readfirstlane(bt_off + key16)];
+      return base + (((int64_t)blk * a.Hkv + kvh) * 16) * D;
     } else {
-      return base + ((int64_t)(tok_off + key) * a.Hkv + kvh) * D;
+      return base + ((int64_t)(tok_off + key16 * 16) * a.Hkv + kvh) * D;
     }
   };
-  auto gload = [&](int kt) {
+  constexpr int64_t kRowPaged = D;
+  const int64_t rstride = PAGED ? kRowPaged : (int64_t)a.Hkv * D;   // elements between rows of a block
+  const uint16_t* k_last = block_base(a.k, last_key >> 4) + (last_key & 15) * rstride;
+  const uint16_t* v_last = PV ? block_base(a.v, last_key >> 4) + (last_key & 15) * rstride : nullptr;
+  // One 16-byte global -> LDS transfer per lane; the destination (M0) is wave-uniform and lane l
+  // lands at dst + 16 l.  Issued as inline assembly so the compiler does not order every later
+  // LDS read behind it: the wait for these transfers is explicit (vmcnt(0) + barrier before a
+  // tile is read).  The statement is volatile, so it stays between the barriers around it; it
+  // declares no memory clobber, which keeps the read-only index loads on the scalar unit.
+  auto dma16 = [&](const void* src, const char* dst) {
+    const uint32_t m0 = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) const char*)dst;
+    asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(src), "s"(m0) : "m0");
+  };
+  auto issue = [&](int kt, char* Kd, char* Vd) {
     const int kbase = kt * KT;
 #pragma unroll
-    for (int e = 0; e < KVEC; ++e) {
-      const int vid = tid + 256 * e;
-      const int key = vid / (D / 8);
-      const int dc = vid - key * (D / 8);
-      const int j = kbase + key;
-      const uint4 t = *(const uint4*)(key_row(a.k, min(j, T - 1)) + dc * 8);   // clamped, branch-free
-      kreg[e] = j < T ? t : make_uint4(0, 0, 0, 0);
-    }
-    if constexpr (PV) {
-      const int run = tid >> 4;
-      const int dc = tid & 15;
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int j = kbase + run * 4 + i;
-        const uint16_t* vp = key_row(a.v, min(j, T - 1));
-        if constexpr (DV == 8) {
-          const uint4 t = *(const uint4*)(vp + dc * 8);
-          vreg[i] = j < T ? t : make_uint4(0, 0, 0, 0);
-        } else {
-          const uint2 t2 = *(const uint2*)(vp + dc * 4);
-          vreg[i] = j < T ? make_uint4(t2.x, t2.y, 0, 0) : make_uint4(0, 0, 0, 0);
-        }
-      }
-    }
-  };
-  auto lstore = [&](int buf) {
-#pragma unroll
-    for (int e = 0; e < KVEC; ++e) {
-      const int vid = tid + 256 * e;
-      const int key = vid / (D / 8);
-      const int dc = vid - key * (D / 8);
-      *(uint4*)(&Ks[buf * KBUF + key * KSTRIDE + dc * 8]) = kreg[e];
-    }
-    if constexpr (PV) {
-      const int run = tid >> 4;
-      const int dc = tid & 15;
-      uint16_t* dst = &Vs[buf * VBUF + (run * D + dc * DV) * 4];
-#pragma unroll
-      for (int c = 0; c < DV; c += 2) {
-        uint4 t;
-        t.x = elem8(vreg[0], c) | (elem8(vreg[1], c) << 16);
-        t.y = elem8(vreg[2], c) | (elem8(vreg[3], c) << 16);
-        t.z = elem8(vreg[0], c + 1) | (elem8(vreg[1], c + 1) << 16);
-        t.w = elem8(vreg[2], c + 1) | (elem8(vreg[3], c + 1) << 16);
-        *(uint4*)(dst + c * 4) = t;
+    for (int i = 0; i < IPW; ++i) {
+      const int q = wu * IPW + i;                 // wave-uniform
+      const int rr = q * RPK + lrow_in;
+      const int key = kbase + rr;
+      const bool past = key > last_key;
+      const int kb16 = __builtin_amdgcn_readfirstlane(min((kbase + q * RPK) >> 4, last_key >> 4));  // uniform
+      const int ck = pchunk ^ (rr & (NCH - 1));
+      // block bases are loaded unconditionally (wave-uniform, scalar loads); the clamp of keys
+      // past the end is a per-lane select
+      const uint16_t* kblk = block_base(a.k, kb16);
+      const uint16_t* vblk = PV ? block_base(a.v, kb16) : nullptr;
+      const int64_t roff = (int64_t)(key & 15) * rstride;
+      const uint16_t* krow = past ? k_last : kblk + roff;
+      dma16(krow + ck * 8, Kd + q * 1024);
+      if constexpr (PV) {
+        const int cv = pchunk ^ (2 * (rr & (NCH / 2 - 1)));
+        const uint16_t* vrow = past ? v_last : vblk + roff;
+        dma16(vrow + cv * 8, Vd + q * 1024);
       }
     }
   };
 
-  gload(0);
-  lstore(0);
-  if (nkt > 1) gload(1);
+  issue(0, K0, V0);
+  if (nkt > 1) {
+    issue(1, K1, V1);
+    SX_WAIT_VMCNT(IPW * NMAT);   // tile 0 landed (tile 1 may still be in flight)
+  } else {
+    SX_WAIT_VMCNT(0);
+  }
   __syncthreads();
   const float c2 = a.scale_log2;
-  for (int kt = 0; kt < nkt; ++kt) {
-    const int buf = kt & 1;
+  // V^T operand addressing (transposed 8-byte reads): lane 4k + c of each 16-lane group points
+  // at row k, dims 4c .. 4c+3 of its 16-dim slice; the group's lane j receives dim j of 4 rows.
+  const int tg = lane >> 4;           // 16-lane group
+  const int tk = (lane & 15) >> 2;    // row inside the group's 4 rows
+  const int tc = lane & 3;            // 4-dim piece
+  // one tile: compute from (Kb, Vb), then (after the barrier) refill them with tile kt + 2
+  auto step = [&](int kt, char* Kb, char* Vb) {
     const int kbase = kt * KT;
     if (kbase <= wave_max) {   // otherwise every column of this wave is before the tile
-      const uint16_t* Kb = Ks + buf * KBUF;
       // S^T = K Q^T for the 64 keys of the tile: two 32-key M tiles
       f32x16_t sacc[2];
+      const f32x16_t zero16 = {};
 #pragma unroll
       for (int mt = 0; mt < 2; ++mt) {
-#pragma unroll
-        for (int e = 0; e < 16; ++e) sacc[mt][e] = 0.f;
+        const int rr = mt * 32 + l32;
 #pragma unroll
         for (int s = 0; s < D / 16; ++s) {
-          const bf16x8_t ka = *(const bf16x8_t*)(&Kb[(mt * 32 + l32) * KSTRIDE + s * 16 + hg * 8]);
-          sacc[mt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka, qb[s], sacc[mt], 0, 0, 0);
+          const int c = 2 * s + hg;
+          const bf16x8_t ka = *(const bf16x8_t*)(Kb + rr * ROWB + ((c ^ (rr & (NCH - 1))) << 4));
+          sacc[mt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka, qb[s], s == 0 ? zero16 : sacc[mt], 0, 0, 0);
         }
       }
       // lane value e of M tile mt is key kbase + 32 mt + 8 (e / 4) + 4 hg + e % 4 of the lane's column
@@ -252,7 +262,6 @@ __global__ __launch_bounds__(256, 2) void attn_mfma_kernel(AttnK a) {
       }
       l_run += psum;
       if constexpr (PV) {
-        const uint16_t* Vb = Vs + buf * VBUF;
         // P^T operand of k-step kk (16 keys) = lane values x[8kk .. 8kk+7]
         bf16x8_t pb[4];
 #pragma unroll
@@ -266,24 +275,36 @@ __global__ __launch_bounds__(256, 2) void attn_mfma_kernel(AttnK a) {
         }
 #pragma unroll
         for (int dt = 0; dt < D / 32; ++dt) {
-          const int d = dt * 32 + l32;
+          // dims 32 dt + 16 (tg & 1) + 4 tc .. +3 -> 16-byte chunk, 8-byte half
+          const int dchunk = 4 * dt + 2 * (tg & 1) + (tc >> 1);
+          const int dhalf = (tc & 1) * 8;
 #pragma unroll
           for (int kk = 0; kk < 4; ++kk) {
-            const uint2 lo = *(const uint2*)(&Vb[((4 * kk + hg) * D + d) * 4]);
-            const uint2 hi = *(const uint2*)(&Vb[((4 * kk + 2 + hg) * D + d) * 4]);
-            const bf16x8_t va = __builtin_bit_cast(bf16x8_t, make_uint4(lo.x, lo.y, hi.x, hi.y));
+            shortx4_t h2[2];
+#pragma unroll
+            for (int h = 0; h < 2; ++h) {
+              // slots 8 hg + 4h + k <-> key 16 kk + 8 h + 4 hg + k (the P^T operand order)
+              const int rr = 16 * kk + 8 * h + 4 * (tg >> 1) + tk;
+              const int off = rr * ROWB + ((dchunk ^ (2 * (rr & (NCH / 2 - 1)))) << 4) + dhalf;
+              h2[h] = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_shortx4_t*)(Vb + off));
+            }
+            const bf16x8_t va = __builtin_bit_cast(
+                bf16x8_t, make_uint4(__builtin_bit_cast(uint2, h2[0]).x, __builtin_bit_cast(uint2, h2[0]).y,
+                                     __builtin_bit_cast(uint2, h2[1]).x, __builtin_bit_cast(uint2, h2[1]).y));
             o[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, pb[kk], o[dt], 0, 0, 0);
           }
         }
       }
     }
-    // stage tile kt+1 (its loads were issued one iteration ago) and start loading tile kt+2;
-    // the buffer written here was last read in iteration kt-1, which every wave has left
     if (kt + 1 < nkt) {
-      lstore(buf ^ 1);
-      if (kt + 2 < nkt) gload(kt + 2);
+      SX_WAIT_VMCNT(0);          // this wave's part of tile kt+1 has landed
+      __syncthreads();           // tile kt+1 visible to all; every wave is done with (Kb, Vb)
+      if (kt + 2 < nkt) issue(kt + 2, Kb, Vb);
     }
-    __syncthreads();
+  };
+  for (int kt = 0; kt < nkt; kt += 2) {
+    step(kt, K0, V0);
+    if (kt + 1 < nkt) step(kt + 1, K1, V1);
   }
 
   const float l_tot = l_run + __shfl_xor(l_run, 32, 64);
