@@ -47,6 +47,8 @@ def parse():
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--layers", type=int, default=None, help="override the number of layers (profiling)")
+    ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
+                    help="also run a plain device copy of BYTES bytes (reference for HBM byte counters)")
     return ap.parse_args()
 
 
@@ -152,6 +154,14 @@ def main():
             tm.run("sx_sparse_attn", lambda: sx.sparse_attn(plan, tl["q"], rows, n_rows, max_rows, tl["kc"], tl["vc"],
                                                             out))
 
+    if args.copy_calibration:
+        src = torch.empty(args.copy_calibration // 2, dtype=torch.bfloat16, device="cuda").fill_(1.0)
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        log(f"copy calibration: {src.numel() * 2} bytes read, {dst.numel() * 2} bytes written")
+        del src, dst
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()

@@ -47,6 +47,14 @@ struct AttnK {
 };
 
 typedef short shortx4_t __attribute__((ext_vector_type(4)));
+
+// XOR applied to the 16-byte chunk index of row r of a V tile.  Each transposed read touches 4
+// consecutive rows; this spreads their 32-byte (per 16 lanes) and 64-byte (per 32 lanes) pieces over
+// distinct banks for both 128- and 256-byte-per-clock LDS service.  D = 64 rows have 8 chunks.
+template <int NCH>
+__device__ __forceinline__ int v_swz(int r) {
+  return NCH >= 16 ? ((0xCA60 >> ((r & 3) * 4)) & 15) : ((0x4260 >> ((r & 3) * 4)) & 7);
+}
 typedef __attribute__((address_space(3))) shortx4_t lds_shortx4_t;
 
 // s_waitcnt with vmcnt <= n (n < 16), expcnt and lgkmcnt left unconstrained (gfx9 encoding).
@@ -61,8 +69,8 @@ __global__ __launch_bounds__(256, 2) void attn_mfma_kernel(AttnK a) {
   constexpr int IPW = TILEB / 1024 / 4;       // direct-load instructions per wave per matrix
   constexpr int NMAT = PV ? 2 : 1;
   // LDS: two buffers of K and V tiles, rows row-major; chunk c of row r of K sits at chunk
-  // c ^ (r mod NCH) (conflict-free 16-byte row reads), of V at c ^ 2 (r mod NCH/2)
-  // (32-byte pairs kept together: conflict-free transposed 8-byte reads).  Each buffer is its
+  // c ^ (r mod NCH) (conflict-free 16-byte row reads), of V at c ^ v_swz(r) (conflict-free
+  // transposed 8-byte reads).  Each buffer is its
   // own array so the compiler can tell the in-flight loads into one buffer from the reads of
   // the other (no false waits).
   __shared__ __attribute__((aligned(1024))) char K0[TILEB];
@@ -182,7 +190,7 @@ __global__ __launch_bounds__(256, 2) void attn_mfma_kernel(AttnK a) {
       const uint16_t* krow = past ? k_last : kblk + roff;
       dma16(krow + ck * 8, Kd + q * 1024);
       if constexpr (PV) {
-        const int cv = pchunk ^ (2 * (rr & (NCH / 2 - 1)));
+        const int cv = pchunk ^ v_swz<NCH>(rr);
         const uint16_t* vrow = past ? v_last : vblk + roff;
         dma16(vrow + cv * 8, Vd + q * 1024);
       }
@@ -285,7 +293,7 @@ __global__ __launch_bounds__(256, 2) void attn_mfma_kernel(AttnK a) {
             for (int h = 0; h < 2; ++h) {
               // slots 8 hg + 4h + k <-> key 16 kk + 8 h + 4 hg + k (the P^T operand order)
               const int rr = 16 * kk + 8 * h + 4 * (tg >> 1) + tk;
-              const int off = rr * ROWB + ((dchunk ^ (2 * (rr & (NCH / 2 - 1)))) << 4) + dhalf;
+              const int off = rr * ROWB + ((dchunk ^ v_swz<NCH>(rr)) << 4) + dhalf;
               h2[h] = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_shortx4_t*)(Vb + off));
             }
             const bf16x8_t va = __builtin_bit_cast(
