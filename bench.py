@@ -49,7 +49,71 @@ def parse():
     ap.add_argument("--layers", type=int, default=None, help="override the number of layers (profiling)")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
                     help="also run a plain device copy of BYTES bytes (reference for HBM byte counters)")
+    ap.add_argument("--record-traffic", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
+                    help="turn two rocprofv3 --pmc counter CSVs (FETCH_SIZE, WRITE_SIZE) of a run with "
+                         "--copy-calibration into profiles/traffic_<workload>.json, then exit")
     return ap.parse_args()
+
+
+# kernel symbol -> (entry point, source file holding it)
+KERNELS = {
+    "attn_mfma_kernel<128, true, true>": ("sx_sparse_attn", "k_attn.hip"),
+    "attn_mfma_kernel<128, false, true>": ("sx_full_attn", "k_attn.hip"),
+    "attn_mfma_kernel<128, true, false>": ("sx_sparseq_score", "k_attn.hip"),
+    "colsum_mfma_kernel<128>": ("sx_sparseq_score", "k_attn.hip"),
+    "head_reduce_kernel": ("sx_sparseq_score", "k_copy.hip"),
+    "realign_kernel": ("sx_rope_realign", "k_copy.hip"),
+    "scatter_kernel": ("sx_kv_scatter", "k_copy.hip"),
+    "topk_kernel": ("sx_topk_select", "k_topk.hip"),
+}
+
+
+def source_hash(fname):
+    import hashlib
+    path = os.path.join(ROOT, "paper_2606_01751_amd", "csrc", fname)
+    return hashlib.sha256(open(path, "rb").read()).hexdigest()[:16]
+
+
+def record_traffic(fetch_csv, write_csv, workload):
+    """HBM bytes per dispatch of each kernel from FETCH_SIZE / WRITE_SIZE (KiB per dispatch),
+    scaled by the ratio of the true bytes of the largest plain device copy in the same run to
+    what the counters report for it."""
+    import csv
+    import re
+
+    def per_kernel(path, counter):
+        acc, copy = {}, []
+        for r in csv.DictReader(open(path)):
+            if r["Counter_Name"] != counter:
+                continue
+            v = float(r["Counter_Value"])
+            if "copyBuffer" in r["Kernel_Name"]:
+                copy.append((int(r["Grid_Size"]), v))
+            for sym in KERNELS:
+                if sym.replace(" ", "") in re.sub(r"\s", "", r["Kernel_Name"]):
+                    acc.setdefault(sym, []).append(v)
+        return acc, max(copy)[1] if copy else None
+
+    fetch, cf = per_kernel(fetch_csv, "FETCH_SIZE")
+    write, cw = per_kernel(write_csv, "WRITE_SIZE")
+    return fetch, write, cf, cw
+
+
+def load_traffic(workload):
+    path = os.path.join(ROOT, "profiles", f"traffic_{workload}.json")
+    if not os.path.exists(path):
+        return {}
+    d = json.load(open(path))
+    out, stale = {}, set()
+    for sym, e in d.get("kernels", {}).items():
+        if sym not in KERNELS:
+            continue
+        entry = KERNELS[sym][0]
+        if e.get("source_sha256") != source_hash(KERNELS[sym][1]):
+            stale.add(entry)       # the kernel changed since its counters were taken
+            continue
+        out[entry] = out.get(entry, 0.0) + e["bytes_per_dispatch"]
+    return {k: v for k, v in out.items() if k not in stale}
 
 
 class Timers:
@@ -85,6 +149,25 @@ def main():
         print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported (the step is not sharded).",
               file=sys.stderr)
         sys.exit(2)
+    if args.record_traffic:
+        import workloads as W
+        w = W.config(args.config, seed=args.seed)
+        fetch, write, cf, cw = record_traffic(*args.record_traffic, w.name)
+        nbytes = args.copy_calibration
+        assert nbytes and cf and cw, "need --copy-calibration BYTES and a copy in both counter runs"
+        kf, kw = nbytes / 1024.0 / cf, nbytes / 1024.0 / cw
+        rec = {"workload": w.name, "copy_bytes": nbytes, "copy_fetch_kib": cf, "copy_write_kib": cw,
+               "fetch_factor": kf, "write_factor": kw, "kernels": {}}
+        for sym in sorted(set(fetch) | set(write)):
+            f = float(np.mean(fetch.get(sym, [0.0])))
+            wr = float(np.mean(write.get(sym, [0.0])))
+            rec["kernels"][sym] = {"entry_point": KERNELS[sym][0], "source_sha256": source_hash(KERNELS[sym][1]),
+                                   "fetch_kib": f, "write_kib": wr,
+                                   "bytes_per_dispatch": (f * kf + wr * kw) * 1024.0}
+        out = os.path.join(ROOT, "profiles", f"traffic_{w.name}.json")
+        json.dump(rec, open(out, "w"), indent=1)
+        print(json.dumps(rec, indent=1))
+        return
     import torch
 
     import paper_2606_01751_amd as sx
@@ -221,12 +304,18 @@ def main():
     dom = max(kern, key=lambda n: kern[n]["total_ms"])
     kind, amount = work[dom]
     sec = kern[dom]["avg_ms"] / 1e3
+    traffic = load_traffic(w.name)
+    for name, e in kernels.items():
+        if name in traffic:
+            e["hbm_bytes_per_launch"] = round(traffic[name])
     if kind == "hbm":
         roof = {"kernel": dom, "bound": "hbm", "achieved": round(amount / sec / 1e9, 1), "peak": PEAK_HBM_GBS,
-                "unit": "GB/s", "frac": round(amount / sec / 1e9 / PEAK_HBM_GBS, 4), "traffic": None}
+                "unit": "GB/s", "frac": round(amount / sec / 1e9 / PEAK_HBM_GBS, 4),
+                "traffic": round(traffic[dom]) if dom in traffic else None, "algorithmic_per_launch": amount}
     else:
         roof = {"kernel": dom, "bound": "mfma", "achieved": round(amount / sec / 1e12, 2), "peak": peak,
-                "unit": "TFLOP/s", "frac": round(amount / sec / 1e12 / peak, 4), "traffic": None,
+                "unit": "TFLOP/s", "frac": round(amount / sec / 1e12 / peak, 4),
+                "traffic": round(traffic[dom]) if dom in traffic else None, "traffic_unit": "HBM bytes per launch",
                 "algorithmic_per_launch": amount}
 
     value = T * L / (ms_per_step / 1e3)
