@@ -21,6 +21,8 @@
 //     heads the round-robin dispatch keeps all tiles of one head on one XCD (one L2).
 //   * Softmax: the running max is only raised when it grows by more than 8 (log2 units), so the
 //     O^T rescale is rare; probabilities then stay below 2^8, safe in float32 and bfloat16.
+#include <type_traits>
+
 #include "sx_device.h"
 #include "sx_internal.h"
 
@@ -172,8 +174,33 @@ __global__ __launch_bounds__(256, 2) void attn_mfma_kernel(AttnK a) {
     const uint32_t m0 = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) const char*)dst;
     asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(src), "s"(m0) : "m0");
   };
+  // Per-lane byte offsets of the transfers inside a (block, head) run of 16 rows.  Tiles start at
+  // multiples of 64 keys, so these are the same for every tile.
+  uint32_t koff[IPW], voff[IPW];
+#pragma unroll
+  for (int i = 0; i < IPW; ++i) {
+    const int rr = (wu * IPW + i) * RPK + lrow_in;
+    koff[i] = (uint32_t)(((rr & 15) * rstride + (pchunk ^ (rr & (NCH - 1))) * 8) * 2);
+    voff[i] = (uint32_t)(((rr & 15) * rstride + (pchunk ^ v_swz<NCH>(rr)) * 8) * 2);
+  }
+  // global (SGPR base + VGPR byte offset) -> LDS transfer of 16 bytes per lane
+  auto dma16_sb = [&](const uint16_t* sbase, uint32_t voffset, const char* dst) {
+    const uint32_t m0 = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) const char*)dst;
+    asm volatile("s_mov_b32 m0, %2\n\tglobal_load_lds_dwordx4 %0, %1" ::"v"(voffset), "s"(sbase), "s"(m0) : "m0");
+  };
   auto issue = [&](int kt, char* Kd, char* Vd) {
     const int kbase = kt * KT;
+    if (kbase + KT - 1 <= last_key) {
+      // whole tile inside the request: wave-uniform block base + precomputed lane offset
+#pragma unroll
+      for (int i = 0; i < IPW; ++i) {
+        const int q = wu * IPW + i;
+        const int kb16 = __builtin_amdgcn_readfirstlane((kbase + q * RPK) >> 4);
+        dma16_sb(block_base(a.k, kb16), koff[i], Kd + q * 1024);
+        if constexpr (PV) dma16_sb(block_base(a.v, kb16), voff[i], Vd + q * 1024);
+      }
+      return;
+    }
 #pragma unroll
     for (int i = 0; i < IPW; ++i) {
       const int q = wu * IPW + i;                 // wave-uniform
@@ -212,97 +239,143 @@ __global__ __launch_bounds__(256, 2) void attn_mfma_kernel(AttnK a) {
   const int tk = (lane & 15) >> 2;    // row inside the group's 4 rows
   const int tc = lane & 3;            // 4-dim piece
   // one tile: compute from (Kb, Vb), then (after the barrier) refill them with tile kt + 2
+  // ---- one tile in two 32-key halves, so that each half's softmax (vector ALU) has independent
+  // matrix work beside it: S of half 1 runs beside the softmax of half 0, and P.V of half 0 beside
+  // the softmax of half 1. ----
+  // S^T of half mt: keys kbase + 32 mt .. + 31
+  auto s_half = [&](const char* Kb, int mt) -> f32x16_t {
+    f32x16_t acc;
+    const f32x16_t zero16 = {};
+    const int rr = mt * 32 + l32;
+#pragma unroll
+    for (int s = 0; s < D / 16; ++s) {
+      const int c = 2 * s + hg;
+      const bf16x8_t ka = *(const bf16x8_t*)(Kb + rr * ROWB + ((c ^ (rr & (NCH - 1))) << 4));
+      acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka, qb[s], s == 0 ? zero16 : acc, 0, 0, 0);
+    }
+    return acc;
+  };
+  // Online softmax of one half (lane value e = key k0 + 8 (e / 4) + 4 hg + e % 4 of the lane's
+  // column).  The running max is raised only when it grows by more than 8 (log2 units); alpha is
+  // the factor for what was accumulated before (1 when not raised).  Returns the P^T operands of
+  // the half's two 16-key k-steps.
+  struct HalfP {
+    bf16x8_t pb[2];
+    float alpha;
+    bool rescale;   // wave-uniform: some lane raised its max
+  };
+  auto softmax_half = [&](f32x16_t sv, int k0, auto masked) -> HalfP {
+    float x[16];
+#pragma unroll
+    for (int e = 0; e < 16; ++e) x[e] = sv[e];
+    if constexpr (decltype(masked)::value) {
+      const int lim = pos - k0 - hg * 4;   // mask keys with offset > lim
+#pragma unroll
+      for (int e = 0; e < 16; ++e)
+        if ((e >> 2) * 8 + (e & 3) > lim) x[e] = -INFINITY;
+    }
+    float mx = x[0];
+#pragma unroll
+    for (int e = 1; e < 16; ++e) mx = fmaxf(mx, x[e]);
+    mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+    const float m_tile = mx * c2;             // scaled, log2 domain (c2 > 0)
+    const bool grow = m_tile > m_run + 8.f;
+    const float m_new = grow ? m_tile : m_run;
+    HalfP r;
+    r.alpha = __builtin_amdgcn_exp2f(m_run - m_new);   // 1 when kept; m_run = -inf -> 0
+    r.rescale = __ballot(grow) != 0;
+    m_run = m_new;
+    const float m_use = m_run == -INFINITY ? 0.f : m_run;
+    float psum = 0.f;
+#pragma unroll
+    for (int e = 0; e < 16; ++e) {
+      x[e] = __builtin_amdgcn_exp2f(__builtin_fmaf(x[e], c2, -m_use));
+      psum += x[e];
+    }
+    l_run = l_run * r.alpha + psum;
+#pragma unroll
+    for (int kk = 0; kk < 2; ++kk) {
+      uint4 t;
+      t.x = pack_bf16x2(x[8 * kk + 0], x[8 * kk + 1]);
+      t.y = pack_bf16x2(x[8 * kk + 2], x[8 * kk + 3]);
+      t.z = pack_bf16x2(x[8 * kk + 4], x[8 * kk + 5]);
+      t.w = pack_bf16x2(x[8 * kk + 6], x[8 * kk + 7]);
+      r.pb[kk] = __builtin_bit_cast(bf16x8_t, t);
+    }
+    return r;
+  };
+  auto rescale_o = [&](float alpha) {
+    if constexpr (PV) {
+#pragma unroll
+      for (int dt = 0; dt < D / 32; ++dt)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) o[dt][e] *= alpha;
+    }
+  };
+  // O^T += V^T P^T for the keys of half mt (k-steps 2 mt, 2 mt + 1)
+  auto pv_half = [&](const char* Vb, int mt, const HalfP& P) {
+    if constexpr (PV) {
+#pragma unroll
+      for (int dt = 0; dt < D / 32; ++dt) {
+        // dims 32 dt + 16 (tg & 1) + 4 tc .. +3 -> 16-byte chunk, 8-byte half
+        const int dchunk = 4 * dt + 2 * (tg & 1) + (tc >> 1);
+        const int dhalf = (tc & 1) * 8;
+#pragma unroll
+        for (int j = 0; j < 2; ++j) {
+          const int kk = 2 * mt + j;
+          shortx4_t h2[2];
+#pragma unroll
+          for (int h = 0; h < 2; ++h) {
+            // slots 8 hg + 4h + k <-> key 16 kk + 8 h + 4 hg + k (the P^T operand order)
+            const int rr = 16 * kk + 8 * h + 4 * (tg >> 1) + tk;
+            const int off = rr * ROWB + ((dchunk ^ v_swz<NCH>(rr)) << 4) + dhalf;
+            h2[h] = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_shortx4_t*)(Vb + off));
+          }
+          const bf16x8_t va = __builtin_bit_cast(
+              bf16x8_t, make_uint4(__builtin_bit_cast(uint2, h2[0]).x, __builtin_bit_cast(uint2, h2[0]).y,
+                                   __builtin_bit_cast(uint2, h2[1]).x, __builtin_bit_cast(uint2, h2[1]).y));
+          o[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, P.pb[j], o[dt], 0, 0, 0);
+        }
+      }
+    }
+  };
+  // Scheduling hints (instruction classes: 0x2 VALU, 0x8 MFMA, 0x100 LDS read): ask for the matrix
+  // instructions of one half to be spread through the vector-ALU softmax of the other.
+#define SX_SG(mask, n) __builtin_amdgcn_sched_group_barrier(mask, n, 0)
+  auto key_tile = [&](const char* Kb, const char* Vb, int kbase, auto masked) {
+    const f32x16_t s0 = s_half(Kb, 0);
+    const f32x16_t s1 = s_half(Kb, 1);
+    const HalfP p0 = softmax_half(s0, kbase, masked);
+    // K reads, S of half 0, then S of half 1 beside softmax 0
+    SX_SG(0x100, 16);
+    SX_SG(0x008, 8);
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      SX_SG(0x008, 1);
+      SX_SG(0x002, 10);
+    }
+    if (p0.rescale) rescale_o(p0.alpha);
+    pv_half(Vb, 0, p0);
+    const HalfP p1 = softmax_half(s1, kbase + 32, masked);
+    if constexpr (PV) {   // P.V of half 0 beside softmax 1
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        SX_SG(0x100, 2);
+        SX_SG(0x008, 1);
+        SX_SG(0x002, 10);
+      }
+    }
+    if (p1.rescale) rescale_o(p1.alpha);
+    pv_half(Vb, 1, p1);
+  };
+  // one tile: compute from (Kb, Vb), then (after the barrier) refill them with tile kt + 2
   auto step = [&](int kt, char* Kb, char* Vb) {
     const int kbase = kt * KT;
     if (kbase <= wave_max) {   // otherwise every column of this wave is before the tile
-      // S^T = K Q^T for the 64 keys of the tile: two 32-key M tiles
-      f32x16_t sacc[2];
-      const f32x16_t zero16 = {};
-#pragma unroll
-      for (int mt = 0; mt < 2; ++mt) {
-        const int rr = mt * 32 + l32;
-#pragma unroll
-        for (int s = 0; s < D / 16; ++s) {
-          const int c = 2 * s + hg;
-          const bf16x8_t ka = *(const bf16x8_t*)(Kb + rr * ROWB + ((c ^ (rr & (NCH - 1))) << 4));
-          sacc[mt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka, qb[s], s == 0 ? zero16 : sacc[mt], 0, 0, 0);
-        }
-      }
-      // lane value e of M tile mt is key kbase + 32 mt + 8 (e / 4) + 4 hg + e % 4 of the lane's column
-      float x[32];
-#pragma unroll
-      for (int mt = 0; mt < 2; ++mt)
-#pragma unroll
-        for (int e = 0; e < 16; ++e) x[mt * 16 + e] = sacc[mt][e];
-      if (kbase + KT - 1 > wave_min) {
-        const int lim = pos - kbase - hg * 4;   // mask keys with offset > lim
-#pragma unroll
-        for (int i = 0; i < 32; ++i) {
-          const int koff = (i >> 4) * 32 + ((i & 15) >> 2) * 8 + (i & 3);
-          if (koff > lim) x[i] = -INFINITY;
-        }
-      }
-      float mx = x[0];
-#pragma unroll
-      for (int i = 1; i < 32; ++i) mx = fmaxf(mx, x[i]);
-      mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
-      const float m_tile = mx * c2;             // scaled, log2 domain (c2 > 0)
-      // raise the running max only when it grows by more than 8
-      const bool grow = m_tile > m_run + 8.f;
-      if (__ballot(grow)) {
-        const float m_new = grow ? m_tile : m_run;
-        const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);   // m_run = -inf -> 0
-        l_run *= alpha;
-        if constexpr (PV) {
-#pragma unroll
-          for (int dt = 0; dt < D / 32; ++dt)
-#pragma unroll
-            for (int e = 0; e < 16; ++e) o[dt][e] *= alpha;
-        }
-        m_run = m_new;
-      }
-      const float m_use = m_run == -INFINITY ? 0.f : m_run;
-      float psum = 0.f;
-#pragma unroll
-      for (int i = 0; i < 32; ++i) {
-        x[i] = __builtin_amdgcn_exp2f(__builtin_fmaf(x[i], c2, -m_use));
-        psum += x[i];
-      }
-      l_run += psum;
-      if constexpr (PV) {
-        // P^T operand of k-step kk (16 keys) = lane values x[8kk .. 8kk+7]
-        bf16x8_t pb[4];
-#pragma unroll
-        for (int kk = 0; kk < 4; ++kk) {
-          uint4 t;
-          t.x = pack_bf16x2(x[8 * kk + 0], x[8 * kk + 1]);
-          t.y = pack_bf16x2(x[8 * kk + 2], x[8 * kk + 3]);
-          t.z = pack_bf16x2(x[8 * kk + 4], x[8 * kk + 5]);
-          t.w = pack_bf16x2(x[8 * kk + 6], x[8 * kk + 7]);
-          pb[kk] = __builtin_bit_cast(bf16x8_t, t);
-        }
-#pragma unroll
-        for (int dt = 0; dt < D / 32; ++dt) {
-          // dims 32 dt + 16 (tg & 1) + 4 tc .. +3 -> 16-byte chunk, 8-byte half
-          const int dchunk = 4 * dt + 2 * (tg & 1) + (tc >> 1);
-          const int dhalf = (tc & 1) * 8;
-#pragma unroll
-          for (int kk = 0; kk < 4; ++kk) {
-            shortx4_t h2[2];
-#pragma unroll
-            for (int h = 0; h < 2; ++h) {
-              // slots 8 hg + 4h + k <-> key 16 kk + 8 h + 4 hg + k (the P^T operand order)
-              const int rr = 16 * kk + 8 * h + 4 * (tg >> 1) + tk;
-              const int off = rr * ROWB + ((dchunk ^ v_swz<NCH>(rr)) << 4) + dhalf;
-              h2[h] = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_shortx4_t*)(Vb + off));
-            }
-            const bf16x8_t va = __builtin_bit_cast(
-                bf16x8_t, make_uint4(__builtin_bit_cast(uint2, h2[0]).x, __builtin_bit_cast(uint2, h2[0]).y,
-                                     __builtin_bit_cast(uint2, h2[1]).x, __builtin_bit_cast(uint2, h2[1]).y));
-            o[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, pb[kk], o[dt], 0, 0, 0);
-          }
-        }
-      }
+      if (kbase + KT - 1 > wave_min)
+        key_tile(Kb, Vb, kbase, std::true_type{});
+      else
+        key_tile(Kb, Vb, kbase, std::false_type{});
     }
     if (kt + 1 < nkt) {
       SX_WAIT_VMCNT(0);          // this wave's part of tile kt+1 has landed
