@@ -30,7 +30,7 @@ namespace sx {
 namespace {
 
 constexpr int KT = 64;     // keys per tile
-constexpr int COLS = 128;  // query columns per workgroup (32 per wave)
+constexpr int COLS = 256;  // query columns per workgroup (8 waves x 32)
 
 struct AttnK {
   const uint16_t* q;
@@ -63,18 +63,16 @@ typedef __attribute__((address_space(3))) shortx4_t lds_shortx4_t;
 #define SX_WAIT_VMCNT(n) __builtin_amdgcn_s_waitcnt(((n) & 0xF) | (0x7 << 4) | (0xF << 8))
 
 template <int D, bool PAGED, bool PV>
-__global__ __launch_bounds__(256, 2) void attn_mfma_kernel(AttnK a) {
+__global__ __launch_bounds__(512, 1) void attn_mfma_kernel(AttnK a) {
+  constexpr int NW = 8;                       // waves: two groups of 4
   constexpr int ROWB = D * 2;                 // bytes of one key row
   constexpr int NCH = ROWB / 16;              // 16-byte chunks per row
   constexpr int TILEB = KT * ROWB;            // bytes of one K (or V) tile
-  constexpr int RPK = 1024 / ROWB;            // rows per 1 KB direct-load instruction
-  constexpr int IPW = TILEB / 1024 / 4;       // direct-load instructions per wave per matrix
-  constexpr int NMAT = PV ? 2 : 1;
+  constexpr int RPK = 1024 / ROWB;            // rows per 1 KB transfer instruction
+  constexpr int IPW = TILEB / 1024 / NW;      // transfer instructions per wave per matrix
   // LDS: two buffers of K and V tiles, rows row-major; chunk c of row r of K sits at chunk
   // c ^ (r mod NCH) (conflict-free 16-byte row reads), of V at c ^ v_swz(r) (conflict-free
-  // transposed 8-byte reads).  Each buffer is its
-  // own array so the compiler can tell the in-flight loads into one buffer from the reads of
-  // the other (no false waits).
+  // transposed 8-byte reads).
   __shared__ __attribute__((aligned(1024))) char K0[TILEB];
   __shared__ __attribute__((aligned(1024))) char K1[TILEB];
   __shared__ __attribute__((aligned(1024))) char V0[PV ? TILEB : 16];
@@ -83,6 +81,8 @@ __global__ __launch_bounds__(256, 2) void attn_mfma_kernel(AttnK a) {
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int w = tid >> 6;
+  const int wu = __builtin_amdgcn_readfirstlane(w);
+  const int grp = wu >> 2;                    // 0: group X, 1: group Y
   const int l32 = lane & 31;
   const int hg = lane >> 5;
   const int kvh = (int)(blockIdx.x % (unsigned)a.Hkv);
@@ -105,8 +105,8 @@ __global__ __launch_bounds__(256, 2) void attn_mfma_kernel(AttnK a) {
   const int rpw = a.rpw;
   const int ntiles = (nrows + rpw - 1) / rpw;
   if (rank >= ntiles) return;
-  const int tile = ntiles - 1 - rank;
-  const int row0 = tile * rpw;
+  const int row_tile = ntiles - 1 - rank;
+  const int row0 = row_tile * rpw;
   const int col = w * 32 + l32;
   const int lrow = col / a.G;
   const int hh = col - lrow * a.G;
@@ -142,15 +142,14 @@ __global__ __launch_bounds__(256, 2) void attn_mfma_kernel(AttnK a) {
     for (int e = 0; e < 16; ++e) o[i][e] = 0.f;
   float m_run = -INFINITY;
   float l_run = 0.f;
+  const float c2 = a.scale_log2;
 
-  // ---- direct global -> LDS tile loads.  Instruction q (1 KB) of a tile holds rows
-  // RPK*q .. RPK*q + RPK - 1, all inside one 16-key block; keys past the end read row T-1 (they
-  // are masked: every query row is < T). ----
+  // ---- global -> LDS tile transfers (16 bytes per lane, all 8 waves share each tile).
+  // Transfer q (1 KB) of a tile holds rows RPK*q .. RPK*q + RPK - 1, all inside one 16-key block;
+  // keys past the end read row T-1 (they are masked: every query row is < T). ----
   const int last_key = T - 1;
-  const int lrow_in = lane / NCH;     // row of this lane inside its 1 KB chunk
+  const int lrow_in = lane / NCH;     // row of this lane inside its 1 KB piece
   const int pchunk = lane % NCH;      // physical chunk this lane fills
-  const int wu = __builtin_amdgcn_readfirstlane(w);
-  // base of (block, head) for the wave's 16-key block, and for the block holding key T-1
   auto block_base = [&](const uint16_t* base, int key16) -> const uint16_t* {
     if constexpr (PAGED) {
       // the block table is read-only here: read it through the constant address space (scalar loads)
@@ -174,8 +173,12 @@ __global__ __launch_bounds__(256, 2) void attn_mfma_kernel(AttnK a) {
     const uint32_t m0 = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) const char*)dst;
     asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(src), "s"(m0) : "m0");
   };
-  // Per-lane byte offsets of the transfers inside a (block, head) run of 16 rows.  Tiles start at
-  // multiples of 64 keys, so these are the same for every tile.
+  auto dma16_sb = [&](const uint16_t* sbase, uint32_t voffset, const char* dst) {
+    const uint32_t m0 = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) const char*)dst;
+    asm volatile("s_mov_b32 m0, %2\n\tglobal_load_lds_dwordx4 %0, %1" ::"v"(voffset), "s"(sbase), "s"(m0) : "m0");
+  };
+  // per-lane byte offsets of the transfers inside a (block, head) run; tiles start at multiples
+  // of 64 keys, so they are the same for every tile
   uint32_t koff[IPW], voff[IPW];
 #pragma unroll
   for (int i = 0; i < IPW; ++i) {
@@ -183,146 +186,119 @@ __global__ __launch_bounds__(256, 2) void attn_mfma_kernel(AttnK a) {
     koff[i] = (uint32_t)(((rr & 15) * rstride + (pchunk ^ (rr & (NCH - 1))) * 8) * 2);
     voff[i] = (uint32_t)(((rr & 15) * rstride + (pchunk ^ v_swz<NCH>(rr)) * 8) * 2);
   }
-  // global (SGPR base + VGPR byte offset) -> LDS transfer of 16 bytes per lane
-  auto dma16_sb = [&](const uint16_t* sbase, uint32_t voffset, const char* dst) {
-    const uint32_t m0 = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) const char*)dst;
-    asm volatile("s_mov_b32 m0, %2\n\tglobal_load_lds_dwordx4 %0, %1" ::"v"(voffset), "s"(sbase), "s"(m0) : "m0");
-  };
-  auto issue = [&](int kt, char* Kd, char* Vd) {
+  // transfer of one matrix (K or V) tile kt into dst
+  auto issue = [&](const uint16_t* base, const uint16_t* row_last, int kt, char* dst, bool is_v) {
     const int kbase = kt * KT;
     if (kbase + KT - 1 <= last_key) {
-      // whole tile inside the request: wave-uniform block base + precomputed lane offset
 #pragma unroll
       for (int i = 0; i < IPW; ++i) {
         const int q = wu * IPW + i;
         const int kb16 = __builtin_amdgcn_readfirstlane((kbase + q * RPK) >> 4);
-        dma16_sb(block_base(a.k, kb16), koff[i], Kd + q * 1024);
-        if constexpr (PV) dma16_sb(block_base(a.v, kb16), voff[i], Vd + q * 1024);
+        dma16_sb(block_base(base, kb16), is_v ? voff[i] : koff[i], dst + q * 1024);
       }
       return;
     }
 #pragma unroll
     for (int i = 0; i < IPW; ++i) {
-      const int q = wu * IPW + i;                 // wave-uniform
+      const int q = wu * IPW + i;
       const int rr = q * RPK + lrow_in;
       const int key = kbase + rr;
-      const bool past = key > last_key;
-      const int kb16 = __builtin_amdgcn_readfirstlane(min((kbase + q * RPK) >> 4, last_key >> 4));  // uniform
-      const int ck = pchunk ^ (rr & (NCH - 1));
-      // block bases are loaded unconditionally (wave-uniform, scalar loads); the clamp of keys
-      // past the end is a per-lane select
-      const uint16_t* kblk = block_base(a.k, kb16);
-      const uint16_t* vblk = PV ? block_base(a.v, kb16) : nullptr;
-      const int64_t roff = (int64_t)(key & 15) * rstride;
-      const uint16_t* krow = past ? k_last : kblk + roff;
-      dma16(krow + ck * 8, Kd + q * 1024);
-      if constexpr (PV) {
-        const int cv = pchunk ^ v_swz<NCH>(rr);
-        const uint16_t* vrow = past ? v_last : vblk + roff;
-        dma16(vrow + cv * 8, Vd + q * 1024);
-      }
+      const int kb16 = __builtin_amdgcn_readfirstlane(min((kbase + q * RPK) >> 4, last_key >> 4));
+      const int c = pchunk ^ (is_v ? v_swz<NCH>(rr) : (rr & (NCH - 1)));
+      const uint16_t* blk = block_base(base, kb16);
+      const uint16_t* row = key > last_key ? row_last : blk + (int64_t)(key & 15) * rstride;
+      dma16(row + c * 8, dst + q * 1024);
     }
   };
 
-  issue(0, K0, V0);
-  if (nkt > 1) {
-    issue(1, K1, V1);
-    SX_WAIT_VMCNT(IPW * NMAT);   // tile 0 landed (tile 1 may still be in flight)
-  } else {
-    SX_WAIT_VMCNT(0);
-  }
-  __syncthreads();
-  const float c2 = a.scale_log2;
-  // V^T operand addressing (transposed 8-byte reads): lane 4k + c of each 16-lane group points
-  // at row k, dims 4c .. 4c+3 of its 16-dim slice; the group's lane j receives dim j of 4 rows.
-  const int tg = lane >> 4;           // 16-lane group
-  const int tk = (lane & 15) >> 2;    // row inside the group's 4 rows
-  const int tc = lane & 3;            // 4-dim piece
-  // one tile: compute from (Kb, Vb), then (after the barrier) refill them with tile kt + 2
-  // ---- one tile in two 32-key halves, so that each half's softmax (vector ALU) has independent
-  // matrix work beside it: S of half 1 runs beside the softmax of half 0, and P.V of half 0 beside
-  // the softmax of half 1. ----
-  // S^T of half mt: keys kbase + 32 mt .. + 31
-  auto s_half = [&](const char* Kb, int mt) -> f32x16_t {
-    f32x16_t acc;
+  // ---- tile computations ----
+  // S^T = K Q^T for the 64 keys of a tile (two 32-key M tiles)
+  f32x16_t sacc[2];
+  auto s_tile = [&](const char* Kb) {
     const f32x16_t zero16 = {};
-    const int rr = mt * 32 + l32;
 #pragma unroll
-    for (int s = 0; s < D / 16; ++s) {
-      const int c = 2 * s + hg;
-      const bf16x8_t ka = *(const bf16x8_t*)(Kb + rr * ROWB + ((c ^ (rr & (NCH - 1))) << 4));
-      acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka, qb[s], s == 0 ? zero16 : acc, 0, 0, 0);
+    for (int mt = 0; mt < 2; ++mt) {
+      const int rr = mt * 32 + l32;
+#pragma unroll
+      for (int s = 0; s < D / 16; ++s) {
+        const int c = 2 * s + hg;
+        const bf16x8_t ka = *(const bf16x8_t*)(Kb + rr * ROWB + ((c ^ (rr & (NCH - 1))) << 4));
+        sacc[mt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka, qb[s], s == 0 ? zero16 : sacc[mt], 0, 0, 0);
+        // keep at most a few K operands in flight (register budget of two waves per SIMD)
+        if ((s & 3) == 3) __builtin_amdgcn_sched_barrier(0);
+      }
     }
-    return acc;
   };
-  // Online softmax of one half (lane value e = key k0 + 8 (e / 4) + 4 hg + e % 4 of the lane's
-  // column).  The running max is raised only when it grows by more than 8 (log2 units); alpha is
-  // the factor for what was accumulated before (1 when not raised).  Returns the P^T operands of
-  // the half's two 16-key k-steps.
-  struct HalfP {
-    bf16x8_t pb[2];
-    float alpha;
-    bool rescale;   // wave-uniform: some lane raised its max
-  };
-  auto softmax_half = [&](f32x16_t sv, int k0, auto masked) -> HalfP {
-    float x[16];
+  // online softmax of the tile in sacc (lane value e of M tile mt is key
+  // kbase + 32 mt + 8 (e / 4) + 4 hg + e % 4 of the lane's column) -> P^T operands
+  bf16x8_t pb[4];
+  auto softmax_tile = [&](int kbase) {
+    float x[32];
 #pragma unroll
-    for (int e = 0; e < 16; ++e) x[e] = sv[e];
-    if constexpr (decltype(masked)::value) {
-      const int lim = pos - k0 - hg * 4;   // mask keys with offset > lim
+    for (int mt = 0; mt < 2; ++mt)
 #pragma unroll
-      for (int e = 0; e < 16; ++e)
-        if ((e >> 2) * 8 + (e & 3) > lim) x[e] = -INFINITY;
+      for (int e = 0; e < 16; ++e) x[mt * 16 + e] = sacc[mt][e];
+    if (kbase + KT - 1 > wave_min) {
+      const int lim = pos - kbase - hg * 4;   // mask keys with offset > lim
+#pragma unroll
+      for (int i = 0; i < 32; ++i) {
+        const int koff = (i >> 4) * 32 + ((i & 15) >> 2) * 8 + (i & 3);
+        if (koff > lim) x[i] = -INFINITY;
+      }
     }
     float mx = x[0];
 #pragma unroll
-    for (int e = 1; e < 16; ++e) mx = fmaxf(mx, x[e]);
+    for (int i = 1; i < 32; ++i) mx = fmaxf(mx, x[i]);
     mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
     const float m_tile = mx * c2;             // scaled, log2 domain (c2 > 0)
+    // the running max is raised only when it grows by more than 8: the O^T rescale is rare and
+    // probabilities stay below 2^8
     const bool grow = m_tile > m_run + 8.f;
-    const float m_new = grow ? m_tile : m_run;
-    HalfP r;
-    r.alpha = __builtin_amdgcn_exp2f(m_run - m_new);   // 1 when kept; m_run = -inf -> 0
-    r.rescale = __ballot(grow) != 0;
-    m_run = m_new;
+    if (__ballot(grow)) {
+      const float m_new = grow ? m_tile : m_run;
+      const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);   // m_run = -inf -> 0
+      l_run *= alpha;
+      if constexpr (PV) {
+#pragma unroll
+        for (int dt = 0; dt < D / 32; ++dt)
+#pragma unroll
+          for (int e = 0; e < 16; ++e) o[dt][e] *= alpha;
+      }
+      m_run = m_new;
+    }
     const float m_use = m_run == -INFINITY ? 0.f : m_run;
     float psum = 0.f;
 #pragma unroll
-    for (int e = 0; e < 16; ++e) {
-      x[e] = __builtin_amdgcn_exp2f(__builtin_fmaf(x[e], c2, -m_use));
-      psum += x[e];
+    for (int i = 0; i < 32; ++i) {
+      x[i] = __builtin_amdgcn_exp2f(__builtin_fmaf(x[i], c2, -m_use));
+      psum += x[i];
     }
-    l_run = l_run * r.alpha + psum;
+    l_run += psum;
 #pragma unroll
-    for (int kk = 0; kk < 2; ++kk) {
+    for (int kk = 0; kk < 4; ++kk) {
       uint4 t;
       t.x = pack_bf16x2(x[8 * kk + 0], x[8 * kk + 1]);
       t.y = pack_bf16x2(x[8 * kk + 2], x[8 * kk + 3]);
       t.z = pack_bf16x2(x[8 * kk + 4], x[8 * kk + 5]);
       t.w = pack_bf16x2(x[8 * kk + 6], x[8 * kk + 7]);
-      r.pb[kk] = __builtin_bit_cast(bf16x8_t, t);
-    }
-    return r;
-  };
-  auto rescale_o = [&](float alpha) {
-    if constexpr (PV) {
-#pragma unroll
-      for (int dt = 0; dt < D / 32; ++dt)
-#pragma unroll
-        for (int e = 0; e < 16; ++e) o[dt][e] *= alpha;
+      pb[kk] = __builtin_bit_cast(bf16x8_t, t);
     }
   };
-  // O^T += V^T P^T for the keys of half mt (k-steps 2 mt, 2 mt + 1)
-  auto pv_half = [&](const char* Vb, int mt, const HalfP& P) {
+  // V^T operand addressing (transposed 8-byte reads): lane 4k + c of each 16-lane group points
+  // at row k, dims 4c .. 4c+3 of its 16-dim slice; the group's lane j receives dim j of 4 rows.
+  const int tg = lane >> 4;
+  const int tk = (lane & 15) >> 2;
+  const int tc = lane & 3;
+  // O^T += V^T P^T
+  auto pv_tile = [&](const char* Vb) {
     if constexpr (PV) {
 #pragma unroll
-      for (int dt = 0; dt < D / 32; ++dt) {
-        // dims 32 dt + 16 (tg & 1) + 4 tc .. +3 -> 16-byte chunk, 8-byte half
-        const int dchunk = 4 * dt + 2 * (tg & 1) + (tc >> 1);
-        const int dhalf = (tc & 1) * 8;
+      for (int kk = 0; kk < 4; ++kk)
 #pragma unroll
-        for (int j = 0; j < 2; ++j) {
-          const int kk = 2 * mt + j;
+        for (int dt = 0; dt < D / 32; ++dt) {
+          // dims 32 dt + 16 (tg & 1) + 4 tc .. +3 -> 16-byte chunk, 8-byte half
+          const int dchunk = 4 * dt + 2 * (tg & 1) + (tc >> 1);
+          const int dhalf = (tc & 1) * 8;
           shortx4_t h2[2];
 #pragma unroll
           for (int h = 0; h < 2; ++h) {
@@ -334,58 +310,53 @@ __global__ __launch_bounds__(256, 2) void attn_mfma_kernel(AttnK a) {
           const bf16x8_t va = __builtin_bit_cast(
               bf16x8_t, make_uint4(__builtin_bit_cast(uint2, h2[0]).x, __builtin_bit_cast(uint2, h2[0]).y,
                                    __builtin_bit_cast(uint2, h2[1]).x, __builtin_bit_cast(uint2, h2[1]).y));
-          o[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, P.pb[j], o[dt], 0, 0, 0);
+          o[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, pb[kk], o[dt], 0, 0, 0);
         }
-      }
     }
   };
-  // Scheduling hints (instruction classes: 0x2 VALU, 0x8 MFMA, 0x100 LDS read): ask for the matrix
-  // instructions of one half to be spread through the vector-ALU softmax of the other.
-#define SX_SG(mask, n) __builtin_amdgcn_sched_group_barrier(mask, n, 0)
-  auto key_tile = [&](const char* Kb, const char* Vb, int kbase, auto masked) {
-    const f32x16_t s0 = s_half(Kb, 0);
-    const f32x16_t s1 = s_half(Kb, 1);
-    const HalfP p0 = softmax_half(s0, kbase, masked);
-    // K reads, S of half 0, then S of half 1 beside softmax 0
-    SX_SG(0x100, 16);
-    SX_SG(0x008, 8);
-#pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      SX_SG(0x008, 1);
-      SX_SG(0x002, 10);
-    }
-    if (p0.rescale) rescale_o(p0.alpha);
-    pv_half(Vb, 0, p0);
-    const HalfP p1 = softmax_half(s1, kbase + 32, masked);
-    if constexpr (PV) {   // P.V of half 0 beside softmax 1
-#pragma unroll
-      for (int i = 0; i < 8; ++i) {
-        SX_SG(0x100, 2);
-        SX_SG(0x008, 1);
-        SX_SG(0x002, 10);
-      }
-    }
-    if (p1.rescale) rescale_o(p1.alpha);
-    pv_half(Vb, 1, p1);
-  };
-  // one tile: compute from (Kb, Vb), then (after the barrier) refill them with tile kt + 2
-  auto step = [&](int kt, char* Kb, char* Vb) {
-    const int kbase = kt * KT;
-    if (kbase <= wave_max) {   // otherwise every column of this wave is before the tile
-      if (kbase + KT - 1 > wave_min)
-        key_tile(Kb, Vb, kbase, std::true_type{});
-      else
-        key_tile(Kb, Vb, kbase, std::false_type{});
-    }
-    if (kt + 1 < nkt) {
-      SX_WAIT_VMCNT(0);          // this wave's part of tile kt+1 has landed
-      __syncthreads();           // tile kt+1 visible to all; every wave is done with (Kb, Vb)
-      if (kt + 2 < nkt) issue(kt + 2, Kb, Vb);
+
+  // ---- ping-pong schedule.  Slots are separated by workgroup barriers.  Group X (waves 0-3)
+  // runs its matrix phase M(j) = [P.V of tile j-1, S of tile j] in slot 2j and its softmax of tile
+  // j in slot 2j+1; group Y is one slot behind.  So in every slot one wave of each SIMD issues
+  // MFMAs while the other runs the softmax on the vector ALU.  Tile j's K is read in slots 2j and
+  // 2j+1, its V in slots 2j+2 and 2j+3.  At the start of slot 2j the transfers of K(j+1) (into
+  // the buffer of K(j-1)) and V(j) (into the buffer of V(j-2)) are issued; they are waited for at
+  // the end of slot 2j+1. ----
+  issue(a.k, k_last, 0, K0, false);
+  SX_WAIT_VMCNT(0);
+  __syncthreads();
+  auto slot_start = [&](int j) {   // start of slot 2j: transfers of K(j+1) and V(j)
+    if (j + 1 < nkt) issue(a.k, k_last, j + 1, ((j + 1) & 1) ? K1 : K0, false);
+    if constexpr (PV) {
+      if (j < nkt) issue(a.v, v_last, j, (j & 1) ? V1 : V0, true);
     }
   };
-  for (int kt = 0; kt < nkt; kt += 2) {
-    step(kt, K0, V0);
-    if (kt + 1 < nkt) step(kt + 1, K1, V1);
+  auto matrix_phase = [&](int j) {   // M(j) = [P.V of tile j-1, S of tile j]
+    if (j >= 1 && (j - 1) * KT <= wave_max) pv_tile(((j - 1) & 1) ? V1 : V0);
+    if (j < nkt && j * KT <= wave_max) s_tile((j & 1) ? K1 : K0);
+  };
+  auto vector_phase = [&](int j) {   // softmax of tile j
+    if (j >= 0 && j < nkt && j * KT <= wave_max) softmax_tile(j * KT);
+  };
+  // slots 2j and 2j+1 for j = 0 .. nkt; both groups pass the same barriers
+  if (grp == 0) {
+    for (int j = 0; j <= nkt; ++j) {
+      slot_start(j);
+      matrix_phase(j);
+      __syncthreads();
+      vector_phase(j);
+      SX_WAIT_VMCNT(0);   // this wave's transfers of slot 2j have landed
+      __syncthreads();
+    }
+  } else {
+    for (int j = 0; j <= nkt; ++j) {
+      slot_start(j);
+      vector_phase(j - 1);
+      __syncthreads();
+      matrix_phase(j);
+      SX_WAIT_VMCNT(0);
+      __syncthreads();
+    }
   }
 
   const float l_tot = l_run + __shfl_xor(l_run, 32, 64);
@@ -549,7 +520,7 @@ hipError_t launch_mfma(const AttnLaunch& L, hipStream_t s) {
   a.n_req = L.n_req;
   const int64_t ntiles = (L.grid_rows + a.rpw - 1) / a.rpw;
   const dim3 grid((unsigned)(ntiles * L.Hkv * L.n_req));
-  hipLaunchKernelGGL((attn_mfma_kernel<D, PAGED, PV>), grid, dim3(256), 0, s, a);
+  hipLaunchKernelGGL((attn_mfma_kernel<D, PAGED, PV>), grid, dim3(512), 0, s, a);
   return hipGetLastError();
 }
 
