@@ -224,8 +224,6 @@ __global__ __launch_bounds__(512, 1) void attn_mfma_kernel(AttnK a) {
         const int c = 2 * s + hg;
         const bf16x8_t ka = *(const bf16x8_t*)(Kb + rr * ROWB + ((c ^ (rr & (NCH - 1))) << 4));
         sacc[mt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka, qb[s], s == 0 ? zero16 : sacc[mt], 0, 0, 0);
-        // keep at most a few K operands in flight (register budget of two waves per SIMD)
-        if ((s & 3) == 3) __builtin_amdgcn_sched_barrier(0);
       }
     }
   };
