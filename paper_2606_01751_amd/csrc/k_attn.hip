@@ -5,22 +5,23 @@
 //   * the per-key column sums of the Sparse-Q probabilities (Eq. sparseq-score).
 //
 // CDNA4 design (gfx950, wave64, v_mfma_f32_32x32x16_bf16):
-//   * One workgroup = 4 waves = 128 query columns of one KV head; a column is a (query row,
+//   * One workgroup = 8 waves = 256 query columns of one KV head; a column is a (query row,
 //     query head) pair, so the G = Hq/Hkv heads that share a KV head share every K/V tile.
 //   * Scores are formed transposed, S^T = K Q^T: each lane then owns one query column, so the
-//     running max / sum of the online softmax stay in the lane (one cross-half exchange per tile).
+//     running max / sum of the online softmax stay in the lane (one cross-half exchange).
 //   * The output is accumulated transposed, O^T += V^T P^T: the B operand P^T is exactly the
 //     lane's own S^T accumulator registers (converted to bf16), no data movement.
-//   * K tiles sit in LDS row-major (padded rows, conflict-free 16-byte reads).  V tiles sit in
-//     LDS as [key run of 4][d][4 keys], so the V^T A operand of a lane is two contiguous 8-byte
-//     reads and each loader thread writes 64 contiguous bytes.
-//   * K/V tiles are double-buffered in LDS (one barrier per tile); global loads of tile j+2 are
-//     in flight while tile j is computed.
+//   * K and V tiles (64 keys) move global -> LDS directly (16 bytes per lane), triple-buffered;
+//     they sit row-major with XOR-swizzled 16-byte chunks: conflict-free 16-byte K reads and
+//     transposed 8-byte V^T reads.
+//   * Ping-pong: two groups of 4 waves (one of each per SIMD) alternate a matrix phase
+//     (MFMAs fed by pipelined LDS reads) and a softmax phase, so the matrix cores and the vector
+//     ALU of a SIMD work at the same time; tile transfers are issued from the softmax phase.
 //   * The 1-D grid is decoded KV head fastest, then request, then query-row tile from the latest
 //     rows (most keys) to the earliest: the heaviest tiles of every head start first, and with 8 KV
 //     heads the round-robin dispatch keeps all tiles of one head on one XCD (one L2).
-//   * Softmax: the running max is only raised when it grows by more than 8 (log2 units), so the
-//     O^T rescale is rare; probabilities then stay below 2^8, safe in float32 and bfloat16.
+//   * Softmax in the log2 domain; the running max is raised only when a probability would reach
+//     2^64, so the O^T rescale is rare and there is no max reduction on the common path.
 #include <type_traits>
 
 #include "sx_device.h"
@@ -61,8 +62,25 @@ typedef __attribute__((address_space(3))) shortx4_t lds_shortx4_t;
 
 // s_waitcnt with vmcnt <= n (n < 16), expcnt and lgkmcnt left unconstrained (gfx9 encoding).
 #define SX_WAIT_VMCNT(n) __builtin_amdgcn_s_waitcnt(((n) & 0xF) | (0x7 << 4) | (0xF << 8))
+// Scheduling groups (instruction classes of the sched_group_barrier builtin): the next `n`
+// instructions of class `mask` are placed here, in program order of the groups.
+#define SX_SG(mask, n) __builtin_amdgcn_sched_group_barrier(mask, n, 0)
+constexpr int kSgMfma = 0x8, kSgDsRead = 0x100;
+// Order of a matrix phase of NM MFMAs whose operands come from NR LDS reads each: the reads of
+// the first PRE MFMAs go first, then every MFMA is followed by the reads of the MFMA PRE places
+// later, so each read has PRE MFMAs (32 cycles each) to complete.
+template <int NM, int NR, int PRE>
+__device__ __forceinline__ void sched_pipelined() {
+  SX_SG(kSgDsRead, NR * PRE);
+#pragma unroll
+  for (int i = 0; i < NM - PRE; ++i) {
+    SX_SG(kSgMfma, 1);
+    SX_SG(kSgDsRead, NR);
+  }
+  SX_SG(kSgMfma, PRE);
+}
 
-template <int D, bool PAGED, bool PV>
+template <int D, bool PAGED, bool PV, bool PRESCALE>
 __global__ __launch_bounds__(512, 1) void attn_mfma_kernel(AttnK a) {
   constexpr int NW = 8;                       // waves: two groups of 4
   constexpr int ROWB = D * 2;                 // bytes of one key row
@@ -70,13 +88,21 @@ __global__ __launch_bounds__(512, 1) void attn_mfma_kernel(AttnK a) {
   constexpr int TILEB = KT * ROWB;            // bytes of one K (or V) tile
   constexpr int RPK = 1024 / ROWB;            // rows per 1 KB transfer instruction
   constexpr int IPW = TILEB / 1024 / NW;      // transfer instructions per wave per matrix
-  // LDS: two buffers of K and V tiles, rows row-major; chunk c of row r of K sits at chunk
-  // c ^ (r mod NCH) (conflict-free 16-byte row reads), of V at c ^ v_swz(r) (conflict-free
-  // transposed 8-byte reads).
-  __shared__ __attribute__((aligned(1024))) char K0[TILEB];
-  __shared__ __attribute__((aligned(1024))) char K1[TILEB];
-  __shared__ __attribute__((aligned(1024))) char V0[PV ? TILEB : 16];
-  __shared__ __attribute__((aligned(1024))) char V1[PV ? TILEB : 16];
+  static_assert(IPW * RPK == 8, "a wave moves 8 consecutive rows of every tile");
+  // PRESCALE (attention output without log-sum-exp): the scores are formed in the log2 domain by
+  // the MFMA itself: Q is multiplied by scale * log2(e) when it is loaded (and rounded to
+  // bfloat16) and the S^T accumulator starts at -m_run, so it holds c2 s - m_run and p = 2^(S^T).
+  // Otherwise (the log-sum-exp pass of Sparse-Q scoring, or a requested log-sum-exp output) Q is
+  // exact and the scale is applied in float32, because the column sums reuse that result with
+  // exact logits.
+  static_assert(PV || !PRESCALE, "the log-sum-exp pass keeps exact logits");
+  // LDS: three buffers each of K and V tiles (tile t in buffer t mod 3), rows row-major; chunk c of
+  // row r of K sits at chunk c ^ (r mod NCH) (conflict-free 16-byte row reads), of V at
+  // c ^ v_swz(r) (conflict-free transposed 8-byte reads).
+  constexpr int NBUF = 3;
+  __shared__ __attribute__((aligned(1024))) char smem[(PV ? 2 : 1) * NBUF * TILEB];
+  char* const kbuf = smem;
+  char* const vbuf = smem + (PV ? NBUF * TILEB : 0);
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -120,6 +146,7 @@ __global__ __launch_bounds__(512, 1) void attn_mfma_kernel(AttnK a) {
   const int wave_min = wave_min_i(valid ? pos : 0x7fffffff);
   const int nkt = wg_max / KT + 1;
   const int qh = kvh * a.G + hh;
+  const float c2 = a.scale_log2;
 
   // Q^T as the B operand: lane owns column l32, d-slots 16s + 8hg .. +7.
   bf16x8_t qb[D / 16];
@@ -128,8 +155,28 @@ __global__ __launch_bounds__(512, 1) void attn_mfma_kernel(AttnK a) {
 #pragma unroll
     for (int s = 0; s < D / 16; ++s) {
       uint4 v = valid ? *(const uint4*)(qp + 16 * s) : make_uint4(0, 0, 0, 0);
+      if constexpr (PRESCALE) {
+        uint32_t u[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+          u[i] = pack_bf16x2(__uint_as_float(u[i] << 16) * c2, __uint_as_float(u[i] & 0xffff0000u) * c2);
+        v = make_uint4(u[0], u[1], u[2], u[3]);
+      }
       qb[s] = __builtin_bit_cast(bf16x8_t, v);
     }
+  }
+  // Block table (paged caches): lane l of a wave holds the block of logical block 64 c + l of
+  // window c.  A wave moves rows 8 wu .. 8 wu + 7 of every tile, all inside logical block
+  // 4 t + wu / 2 of tile t, so one readlane per matrix and tile gives the block, with no memory
+  // access in the loop.  Windows c and c + 1 are held; window c + 2 is loaded 16 tiles before its
+  // first use.
+  const int nblk = (T + 15) >> 4;
+  int win_c = 0;
+  int32_t win0 = 0, win1 = 0;
+  auto load_win = [&](int c) -> int32_t { return a.bt[bt_off + min(64 * c + lane, nblk - 1)]; };
+  if constexpr (PAGED) {
+    win0 = load_win(0);
+    win1 = load_win(1);
   }
   // Q must be complete before any tile transfer is issued: the compiler does not see those
   // transfers, so a later wait of its own for Q would also wait for them.
@@ -140,9 +187,10 @@ __global__ __launch_bounds__(512, 1) void attn_mfma_kernel(AttnK a) {
   for (int i = 0; i < (PV ? D / 32 : 1); ++i)
 #pragma unroll
     for (int e = 0; e < 16; ++e) o[i][e] = 0.f;
-  float m_run = -INFINITY;
+  // Running max (log2 domain).  With PRESCALE it starts as a placeholder 0 that the first tile
+  // replaces; otherwise columns without a row start at 0 so their (unused) sums stay finite.
+  float m_run = PRESCALE ? 0.f : (valid ? -INFINITY : 0.f);
   float l_run = 0.f;
-  const float c2 = a.scale_log2;
 
   // ---- global -> LDS tile transfers (16 bytes per lane, all 8 waves share each tile).
   // Transfer q (1 KB) of a tile holds rows RPK*q .. RPK*q + RPK - 1, all inside one 16-key block;
@@ -160,14 +208,24 @@ __global__ __launch_bounds__(512, 1) void attn_mfma_kernel(AttnK a) {
       return base + ((int64_t)(tok_off + key16 * 16) * a.Hkv + kvh) * D;
     }
   };
+  // base of the (block, head) run of logical block key16 (inside windows win_c, win_c + 1)
+  auto block_base_w = [&](const uint16_t* base, int key16) -> const uint16_t* {
+    if constexpr (PAGED) {
+      const int32_t wv = (key16 >> 6) == win_c ? win0 : win1;
+      const int32_t blk = __builtin_amdgcn_readlane(wv, key16 & 63);
+      return base + (((int64_t)blk * a.Hkv + kvh) * 16) * D;
+    } else {
+      return block_base(base, key16);
+    }
+  };
   constexpr int64_t kRowPaged = D;
   const int64_t rstride = PAGED ? kRowPaged : (int64_t)a.Hkv * D;   // elements between rows of a block
   const uint16_t* k_last = block_base(a.k, last_key >> 4) + (last_key & 15) * rstride;
   const uint16_t* v_last = PV ? block_base(a.v, last_key >> 4) + (last_key & 15) * rstride : nullptr;
   // One 16-byte global -> LDS transfer per lane; the destination (M0) is wave-uniform and lane l
   // lands at dst + 16 l.  Issued as inline assembly so the compiler does not order every later
-  // LDS read behind it: the wait for these transfers is explicit (vmcnt(0) + barrier before a
-  // tile is read).  The statement is volatile, so it stays between the barriers around it; it
+  // LDS read behind it: the wait for these transfers is explicit (vmcnt + barrier before a tile
+  // is read).  The statement is volatile, so it stays between the barriers around it; it
   // declares no memory clobber, which keeps the read-only index loads on the scalar unit.
   auto dma16 = [&](const void* src, const char* dst) {
     const uint32_t m0 = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) const char*)dst;
@@ -186,15 +244,15 @@ __global__ __launch_bounds__(512, 1) void attn_mfma_kernel(AttnK a) {
     koff[i] = (uint32_t)(((rr & 15) * rstride + (pchunk ^ (rr & (NCH - 1))) * 8) * 2);
     voff[i] = (uint32_t)(((rr & 15) * rstride + (pchunk ^ v_swz<NCH>(rr)) * 8) * 2);
   }
-  // transfer of one matrix (K or V) tile kt into dst
+  // transfer of this wave's share of one matrix (K or V) tile kt into dst
   auto issue = [&](const uint16_t* base, const uint16_t* row_last, int kt, char* dst, bool is_v) {
     const int kbase = kt * KT;
     if (kbase + KT - 1 <= last_key) {
+      const uint16_t* b = block_base_w(base, (kbase >> 4) + (wu >> 1));
 #pragma unroll
       for (int i = 0; i < IPW; ++i) {
         const int q = wu * IPW + i;
-        const int kb16 = __builtin_amdgcn_readfirstlane((kbase + q * RPK) >> 4);
-        dma16_sb(block_base(base, kb16), is_v ? voff[i] : koff[i], dst + q * 1024);
+        dma16_sb(b, is_v ? voff[i] : koff[i], dst + q * 1024);
       }
       return;
     }
@@ -205,56 +263,102 @@ __global__ __launch_bounds__(512, 1) void attn_mfma_kernel(AttnK a) {
       const int key = kbase + rr;
       const int kb16 = __builtin_amdgcn_readfirstlane(min((kbase + q * RPK) >> 4, last_key >> 4));
       const int c = pchunk ^ (is_v ? v_swz<NCH>(rr) : (rr & (NCH - 1)));
-      const uint16_t* blk = block_base(base, kb16);
+      const uint16_t* blk = block_base_w(base, kb16);
       const uint16_t* row = key > last_key ? row_last : blk + (int64_t)(key & 15) * rstride;
       dma16(row + c * 8, dst + q * 1024);
     }
   };
+  auto ktile = [&](int t) { return kbuf + (t % NBUF) * TILEB; };
+  auto vtile = [&](int t) { return vbuf + (t % NBUF) * TILEB; };
+  // wait until at most n of this wave's tile transfers (the youngest) are still in flight
+  auto wait_vm = [&](int n) {
+    switch (n) {
+      case 0: SX_WAIT_VMCNT(0); break;
+      case 1: SX_WAIT_VMCNT(1); break;
+      case 2: SX_WAIT_VMCNT(2); break;
+      case 3: SX_WAIT_VMCNT(3); break;
+      case 4: SX_WAIT_VMCNT(4); break;
+      default: SX_WAIT_VMCNT(5); break;
+    }
+  };
+  static_assert(2 * IPW + 1 <= 5, "transfer count per iteration exceeds the wait table");
 
   // ---- tile computations ----
   // S^T = K Q^T for the 64 keys of a tile (two 32-key M tiles)
   f32x16_t sacc[2];
-  auto s_tile = [&](const char* Kb) {
-    const f32x16_t zero16 = {};
-#pragma unroll
-    for (int mt = 0; mt < 2; ++mt) {
-      const int rr = mt * 32 + l32;
-#pragma unroll
-      for (int s = 0; s < D / 16; ++s) {
-        const int c = 2 * s + hg;
-        const bf16x8_t ka = *(const bf16x8_t*)(Kb + rr * ROWB + ((c ^ (rr & (NCH - 1))) << 4));
-        sacc[mt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka, qb[s], s == 0 ? zero16 : sacc[mt], 0, 0, 0);
-      }
-    }
-  };
-  // online softmax of the tile in sacc (lane value e of M tile mt is key
-  // kbase + 32 mt + 8 (e / 4) + 4 hg + e % 4 of the lane's column) -> P^T operands
-  bf16x8_t pb[4];
-  auto softmax_tile = [&](int kbase) {
-    float x[32];
+  auto s_body = [&](const char* Kb) {
+    // accumulator start: -m_run in every slot (PRESCALE), else 0
+    const float init = PRESCALE ? -m_run : 0.f;
 #pragma unroll
     for (int mt = 0; mt < 2; ++mt)
 #pragma unroll
-      for (int e = 0; e < 16; ++e) x[mt * 16 + e] = sacc[mt][e];
-    if (kbase + KT - 1 > wave_min) {
-      const int lim = pos - kbase - hg * 4;   // mask keys with offset > lim
+      for (int e = 0; e < 16; ++e) sacc[mt][e] = init;
 #pragma unroll
-      for (int i = 0; i < 32; ++i) {
-        const int koff = (i >> 4) * 32 + ((i & 15) >> 2) * 8 + (i & 3);
-        if (koff > lim) x[i] = -INFINITY;
+    for (int s = 0; s < D / 16; ++s) {
+#pragma unroll
+      for (int mt = 0; mt < 2; ++mt) {
+        const int rr = mt * 32 + l32;
+        const int c = 2 * s + hg;
+        const bf16x8_t ka = *(const bf16x8_t*)(Kb + rr * ROWB + ((c ^ (rr & (NCH - 1))) << 4));
+        sacc[mt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka, qb[s], sacc[mt], 0, 0, 0);
       }
     }
-    float mx = x[0];
+  };
+  auto s_tile = [&](const char* Kb) {
+    s_body(Kb);
+    sched_pipelined<D / 8, 1, 4>();
+  };
+  // online softmax of the tile in sacc (lane value e of M tile mt is key
+  // kbase + 32 mt + 8 (e / 4) + 4 hg + e % 4 of the lane's column) -> P^T operands.
+  // The running max m_run is not raised tile by tile: p is formed against the current m_run and
+  // m_run is raised (with the O^T / l rescale) only when some p of the wave reaches 2^64 or is not
+  // finite -- on the first tile of a column and when scores grow by more than about 59 in log2
+  // units.  Every p then stays below 2^64, so P, l and O^T keep their float32 / bfloat16
+  // relative precision and cannot overflow; the result is the same softmax.
+  bf16x8_t pb[4];
+  auto softmax_tile = [&](int kbase) {
+    if (kbase + KT - 1 > wave_min) {
+      // keys with offset > lim get -inf; a per-element bit select (no lane-mask registers)
+      const int lim = pos - kbase - hg * 4;
 #pragma unroll
-    for (int i = 1; i < 32; ++i) mx = fmaxf(mx, x[i]);
-    mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
-    const float m_tile = mx * c2;             // scaled, log2 domain (c2 > 0)
-    // the running max is raised only when it grows by more than 8: the O^T rescale is rare and
-    // probabilities stay below 2^8
-    const bool grow = m_tile > m_run + 8.f;
-    if (__ballot(grow)) {
-      const float m_new = grow ? m_tile : m_run;
-      const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);   // m_run = -inf -> 0
+      for (int mt = 0; mt < 2; ++mt)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) {
+          const int koff = mt * 32 + (e >> 2) * 8 + (e & 3);
+          const uint32_t m = (uint32_t)((lim - koff) >> 31);   // all ones where koff > lim
+          sacc[mt][e] = __uint_as_float((__float_as_uint(sacc[mt][e]) & ~m) | (0xff800000u & m));
+        }
+    }
+    float psum = 0.f;
+    // 8 probabilities of slot group kk -> packed P^T operand, added to psum
+    auto emit = [&](int kk, const float* x) {
+      uint4 u;
+      u.x = pack_bf16x2(x[0], x[1]);
+      u.y = pack_bf16x2(x[2], x[3]);
+      u.z = pack_bf16x2(x[4], x[5]);
+      u.w = pack_bf16x2(x[6], x[7]);
+      pb[kk] = __builtin_bit_cast(bf16x8_t, u);
+      if constexpr (PV) {
+        // l sums the bfloat16 probabilities that the P.V product uses
+        const bf16x2_t one2 = __builtin_bit_cast(bf16x2_t, 0x3f803f80u);
+        psum = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, u.x), one2, psum, false);
+        psum = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, u.y), one2, psum, false);
+        psum = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, u.z), one2, psum, false);
+        psum = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, u.w), one2, psum, false);
+      } else {
+#pragma unroll
+        for (int t = 0; t < 8; ++t) psum += x[t];
+      }
+    };
+    auto tile_max = [&]() {
+      float mx = sacc[0][0];
+#pragma unroll
+      for (int mt = 0; mt < 2; ++mt)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) mx = fmaxf(mx, sacc[mt][e]);
+      return fmaxf(mx, __shfl_xor(mx, 32, 64));
+    };
+    auto rescale = [&](float alpha) {
       l_run *= alpha;
       if constexpr (PV) {
 #pragma unroll
@@ -262,25 +366,56 @@ __global__ __launch_bounds__(512, 1) void attn_mfma_kernel(AttnK a) {
 #pragma unroll
           for (int e = 0; e < 16; ++e) o[dt][e] *= alpha;
       }
-      m_run = m_new;
-    }
-    const float m_use = m_run == -INFINITY ? 0.f : m_run;
-    float psum = 0.f;
+    };
+    if constexpr (PRESCALE) {
+      // sacc = c2 s - m_run
+      const bool first = kbase == 0;
+      if (!first) {
 #pragma unroll
-    for (int i = 0; i < 32; ++i) {
-      x[i] = __builtin_amdgcn_exp2f(__builtin_fmaf(x[i], c2, -m_use));
-      psum += x[i];
+        for (int kk = 0; kk < 4; ++kk) {
+          float x[8];
+#pragma unroll
+          for (int t = 0; t < 8; ++t) x[t] = __builtin_amdgcn_exp2f(sacc[kk >> 1][(kk & 1) * 8 + t]);
+          emit(kk, x);
+        }
+      }
+      if (first || __ballot(!(psum < 0x1p64f))) {
+        // raise m_run by the tile's excess (on the first tile: replace the placeholder)
+        const float mx = tile_max();
+        const float sh = mx == -INFINITY ? 0.f : (first ? mx : fmaxf(mx, 0.f));
+        if (!first) rescale(__builtin_amdgcn_exp2f(-sh));
+        m_run += sh;
+        psum = 0.f;
+#pragma unroll
+        for (int kk = 0; kk < 4; ++kk) {
+          float x[8];
+#pragma unroll
+          for (int t = 0; t < 8; ++t) x[t] = __builtin_amdgcn_exp2f(sacc[kk >> 1][(kk & 1) * 8 + t] - sh);
+          emit(kk, x);
+        }
+      }
+    } else {
+      // sacc = s; p = 2^(c2 s - m_run)
+      auto expo = [&](float mneg) {
+        psum = 0.f;
+#pragma unroll
+        for (int kk = 0; kk < 4; ++kk) {
+          float x[8];
+#pragma unroll
+          for (int t = 0; t < 8; ++t)
+            x[t] = __builtin_amdgcn_exp2f(__builtin_fmaf(sacc[kk >> 1][(kk & 1) * 8 + t], c2, mneg));
+          emit(kk, x);
+        }
+      };
+      expo(-m_run);
+      if (__ballot(!(psum < 0x1p64f))) {
+        const float m_new = fmaxf(m_run, tile_max() * c2);          // c2 > 0
+        rescale(m_new == -INFINITY ? 1.f : __builtin_amdgcn_exp2f(m_run - m_new));
+        m_run = m_new;
+        expo(m_new == -INFINITY ? 0.f : -m_new);
+      }
     }
     l_run += psum;
-#pragma unroll
-    for (int kk = 0; kk < 4; ++kk) {
-      uint4 t;
-      t.x = pack_bf16x2(x[8 * kk + 0], x[8 * kk + 1]);
-      t.y = pack_bf16x2(x[8 * kk + 2], x[8 * kk + 3]);
-      t.z = pack_bf16x2(x[8 * kk + 4], x[8 * kk + 5]);
-      t.w = pack_bf16x2(x[8 * kk + 6], x[8 * kk + 7]);
-      pb[kk] = __builtin_bit_cast(bf16x8_t, t);
-    }
   };
   // V^T operand addressing (transposed 8-byte reads): lane 4k + c of each 16-lane group points
   // at row k, dims 4c .. 4c+3 of its 16-dim slice; the group's lane j receives dim j of 4 rows.
@@ -288,7 +423,7 @@ __global__ __launch_bounds__(512, 1) void attn_mfma_kernel(AttnK a) {
   const int tk = (lane & 15) >> 2;
   const int tc = lane & 3;
   // O^T += V^T P^T
-  auto pv_tile = [&](const char* Vb) {
+  auto pv_body = [&](const char* Vb) {
     if constexpr (PV) {
 #pragma unroll
       for (int kk = 0; kk < 4; ++kk)
@@ -312,47 +447,67 @@ __global__ __launch_bounds__(512, 1) void attn_mfma_kernel(AttnK a) {
         }
     }
   };
-
-  // ---- ping-pong schedule.  Slots are separated by workgroup barriers.  Group X (waves 0-3)
-  // runs its matrix phase M(j) = [P.V of tile j-1, S of tile j] in slot 2j and its softmax of tile
-  // j in slot 2j+1; group Y is one slot behind.  So in every slot one wave of each SIMD issues
-  // MFMAs while the other runs the softmax on the vector ALU.  Tile j's K is read in slots 2j and
-  // 2j+1, its V in slots 2j+2 and 2j+3.  At the start of slot 2j the transfers of K(j+1) (into
-  // the buffer of K(j-1)) and V(j) (into the buffer of V(j-2)) are issued; they are waited for at
-  // the end of slot 2j+1. ----
-  issue(a.k, k_last, 0, K0, false);
-  SX_WAIT_VMCNT(0);
-  __syncthreads();
-  auto slot_start = [&](int j) {   // start of slot 2j: transfers of K(j+1) and V(j)
-    if (j + 1 < nkt) issue(a.k, k_last, j + 1, ((j + 1) & 1) ? K1 : K0, false);
+  auto pv_tile = [&](const char* Vb) {
     if constexpr (PV) {
-      if (j < nkt) issue(a.v, v_last, j, (j & 1) ? V1 : V0, true);
+      pv_body(Vb);
+      sched_pipelined<D / 8, 2, 4>();
     }
   };
-  auto matrix_phase = [&](int j) {   // M(j) = [P.V of tile j-1, S of tile j]
-    if (j >= 1 && (j - 1) * KT <= wave_max) pv_tile(((j - 1) & 1) ? V1 : V0);
-    if (j < nkt && j * KT <= wave_max) s_tile((j & 1) ? K1 : K0);
+
+
+  // ---- ping-pong schedule over iterations j = 0 .. nkt.  Iteration j has two slots separated by
+  // workgroup barriers.  Group X (waves 0-3) runs its matrix phase M(j) = [P.V of tile j-1, S of
+  // tile j] in the first slot and the softmax of tile j in the second; group Y runs the softmax of
+  // tile j-1 in the first slot and M(j) in the second.  So in every slot one wave of each SIMD
+  // issues MFMAs while the other runs the softmax on the vector ALU.
+  // Tiles are triple-buffered: at the start of its softmax slot of iteration j each wave issues its
+  // share of the transfers of K(j+2) and V(j+1) (an issue that waits for the address unit then
+  // delays vector work, not MFMAs); they land during iteration j+1 (waited for at its end) and are
+  // read in iteration j+2, and their buffers were last read in iteration j-1. ----
+  auto ncur = [&](int j) {   // transfers (and window loads) this wave issues in iteration j
+    return (j + 2 < nkt ? IPW : 0) + (PV && j + 1 < nkt ? IPW : 0) + ((PAGED && ((j + 2) & 15) == 0) ? 1 : 0);
+  };
+  issue(a.k, k_last, 0, ktile(0), false);
+  if (nkt > 1) issue(a.k, k_last, 1, ktile(1), false);
+  if constexpr (PV) issue(a.v, v_last, 0, vtile(0), true);
+  wait_vm((nkt > 1 ? IPW : 0) + (PV ? IPW : 0));   // K(0) has landed
+  __syncthreads();
+  auto matrix_phase = [&](int j) {
+    if (j >= 1 && (j - 1) * KT <= wave_max) pv_tile(vtile(j - 1));
+    if (j < nkt && j * KT <= wave_max) s_tile(ktile(j));
+  };
+  auto transfer_phase = [&](int j) {   // this wave's share of K(j+2) and V(j+1)
+    if (j + 2 < nkt) issue(a.k, k_last, j + 2, ktile(j + 2), false);
+    if constexpr (PV) {
+      if (j + 1 < nkt) issue(a.v, v_last, j + 1, vtile(j + 1), true);
+    }
+    if constexpr (PAGED) {
+      if (((j + 2) & 15) == 0) {   // tiles j + 2 and j + 3 lie in windows win_c + 1, win_c + 2
+        win0 = win1;
+        win1 = load_win(win_c + 2);
+        ++win_c;
+      }
+    }
   };
   auto vector_phase = [&](int j) {   // softmax of tile j
     if (j >= 0 && j < nkt && j * KT <= wave_max) softmax_tile(j * KT);
   };
-  // slots 2j and 2j+1 for j = 0 .. nkt; both groups pass the same barriers
   if (grp == 0) {
     for (int j = 0; j <= nkt; ++j) {
-      slot_start(j);
       matrix_phase(j);
       __syncthreads();
+      transfer_phase(j);
       vector_phase(j);
-      SX_WAIT_VMCNT(0);   // this wave's transfers of slot 2j have landed
+      wait_vm(ncur(j));   // this wave's transfers of iteration j-1 have landed
       __syncthreads();
     }
   } else {
     for (int j = 0; j <= nkt; ++j) {
-      slot_start(j);
+      transfer_phase(j);
       vector_phase(j - 1);
       __syncthreads();
       matrix_phase(j);
-      SX_WAIT_VMCNT(0);
+      wait_vm(ncur(j));
       __syncthreads();
     }
   }
@@ -496,7 +651,7 @@ __global__ __launch_bounds__(256, 2) void colsum_mfma_kernel(ColsumK a) {
   }
 }
 
-template <int D, bool PAGED, bool PV>
+template <int D, bool PAGED, bool PV, bool PRESCALE>
 hipError_t launch_mfma(const AttnLaunch& L, hipStream_t s) {
   AttnK a{};
   a.q = (const uint16_t*)L.q;
@@ -518,7 +673,7 @@ hipError_t launch_mfma(const AttnLaunch& L, hipStream_t s) {
   a.n_req = L.n_req;
   const int64_t ntiles = (L.grid_rows + a.rpw - 1) / a.rpw;
   const dim3 grid((unsigned)(ntiles * L.Hkv * L.n_req));
-  hipLaunchKernelGGL((attn_mfma_kernel<D, PAGED, PV>), grid, dim3(512), 0, s, a);
+  hipLaunchKernelGGL((attn_mfma_kernel<D, PAGED, PV, PRESCALE>), grid, dim3(512), 0, s, a);
   return hipGetLastError();
 }
 
@@ -530,15 +685,18 @@ hipError_t launch_colsum_f32(const sx_plan* p, const void* q, const void* kc, hi
 
 hipError_t launch_attn_paged(const AttnLaunch& a, hipStream_t s) {
   if (a.dtype == SX_F32) return launch_attn_f32(a, true, s);
+  // with an output and no log-sum-exp requested: pre-scaled Q; the log-sum-exp pass: exact logits
   const bool pv = a.out != nullptr;
-  if (a.D == 128) return pv ? launch_mfma<128, true, true>(a, s) : launch_mfma<128, true, false>(a, s);
-  return pv ? launch_mfma<64, true, true>(a, s) : launch_mfma<64, true, false>(a, s);
+  if (pv && a.lse != nullptr) return hipErrorInvalidValue;
+  if (a.D == 128) return pv ? launch_mfma<128, true, true, true>(a, s) : launch_mfma<128, true, false, false>(a, s);
+  return pv ? launch_mfma<64, true, true, true>(a, s) : launch_mfma<64, true, false, false>(a, s);
 }
 
 hipError_t launch_attn_dense(const AttnLaunch& a, hipStream_t s) {
   if (a.dtype == SX_F32) return launch_attn_f32(a, false, s);
-  if (a.D == 128) return launch_mfma<128, false, true>(a, s);
-  return launch_mfma<64, false, true>(a, s);
+  const bool exact = a.lse != nullptr;   // a requested log-sum-exp keeps exact logits
+  if (a.D == 128) return exact ? launch_mfma<128, false, true, false>(a, s) : launch_mfma<128, false, true, true>(a, s);
+  return exact ? launch_mfma<64, false, true, false>(a, s) : launch_mfma<64, false, true, true>(a, s);
 }
 
 hipError_t launch_colsum(const sx_plan* p, const void* q, const void* kc, hipStream_t s) {
