@@ -47,6 +47,9 @@ def parse():
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--layers", type=int, default=None, help="override the number of layers (profiling)")
+    ap.add_argument("--score-passes", type=int, choices=(1, 2), default=1,
+                    help="Sparse-Q scoring in hybrid stacks: 1 = denominators from the boundary layer's full "
+                         "attention (exact-logit variant), 2 = own log-sum-exp pass")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
                     help="also run a plain device copy of BYTES bytes (reference for HBM byte counters)")
     ap.add_argument("--record-traffic", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
@@ -56,10 +59,14 @@ def parse():
 
 
 # kernel symbol -> (entry point, source file holding it)
+# (attention template arguments: head dim, paged, P.V product, pre-scaled Q)
 KERNELS = {
-    "attn_mfma_kernel<128, true, true>": ("sx_sparse_attn", "k_attn.hip"),
-    "attn_mfma_kernel<128, false, true>": ("sx_full_attn", "k_attn.hip"),
-    "attn_mfma_kernel<128, true, false>": ("sx_sparseq_score", "k_attn.hip"),
+    "attn_mfma_kernel<128, true, true, true>": ("sx_sparse_attn", "k_attn.hip"),
+    "attn_mfma_kernel<128, false, true, true>": ("sx_full_attn", "k_attn.hip"),
+    # the boundary layer's full attention, which also writes the softmax denominators
+    "attn_mfma_kernel<128, false, true, false>": ("sx_full_attn+lse", "k_attn.hip"),
+    # two-pass scoring only (layers without a preceding full layer)
+    "attn_mfma_kernel<128, true, false, false>": ("sx_sparseq_score", "k_attn.hip"),
     "colsum_mfma_kernel<128>": ("sx_sparseq_score", "k_attn.hip"),
     "head_reduce_kernel": ("sx_sparseq_score", "k_copy.hip"),
     "realign_kernel": ("sx_rope_realign", "k_copy.hip"),
@@ -199,6 +206,7 @@ def main():
         tl["vc"] = torch.zeros(pool, dtype=dt, device="cuda")
         layers.append(tl)
     out = torch.empty((T, Hq, d), dtype=dt, device="cuda")
+    lse = torch.empty((T, Hq), dtype=torch.float32, device="cuda")   # boundary layer's denominators
     scores = torch.zeros(T, dtype=torch.float32, device="cuda")
     rows = torch.zeros(T, dtype=torch.int32, device="cuda")
     n_rows = torch.zeros(len(w.requests), dtype=torch.int32, device="cuda")
@@ -213,9 +221,12 @@ def main():
     def step():
         for l in range(nfull):
             tl = layers[l]
+            # the last full layer is the selecting (boundary) layer: with --score-passes 1 its attention
+            # also writes the softmax denominators of every row and the Sparse-Q scoring makes one pass
+            lse_l = lse if (l == nfull - 1 and args.score_passes == 1) else None
             tm.run("sx_kv_scatter", lambda: sx.kv_scatter(plan, tl["k"], tl["v"], tl["kc"], tl["vc"]))
             tm.run("sx_full_attn", lambda: sx.full_attn(desc, tl["q"], tl["k"], tl["v"], cu, len(w.requests), max_T,
-                                                        out))
+                                                        out, lse_l))
         if nfull == 0:
             # single selecting layer: mixed keys (re-aligned cached + fresh uncached)
             tl = layers[0]
@@ -225,7 +236,9 @@ def main():
             sel = tl
         else:
             sel = layers[nfull - 1]
-        tm.run("sx_sparseq_score", lambda: sx.sparseq_score(plan, sel["q"], sel["kc"], scores))
+        tm.run("sx_sparseq_score", lambda: sx.sparseq_score(plan, sel["q"], sel["kc"], scores,
+                                                            lse_in=lse if (nfull > 0 and args.score_passes == 1)
+                                                            else None))
         tm.run("sx_topk_select", lambda: sx.topk_select(plan, scores, ratio, rows, n_rows))
         for l in range(max(nfull, 0), L):
             tl = layers[l]
@@ -328,7 +341,7 @@ def main():
         "vs_baseline": None, "dtype": w.dtype, "data": "synthetic (seeded N(0,1) inputs, layout rules of the workload)",
         "config": {"workload": f"{w.name}: {w.description}", "tokens": T, "layers": L, "full_layers": nfull,
                    "ratio": ratio, "recompute_rows": n_R, "k": int(k_total), "q_heads": Hq, "kv_heads": Hkv,
-                   "head_dim": d, "requests": len(w.requests)},
+                   "head_dim": d, "requests": len(w.requests), "score_passes": args.score_passes},
         "kernels": kernels, "roofline": roof, "cpu_baseline": cpu,
     }
     print(json.dumps(res), flush=True)

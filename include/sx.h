@@ -169,9 +169,15 @@ sx_status sx_kv_scatter(const sx_plan* plan, const void* k_new, const void* v_ne
  * over the probe rows P_r = I_nr U S_tail of request r, reading keys from k_cache (whatever the
  * cache holds: re-aligned cached keys and the fresh keys written so far).  Probabilities and
  * sums are float32 per tile and float64 across tiles; the order of every sum is fixed, so the
- * result is deterministic.  Positions after the last probe get 0.  Uses plan scratch. */
-sx_status sx_sparseq_score(const sx_plan* plan, const void* q, const void* k_cache, float* scores,
-                           void* stream);
+ * result is deterministic.  Positions after the last probe get 0.  Uses plan scratch.
+ * lse_in: NULL (two passes over the keys: the softmax denominators of the probe rows, then the
+ *   column sums), or a DEVICE float32 array [sum T][Hq] of natural-log sums
+ *   log sum_{j <= i} exp(scale * q[i,h] . K[j]) over the keys k_cache holds -- exactly what
+ *   sx_full_attn writes to its lse output when the selecting layer is the last full layer of a
+ *   hybrid stack (Section 3.4), with k_cache holding that layer's keys.  Then the denominators
+ *   are taken from it (one pass); only the probe rows are read. */
+sx_status sx_sparseq_score(const sx_plan* plan, const void* q, const void* k_cache, const float* lse_in,
+                           float* scores, void* stream);
 
 /* Eq. topk, Section 3.3 and Algorithm 1 steps 14-17, per request: S_key = the k_r reused
  * positions with the largest score (k_r as in sx_plan_budget; ties go to the lower index),

@@ -11,7 +11,7 @@ Call pattern of one selecting sparse layer (all on one stream):
     rope_realign(plan, src_k, src_v, k_cache, v_cache)
     nr, n_nr, max_nr = plan.nonreused_rows()
     kv_scatter(plan, k, v, k_cache, v_cache, rows=nr, n_rows=n_nr, max_rows=max_nr)
-    sparseq_score(plan, q, k_cache, scores)
+    sparseq_score(plan, q, k_cache, scores, lse_in=None)
     topk_select(plan, scores, ratio, rows, n_rows)
     kv_scatter(plan, k, v, k_cache, v_cache, rows=rows, n_rows=n_rows, max_rows=plan.budget(ratio)[1])
     sparse_attn(plan, q, rows, n_rows, plan.budget(ratio)[1], k_cache, v_cache, out)
@@ -94,7 +94,7 @@ def lib() -> ctypes.CDLL:
         L.sx_plan_nonreused_rows.argtypes = [VP, P(VP), P(VP), P(I32)]
         L.sx_rope_realign.argtypes = [VP, VP, VP, VP, VP, VP]
         L.sx_kv_scatter.argtypes = [VP, VP, VP, VP, VP, I32, VP, VP, VP]
-        L.sx_sparseq_score.argtypes = [VP, VP, VP, VP, VP]
+        L.sx_sparseq_score.argtypes = [VP, VP, VP, VP, VP, VP]
         L.sx_topk_select.argtypes = [VP, VP, D, VP, VP, VP]
         L.sx_sparse_attn.argtypes = [VP, VP, VP, VP, I32, VP, VP, VP, VP]
         L.sx_full_attn.argtypes = [P(LayerDesc), VP, VP, VP, VP, I32, I32, VP, VP, VP]
@@ -212,8 +212,8 @@ def kv_scatter(plan: Plan, k_new, v_new, k_cache, v_cache, rows=None, n_rows=Non
                                _ptr(k_cache), _ptr(v_cache), _stream(stream)))
 
 
-def sparseq_score(plan: Plan, q, k_cache, scores, stream=None):
-    _check(lib().sx_sparseq_score(plan.handle, _ptr(q), _ptr(k_cache), _ptr(scores), _stream(stream)))
+def sparseq_score(plan: Plan, q, k_cache, scores, lse_in=None, stream=None):
+    _check(lib().sx_sparseq_score(plan.handle, _ptr(q), _ptr(k_cache), _ptr(lse_in), _ptr(scores), _stream(stream)))
 
 
 def topk_select(plan: Plan, scores, ratio: float, rows, n_rows, stream=None):

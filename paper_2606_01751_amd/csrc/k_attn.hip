@@ -338,8 +338,9 @@ __global__ __launch_bounds__(512, 1) void attn_mfma_kernel(AttnK a) {
       u.z = pack_bf16x2(x[4], x[5]);
       u.w = pack_bf16x2(x[6], x[7]);
       pb[kk] = __builtin_bit_cast(bf16x8_t, u);
-      if constexpr (PV) {
-        // l sums the bfloat16 probabilities that the P.V product uses
+      if constexpr (PV && PRESCALE) {
+        // l sums the bfloat16 probabilities that the P.V product uses (without a log-sum-exp
+        // output; with one, the float32 probabilities are summed so the output stays exact)
         const bf16x2_t one2 = __builtin_bit_cast(bf16x2_t, 0x3f803f80u);
         psum = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, u.x), one2, psum, false);
         psum = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, u.y), one2, psum, false);
@@ -473,8 +474,12 @@ __global__ __launch_bounds__(512, 1) void attn_mfma_kernel(AttnK a) {
   wait_vm((nkt > 1 ? IPW : 0) + (PV ? IPW : 0));   // K(0) has landed
   __syncthreads();
   auto matrix_phase = [&](int j) {
+    // the wave in its matrix phase issues first: its MFMAs are not held back by the other
+    // wave's softmax on the same SIMD
+    __builtin_amdgcn_s_setprio(2);
     if (j >= 1 && (j - 1) * KT <= wave_max) pv_tile(vtile(j - 1));
     if (j < nkt && j * KT <= wave_max) s_tile(ktile(j));
+    __builtin_amdgcn_s_setprio(0);
   };
   auto transfer_phase = [&](int j) {   // this wave's share of K(j+2) and V(j+1)
     if (j + 2 < nkt) issue(a.k, k_last, j + 2, ktile(j + 2), false);
@@ -551,6 +556,7 @@ struct ColsumK {
   int64_t total;
   int Hq, Hkv, G, n_req;
   float scale_log2;
+  int lse_tok;   // 0: base-2 sums indexed by probe; 1: natural-log sums indexed by token
 };
 
 template <int D>
@@ -600,29 +606,49 @@ __global__ __launch_bounds__(256, 2) void colsum_mfma_kernel(ColsumK a) {
     acc32[e] = 0.f;
   }
   int pending = 0;
-  for (int c0 = lo * a.G; c0 < ncols; c0 += 32) {
-    const int c = c0 + l32;
+  // Column chunks of 32 are software-pipelined: the Q rows and denominators of the next chunk and
+  // the probe positions of the one after are loaded while the current chunk is computed.
+  auto col_pos = [&](int cc) -> int {
+    const int c = cc + l32;
+    return c < ncols ? probe[c / a.G] : -1;
+  };
+  auto load_chunk = [&](int cc, int pos, bf16x8_t (&qv)[D / 16], float& lse2) {
+    const int c = cc + l32;
     const bool valid = c < ncols;
     const int pidx = valid ? c / a.G : 0;
     const int h = valid ? c - pidx * a.G : 0;
-    const int pos = valid ? probe[pidx] : -1;
-    const float lse2 = valid ? a.lse[(int64_t)(rq.tok_off + pidx) * a.Hq + kvh * a.G + h] : INFINITY;
-    const uint16_t* qp = a.q + ((int64_t)(rq.tok_off + (valid ? pos : 0)) * a.Hq + kvh * a.G + h) * D + hg * 8;
-    f32x16_t s = {};
+    const int qh = kvh * a.G + h;
+    lse2 = !valid ? INFINITY
+                  : a.lse_tok ? a.lse[(int64_t)(rq.tok_off + pos) * a.Hq + qh] * 1.4426950408889634f
+                              : a.lse[(int64_t)(rq.tok_off + pidx) * a.Hq + qh];
+    const uint16_t* qp = a.q + ((int64_t)(rq.tok_off + (valid ? pos : 0)) * a.Hq + qh) * D + hg * 8;
 #pragma unroll
     for (int st = 0; st < D / 16; ++st) {
       uint4 v = valid ? *(const uint4*)(qp + 16 * st) : make_uint4(0, 0, 0, 0);
-      s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka[st], __builtin_bit_cast(bf16x8_t, v), s, 0, 0, 0);
+      qv[st] = __builtin_bit_cast(bf16x8_t, v);
     }
-    // the chunk's first column has the smallest row; no mask when it sees all 32 keys
-    const int first_pos = probe[c0 / a.G];
+  };
+  int c0 = lo * a.G;
+  int pos_cur = col_pos(c0);
+  int pos_nxt = col_pos(c0 + 32);
+  bf16x8_t qcur[D / 16], qnxt[D / 16];
+  float lse_cur = INFINITY, lse_nxt = INFINITY;
+  if (c0 < ncols) load_chunk(c0, pos_cur, qcur, lse_cur);
+  for (; c0 < ncols; c0 += 32) {
+    const int pos_nn = col_pos(c0 + 64);
+    if (c0 + 32 < ncols) load_chunk(c0 + 32, pos_nxt, qnxt, lse_nxt);
+    f32x16_t s = {};
+#pragma unroll
+    for (int st = 0; st < D / 16; ++st) s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka[st], qcur[st], s, 0, 0, 0);
+    // the chunk's first column (lane 0's) has the smallest row; no mask when it sees all 32 keys
+    const int first_pos = __builtin_amdgcn_readfirstlane(pos_cur);
     const bool need_mask = first_pos < jw + 31;
 #pragma unroll
     for (int e = 0; e < 16; ++e) {
-      float p = __builtin_amdgcn_exp2f(s[e] * a.scale_log2 - lse2);
+      float p = __builtin_amdgcn_exp2f(s[e] * a.scale_log2 - lse_cur);
       if (need_mask) {
         const int key = jw + (e >> 2) * 8 + hg * 4 + (e & 3);
-        p = key <= pos ? p : 0.f;
+        p = key <= pos_cur ? p : 0.f;
       }
       acc32[e] += p;
     }
@@ -634,6 +660,11 @@ __global__ __launch_bounds__(256, 2) void colsum_mfma_kernel(ColsumK a) {
       }
       pending = 0;
     }
+#pragma unroll
+    for (int st = 0; st < D / 16; ++st) qcur[st] = qnxt[st];
+    lse_cur = lse_nxt;
+    pos_cur = pos_nxt;
+    pos_nxt = pos_nn;
   }
 #pragma unroll
   for (int e = 0; e < 16; ++e) acc64[e] += (double)acc32[e];
@@ -681,7 +712,8 @@ hipError_t launch_mfma(const AttnLaunch& L, hipStream_t s) {
 
 // float32 variants (vector ALU), defined in k_attn_f32.hip
 hipError_t launch_attn_f32(const AttnLaunch& a, bool paged, hipStream_t s);
-hipError_t launch_colsum_f32(const sx_plan* p, const void* q, const void* kc, hipStream_t s);
+hipError_t launch_colsum_f32(const sx_plan* p, const void* q, const void* kc, const float* lse, int lse_tok,
+                             hipStream_t s);
 
 hipError_t launch_attn_paged(const AttnLaunch& a, hipStream_t s) {
   if (a.dtype == SX_F32) return launch_attn_f32(a, true, s);
@@ -699,12 +731,14 @@ hipError_t launch_attn_dense(const AttnLaunch& a, hipStream_t s) {
   return exact ? launch_mfma<64, false, true, false>(a, s) : launch_mfma<64, false, true, true>(a, s);
 }
 
-hipError_t launch_colsum(const sx_plan* p, const void* q, const void* kc, hipStream_t s) {
-  if (p->desc.dtype == SX_F32) return launch_colsum_f32(p, q, kc, s);
+hipError_t launch_colsum(const sx_plan* p, const void* q, const void* kc, const float* lse, int lse_tok,
+                         hipStream_t s) {
+  if (p->desc.dtype == SX_F32) return launch_colsum_f32(p, q, kc, lse, lse_tok, s);
   ColsumK a{};
   a.q = (const uint16_t*)q;
   a.k = (const uint16_t*)kc;
-  a.lse = p->d_lse;
+  a.lse = lse;
+  a.lse_tok = lse_tok;
   a.reqs = p->d_req;
   a.bt = p->d_bt;
   a.probe = p->d_probe;

@@ -132,6 +132,7 @@ struct ColsumF {
   int64_t total;
   int Hq, Hkv, G;
   float scale;
+  int lse_tok;   // 0: lse indexed by probe; 1: indexed by token position
 };
 
 template <int D>
@@ -166,7 +167,7 @@ __global__ __launch_bounds__(256) void colsum_f32_kernel(ColsumF a) {
 #pragma unroll 8
       for (int x = 0; x < D; ++x) z = fmaf(qp[x], kr[x], z);
       z *= a.scale;
-      const float pr = expf(z - a.lse[(int64_t)(rq.tok_off + p) * a.Hq + qh]);
+      const float pr = expf(z - a.lse[(int64_t)(rq.tok_off + (a.lse_tok ? pos : p)) * a.Hq + qh]);
       if (valid && j <= pos) acc += (double)pr;
     }
   }
@@ -206,11 +207,13 @@ hipError_t launch_attn_f32(const AttnLaunch& L, bool paged, hipStream_t s) {
   return hipGetLastError();
 }
 
-hipError_t launch_colsum_f32(const sx_plan* p, const void* q, const void* kc, hipStream_t s) {
+hipError_t launch_colsum_f32(const sx_plan* p, const void* q, const void* kc, const float* lse, int lse_tok,
+                             hipStream_t s) {
   ColsumF a{};
   a.q = (const float*)q;
   a.k = (const float*)kc;
-  a.lse = p->d_lse;
+  a.lse = lse;
+  a.lse_tok = lse_tok;
   a.reqs = p->d_req;
   a.bt = p->d_bt;
   a.probe = p->d_probe;

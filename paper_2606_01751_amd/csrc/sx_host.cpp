@@ -357,10 +357,17 @@ sx_status sx_kv_scatter(const sx_plan* p, const void* k_new, const void* v_new, 
                       "sx_kv_scatter launch");
 }
 
-sx_status sx_sparseq_score(const sx_plan* p, const void* q, const void* k_cache, float* scores, void* stream) {
+sx_status sx_sparseq_score(const sx_plan* p, const void* q, const void* k_cache, const float* lse_in, float* scores,
+                           void* stream) {
   if (!p) return fail(SX_EINVAL, "plan is NULL");
   if (!q || !k_cache || !scores) return fail(SX_EINVAL, "NULL tensor argument");
   hipStream_t s = (hipStream_t)stream;
+  if (lse_in) {
+    // one pass: the denominators come from the caller (natural log, indexed by token)
+    sx_status st = check_launch(sx::launch_colsum(p, q, k_cache, lse_in, 1, s), "sx_sparseq_score column-sum launch");
+    if (st != SX_OK) return st;
+    return check_launch(sx::launch_head_reduce(p, scores, s), "sx_sparseq_score head-sum launch");
+  }
   // pass 1: log-sum-exp of every (probe row, query head)
   sx::AttnLaunch a{};
   a.Hq = p->desc.n_q_heads;
@@ -386,7 +393,7 @@ sx_status sx_sparseq_score(const sx_plan* p, const void* q, const void* k_cache,
     if (st != SX_OK) return st;
   }
   // pass 2: per-key column sums of the probabilities, per KV head
-  st = check_launch(sx::launch_colsum(p, q, k_cache, s), "sx_sparseq_score pass 2 launch");
+  st = check_launch(sx::launch_colsum(p, q, k_cache, p->d_lse, 0, s), "sx_sparseq_score pass 2 launch");
   if (st != SX_OK) return st;
   // pass 3: fixed-order sum over KV heads
   return check_launch(sx::launch_head_reduce(p, scores, s), "sx_sparseq_score pass 3 launch");

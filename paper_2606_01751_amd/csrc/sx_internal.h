@@ -102,6 +102,9 @@ struct AttnLaunch {
 };
 hipError_t launch_attn_paged(const AttnLaunch& a, hipStream_t s);   // rows over a paged cache
 hipError_t launch_attn_dense(const AttnLaunch& a, hipStream_t s);   // all rows, dense K/V
-hipError_t launch_colsum(const sx_plan* p, const void* q, const void* kc, hipStream_t s);
+// column sums of the Sparse-Q probabilities; lse: base-2 sums indexed by probe (lse_tok = 0, the
+// plan's pass-1 scratch) or natural-log sums indexed by token (lse_tok = 1, a caller's input)
+hipError_t launch_colsum(const sx_plan* p, const void* q, const void* kc, const float* lse, int lse_tok,
+                         hipStream_t s);
 
 }  // namespace sx

@@ -102,7 +102,7 @@ def test_null_arguments_are_rejected():
     L = sx.lib()
     assert L.sx_plan_create(None, None, 0, 1, 1, None) == sx.SX_EINVAL
     assert L.sx_rope_realign(None, None, None, None, None, None) == sx.SX_EINVAL
-    assert L.sx_sparseq_score(None, None, None, None, None) == sx.SX_EINVAL
+    assert L.sx_sparseq_score(None, None, None, None, None, None) == sx.SX_EINVAL
     assert L.sx_topk_select(None, None, 0.5, None, None, None) == sx.SX_EINVAL
     assert L.sx_sparse_attn(None, None, None, None, 1, None, None, None, None) == sx.SX_EINVAL
     assert L.sx_kv_scatter(None, None, None, None, None, 1, None, None, None) == sx.SX_EINVAL

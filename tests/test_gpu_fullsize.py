@@ -1,7 +1,7 @@
 """Parity at the full sizes of the named workloads, in the launch configuration the benchmark uses.
 
-* c3 (32768 tokens, 32/8/128): the boundary full layer, the selection on it and the first sparse
-  layer.  Scores and recompute sets are compared with the oracle's (stored by
+* c3 (32768 tokens, 32/8/128): the boundary full layer (its attention also yields the softmax
+  denominators that the one-pass scoring uses), the selection on it and the first sparse layer.  Scores and recompute sets are compared with the oracle's (stored by
   tests/golden/make_golden.py from the same seeded inputs); attention on sampled rows (every
   output row depends only on its own query row and the cache, so each sampled row is an exact
   check).
@@ -81,9 +81,10 @@ def test_c3_boundary_selection_and_layers():
     scores = torch.zeros(T, dtype=torch.float32, device="cuda")
     rows = torch.zeros(T, dtype=torch.int32, device="cuda")
     n_rows = torch.zeros(1, dtype=torch.int32, device="cuda")
+    lse = torch.zeros((T, w.n_q_heads), dtype=torch.float32, device="cuda")
     sx.kv_scatter(plan, k, v, kc, vc)
-    sx.full_attn(desc_of(w), q, k, v, cu, 1, T, out)
-    sx.sparseq_score(plan, q, kc, scores)
+    sx.full_attn(desc_of(w), q, k, v, cu, 1, T, out, lse)
+    sx.sparseq_score(plan, q, kc, scores, lse_in=lse)     # one pass: the boundary layer's denominators
     sx.topk_select(plan, scores, ratio, rows, n_rows)
     torch.cuda.synchronize()
     gs = host(scores).astype(np.float64)

@@ -271,3 +271,40 @@ def test_config2_layer_matches_oracle():
     err = np.abs(host(g.out)[sample] - ref).max()
     log(f"[c2] attention max-abs on {len(sample)} rows {err:.3g}")
     assert err <= 2e-2
+
+
+@pytest.mark.parametrize("name,w", CASES, ids=IDS)
+def test_one_pass_scores_from_full_attention_lse(name, w):
+    """Hybrid boundary (Section 3.4): the cache holds the layer's fresh keys of every token and the
+    full-attention pass supplies the natural-log denominators; the one-pass scores must match the
+    oracle's scores of the same keys and the two-pass scores."""
+    log(f"[one-pass] {name}")
+    t = W.layer_tensors(w, 0)
+    g = GpuLayer(w, t)
+    offs = w.token_offsets
+    sx.kv_scatter(g.plan, g.t["k"], g.t["v"], g.k_cache, g.v_cache)
+    cu = torch.tensor(offs, dtype=torch.int32, device="cuda")
+    out = torch.zeros_like(g.t["q"])
+    lse = torch.zeros((w.total_tokens, w.n_q_heads), dtype=torch.float32, device="cuda")
+    sx.full_attn(desc_of(w), g.t["q"], g.t["k"], g.t["v"], cu, len(w.requests), max(r.n_tokens for r in w.requests),
+                 out, lse)
+    one = torch.zeros(w.total_tokens, dtype=torch.float32, device="cuda")
+    two = torch.zeros(w.total_tokens, dtype=torch.float32, device="cuda")
+    sx.sparseq_score(g.plan, g.t["q"], g.k_cache, one, lse_in=lse)
+    sx.sparseq_score(g.plan, g.t["q"], g.k_cache, two)
+    torch.cuda.synchronize()
+    s1, s2 = host(one).astype(np.float64), host(two).astype(np.float64)
+    scale = O.softmax_scale(w.head_dim)
+    worst = 0.0
+    for r, req in enumerate(w.requests):
+        sl = slice(offs[r], offs[r + 1])
+        P = O.probe_positions(req.n_tokens, req.segments)
+        s_o = O.sparseq_scores(t["q"][sl], t["k"][sl], P, scale)
+        big = s_o >= 1e-3 * s_o.max()
+        rel = (np.abs(s1[sl] - s_o)[big] / s_o[big]).max()
+        worst = max(worst, rel)
+        assert np.all(s1[sl][s_o == 0] == 0)
+        assert rel < 1e-4, rel
+        rel12 = (np.abs(s1[sl] - s2[sl])[big] / s_o[big]).max()
+        assert rel12 < 2e-5, rel12
+    log(f"  one-pass score rel err {worst:.3g}")
