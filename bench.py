@@ -59,14 +59,12 @@ def parse():
 
 
 # kernel symbol -> (entry point, source file holding it)
-# (attention template arguments: head dim, paged, P.V product, pre-scaled Q)
+# (attention template arguments: head dim, paged, P.V product)
 KERNELS = {
-    "attn_mfma_kernel<128, true, true, true>": ("sx_sparse_attn", "k_attn.hip"),
-    "attn_mfma_kernel<128, false, true, true>": ("sx_full_attn", "k_attn.hip"),
-    # the boundary layer's full attention, which also writes the softmax denominators
-    "attn_mfma_kernel<128, false, true, false>": ("sx_full_attn+lse", "k_attn.hip"),
+    "attn_mfma_kernel<128, true, true>": ("sx_sparse_attn", "k_attn.hip"),
+    "attn_mfma_kernel<128, false, true>": ("sx_full_attn", "k_attn.hip"),
     # two-pass scoring only (layers without a preceding full layer)
-    "attn_mfma_kernel<128, true, false, false>": ("sx_sparseq_score", "k_attn.hip"),
+    "attn_mfma_kernel<128, true, false>": ("sx_sparseq_score", "k_attn.hip"),
     "colsum_mfma_kernel<128>": ("sx_sparseq_score", "k_attn.hip"),
     "head_reduce_kernel": ("sx_sparseq_score", "k_copy.hip"),
     "realign_kernel": ("sx_rope_realign", "k_copy.hip"),

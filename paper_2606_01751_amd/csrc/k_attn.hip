@@ -80,7 +80,7 @@ __device__ __forceinline__ void sched_pipelined() {
   SX_SG(kSgMfma, PRE);
 }
 
-template <int D, bool PAGED, bool PV, bool PRESCALE>
+template <int D, bool PAGED, bool PV>
 __global__ __launch_bounds__(512, 1) void attn_mfma_kernel(AttnK a) {
   constexpr int NW = 8;                       // waves: two groups of 4
   constexpr int ROWB = D * 2;                 // bytes of one key row
@@ -89,13 +89,6 @@ __global__ __launch_bounds__(512, 1) void attn_mfma_kernel(AttnK a) {
   constexpr int RPK = 1024 / ROWB;            // rows per 1 KB transfer instruction
   constexpr int IPW = TILEB / 1024 / NW;      // transfer instructions per wave per matrix
   static_assert(IPW * RPK == 8, "a wave moves 8 consecutive rows of every tile");
-  // PRESCALE (attention output without log-sum-exp): the scores are formed in the log2 domain by
-  // the MFMA itself: Q is multiplied by scale * log2(e) when it is loaded (and rounded to
-  // bfloat16) and the S^T accumulator starts at -m_run, so it holds c2 s - m_run and p = 2^(S^T).
-  // Otherwise (the log-sum-exp pass of Sparse-Q scoring, or a requested log-sum-exp output) Q is
-  // exact and the scale is applied in float32, because the column sums reuse that result with
-  // exact logits.
-  static_assert(PV || !PRESCALE, "the log-sum-exp pass keeps exact logits");
   // LDS: three buffers each of K and V tiles (tile t in buffer t mod 3), rows row-major; chunk c of
   // row r of K sits at chunk c ^ (r mod NCH) (conflict-free 16-byte row reads), of V at
   // c ^ v_swz(r) (conflict-free transposed 8-byte reads).
@@ -155,13 +148,6 @@ __global__ __launch_bounds__(512, 1) void attn_mfma_kernel(AttnK a) {
 #pragma unroll
     for (int s = 0; s < D / 16; ++s) {
       uint4 v = valid ? *(const uint4*)(qp + 16 * s) : make_uint4(0, 0, 0, 0);
-      if constexpr (PRESCALE) {
-        uint32_t u[4] = {v.x, v.y, v.z, v.w};
-#pragma unroll
-        for (int i = 0; i < 4; ++i)
-          u[i] = pack_bf16x2(__uint_as_float(u[i] << 16) * c2, __uint_as_float(u[i] & 0xffff0000u) * c2);
-        v = make_uint4(u[0], u[1], u[2], u[3]);
-      }
       qb[s] = __builtin_bit_cast(bf16x8_t, v);
     }
   }
@@ -187,9 +173,8 @@ __global__ __launch_bounds__(512, 1) void attn_mfma_kernel(AttnK a) {
   for (int i = 0; i < (PV ? D / 32 : 1); ++i)
 #pragma unroll
     for (int e = 0; e < 16; ++e) o[i][e] = 0.f;
-  // Running max (log2 domain).  With PRESCALE it starts as a placeholder 0 that the first tile
-  // replaces; otherwise columns without a row start at 0 so their (unused) sums stay finite.
-  float m_run = PRESCALE ? 0.f : (valid ? -INFINITY : 0.f);
+  // running max (log2 domain); columns without a row start at 0 so their (unused) sums stay finite
+  float m_run = valid ? -INFINITY : 0.f;
   float l_run = 0.f;
 
   // ---- global -> LDS tile transfers (16 bytes per lane, all 8 waves share each tile).
@@ -287,12 +272,10 @@ __global__ __launch_bounds__(512, 1) void attn_mfma_kernel(AttnK a) {
   // S^T = K Q^T for the 64 keys of a tile (two 32-key M tiles)
   f32x16_t sacc[2];
   auto s_body = [&](const char* Kb) {
-    // accumulator start: -m_run in every slot (PRESCALE), else 0
-    const float init = PRESCALE ? -m_run : 0.f;
 #pragma unroll
     for (int mt = 0; mt < 2; ++mt)
 #pragma unroll
-      for (int e = 0; e < 16; ++e) sacc[mt][e] = init;
+      for (int e = 0; e < 16; ++e) sacc[mt][e] = 0.f;
 #pragma unroll
     for (int s = 0; s < D / 16; ++s) {
 #pragma unroll
@@ -338,18 +321,9 @@ __global__ __launch_bounds__(512, 1) void attn_mfma_kernel(AttnK a) {
       u.z = pack_bf16x2(x[4], x[5]);
       u.w = pack_bf16x2(x[6], x[7]);
       pb[kk] = __builtin_bit_cast(bf16x8_t, u);
-      if constexpr (PV && PRESCALE) {
-        // l sums the bfloat16 probabilities that the P.V product uses (without a log-sum-exp
-        // output; with one, the float32 probabilities are summed so the output stays exact)
-        const bf16x2_t one2 = __builtin_bit_cast(bf16x2_t, 0x3f803f80u);
-        psum = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, u.x), one2, psum, false);
-        psum = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, u.y), one2, psum, false);
-        psum = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, u.z), one2, psum, false);
-        psum = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, u.w), one2, psum, false);
-      } else {
+      // l sums the float32 probabilities (exact denominators, also for the log-sum-exp output)
 #pragma unroll
-        for (int t = 0; t < 8; ++t) psum += x[t];
-      }
+      for (int t = 0; t < 8; ++t) psum += x[t];
     };
     auto tile_max = [&]() {
       float mx = sacc[0][0];
@@ -368,53 +342,24 @@ __global__ __launch_bounds__(512, 1) void attn_mfma_kernel(AttnK a) {
           for (int e = 0; e < 16; ++e) o[dt][e] *= alpha;
       }
     };
-    if constexpr (PRESCALE) {
-      // sacc = c2 s - m_run
-      const bool first = kbase == 0;
-      if (!first) {
+    // p = 2^(c2 s - m_run)
+    auto expo = [&](float mneg) {
+      psum = 0.f;
 #pragma unroll
-        for (int kk = 0; kk < 4; ++kk) {
-          float x[8];
+      for (int kk = 0; kk < 4; ++kk) {
+        float x[8];
 #pragma unroll
-          for (int t = 0; t < 8; ++t) x[t] = __builtin_amdgcn_exp2f(sacc[kk >> 1][(kk & 1) * 8 + t]);
-          emit(kk, x);
-        }
+        for (int t = 0; t < 8; ++t)
+          x[t] = __builtin_amdgcn_exp2f(__builtin_fmaf(sacc[kk >> 1][(kk & 1) * 8 + t], c2, mneg));
+        emit(kk, x);
       }
-      if (first || __ballot(!(psum < 0x1p64f))) {
-        // raise m_run by the tile's excess (on the first tile: replace the placeholder)
-        const float mx = tile_max();
-        const float sh = mx == -INFINITY ? 0.f : (first ? mx : fmaxf(mx, 0.f));
-        if (!first) rescale(__builtin_amdgcn_exp2f(-sh));
-        m_run += sh;
-        psum = 0.f;
-#pragma unroll
-        for (int kk = 0; kk < 4; ++kk) {
-          float x[8];
-#pragma unroll
-          for (int t = 0; t < 8; ++t) x[t] = __builtin_amdgcn_exp2f(sacc[kk >> 1][(kk & 1) * 8 + t] - sh);
-          emit(kk, x);
-        }
-      }
-    } else {
-      // sacc = s; p = 2^(c2 s - m_run)
-      auto expo = [&](float mneg) {
-        psum = 0.f;
-#pragma unroll
-        for (int kk = 0; kk < 4; ++kk) {
-          float x[8];
-#pragma unroll
-          for (int t = 0; t < 8; ++t)
-            x[t] = __builtin_amdgcn_exp2f(__builtin_fmaf(sacc[kk >> 1][(kk & 1) * 8 + t], c2, mneg));
-          emit(kk, x);
-        }
-      };
-      expo(-m_run);
-      if (__ballot(!(psum < 0x1p64f))) {
-        const float m_new = fmaxf(m_run, tile_max() * c2);          // c2 > 0
-        rescale(m_new == -INFINITY ? 1.f : __builtin_amdgcn_exp2f(m_run - m_new));
-        m_run = m_new;
-        expo(m_new == -INFINITY ? 0.f : -m_new);
-      }
+    };
+    expo(-m_run);
+    if (__ballot(!(psum < 0x1p64f))) {
+      const float m_new = fmaxf(m_run, tile_max() * c2);          // c2 > 0
+      rescale(m_new == -INFINITY ? 1.f : __builtin_amdgcn_exp2f(m_run - m_new));
+      m_run = m_new;
+      expo(m_new == -INFINITY ? 0.f : -m_new);
     }
     l_run += psum;
   };
@@ -682,7 +627,7 @@ __global__ __launch_bounds__(256, 2) void colsum_mfma_kernel(ColsumK a) {
   }
 }
 
-template <int D, bool PAGED, bool PV, bool PRESCALE>
+template <int D, bool PAGED, bool PV>
 hipError_t launch_mfma(const AttnLaunch& L, hipStream_t s) {
   AttnK a{};
   a.q = (const uint16_t*)L.q;
@@ -704,7 +649,7 @@ hipError_t launch_mfma(const AttnLaunch& L, hipStream_t s) {
   a.n_req = L.n_req;
   const int64_t ntiles = (L.grid_rows + a.rpw - 1) / a.rpw;
   const dim3 grid((unsigned)(ntiles * L.Hkv * L.n_req));
-  hipLaunchKernelGGL((attn_mfma_kernel<D, PAGED, PV, PRESCALE>), grid, dim3(512), 0, s, a);
+  hipLaunchKernelGGL((attn_mfma_kernel<D, PAGED, PV>), grid, dim3(512), 0, s, a);
   return hipGetLastError();
 }
 
@@ -717,18 +662,16 @@ hipError_t launch_colsum_f32(const sx_plan* p, const void* q, const void* kc, co
 
 hipError_t launch_attn_paged(const AttnLaunch& a, hipStream_t s) {
   if (a.dtype == SX_F32) return launch_attn_f32(a, true, s);
-  // with an output and no log-sum-exp requested: pre-scaled Q; the log-sum-exp pass: exact logits
   const bool pv = a.out != nullptr;
   if (pv && a.lse != nullptr) return hipErrorInvalidValue;
-  if (a.D == 128) return pv ? launch_mfma<128, true, true, true>(a, s) : launch_mfma<128, true, false, false>(a, s);
-  return pv ? launch_mfma<64, true, true, true>(a, s) : launch_mfma<64, true, false, false>(a, s);
+  if (a.D == 128) return pv ? launch_mfma<128, true, true>(a, s) : launch_mfma<128, true, false>(a, s);
+  return pv ? launch_mfma<64, true, true>(a, s) : launch_mfma<64, true, false>(a, s);
 }
 
 hipError_t launch_attn_dense(const AttnLaunch& a, hipStream_t s) {
   if (a.dtype == SX_F32) return launch_attn_f32(a, false, s);
-  const bool exact = a.lse != nullptr;   // a requested log-sum-exp keeps exact logits
-  if (a.D == 128) return exact ? launch_mfma<128, false, true, false>(a, s) : launch_mfma<128, false, true, true>(a, s);
-  return exact ? launch_mfma<64, false, true, false>(a, s) : launch_mfma<64, false, true, true>(a, s);
+  if (a.D == 128) return launch_mfma<128, false, true>(a, s);
+  return launch_mfma<64, false, true>(a, s);
 }
 
 hipError_t launch_colsum(const sx_plan* p, const void* q, const void* kc, const float* lse, int lse_tok,
