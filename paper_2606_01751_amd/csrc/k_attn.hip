@@ -485,11 +485,13 @@ __global__ __launch_bounds__(512, 1) void attn_mfma_kernel(AttnK a) {
   }
 }
 
-// Sparse-Q column sums, key-stationary: each wave owns 32 keys of one KV head (K^T held in
-// registers as the A operand) and streams the probe columns (probe row, query head) 32 at a time:
-// S^T = K Q^T, p = 2^(scale*log2e*s - lse2) masked causally, summed per key.  Per-lane partial
-// sums are float32 over 8 column chunks and float64 beyond; the cross-lane sum at the end has a
-// fixed order, so the result is deterministic.
+// Sparse-Q column sums, key-stationary: a workgroup owns 256 keys of one KV head (8 waves x 32; a
+// wave holds K^T of its keys as the MFMA A operand) and streams the probe columns (probe row,
+// query head of the group) 32 at a time: S^T = K Q^T, p = 2^(scale*log2e*s - lse2) masked
+// causally, summed per key.  The Q rows of a chunk are loaded once per workgroup and staged in
+// LDS (double-buffered; loads issued two chunks ahead).  Per-lane partial sums are float32 over
+// 8 chunks and float64 beyond; the cross-lane sum at the end has a fixed order, so the result is
+// deterministic.
 struct ColsumK {
   const uint16_t* q;
   const uint16_t* k;
@@ -504,8 +506,15 @@ struct ColsumK {
   int lse_tok;   // 0: base-2 sums indexed by probe; 1: natural-log sums indexed by token
 };
 
+constexpr int CS_KEYS = 256;   // keys per column-sum workgroup (8 waves x 32)
+
 template <int D>
-__global__ __launch_bounds__(256, 2) void colsum_mfma_kernel(ColsumK a) {
+__global__ __launch_bounds__(512, 1) void colsum_mfma_kernel(ColsumK a) {
+  constexpr int ROWB = D * 2;                 // bytes of one Q row
+  constexpr int NCH = ROWB / 16;              // 16-byte chunks per row
+  constexpr int CPI = 64 / NCH;               // columns per 1 KB load of one wave
+  constexpr int NLD = 32 / CPI;               // waves that load a 32-column chunk
+  __shared__ __attribute__((aligned(1024))) char qs[2][32 * ROWB];
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int w = tid >> 6;
@@ -516,7 +525,7 @@ __global__ __launch_bounds__(256, 2) void colsum_mfma_kernel(ColsumK a) {
   const int rest = (int)(blockIdx.x / (unsigned)a.Hkv);
   const ReqDev rq = a.reqs[rest % a.n_req];
   const int T = rq.T;
-  const int j0 = (rest / a.n_req) * 128;
+  const int j0 = (rest / a.n_req) * CS_KEYS;
   if (j0 >= T) return;
   const int jw = j0 + w * 32;
   // K rows of the wave's 32 keys as the A operand
@@ -540,9 +549,45 @@ __global__ __launch_bounds__(256, 2) void colsum_mfma_kernel(ColsumK a) {
   int lo = 0, hi = np;
   while (lo < hi) {
     const int mid = (lo + hi) >> 1;
-    if (probe[mid] < jw) lo = mid + 1; else hi = mid;
+    if (probe[mid] < j0) lo = mid + 1; else hi = mid;
   }
   const int ncols = np * a.G;
+  const int c_start = lo * a.G;
+  const int nch = (ncols - c_start + 31) / 32;
+  // loading lanes (waves < NLD): column c_start + 32 k + CPI w + lane / NCH, chunk lane % NCH;
+  // the chunk is stored at (column, chunk ^ (column mod NCH)) so the B-operand reads are
+  // conflict-free
+  const bool loader = w < NLD;
+  const int lcol = CPI * w + lane / NCH;
+  const int lpc = lane % NCH;
+  auto ld_pos = [&](int k) -> int {
+    const int c = c_start + 32 * k + lcol;
+    return (loader && c < ncols) ? probe[c / a.G] : -1;
+  };
+  auto ld_q = [&](int k, int pos) -> uint4 {
+    const int c = c_start + 32 * k + lcol;
+    if (!loader || c >= ncols) return make_uint4(0, 0, 0, 0);
+    const int h = c % a.G;
+    const int lc = lpc ^ (lcol & (NCH - 1));   // logical chunk stored at this lane's slot
+    return *(const uint4*)(a.q + ((int64_t)(rq.tok_off + pos) * a.Hq + kvh * a.G + h) * D + lc * 8);
+  };
+  auto st_q = [&](int k, uint4 v) {
+    if (loader) *(uint4*)(qs[k & 1] + lcol * ROWB + lpc * 16) = v;
+  };
+  // computing lanes: column c_start + 32 k + l32 (position, denominator)
+  auto cm_pos = [&](int k) -> int {
+    const int c = c_start + 32 * k + l32;
+    return c < ncols ? probe[c / a.G] : -1;
+  };
+  auto cm_lse = [&](int k, int pos) -> float {
+    const int c = c_start + 32 * k + l32;
+    if (c >= ncols) return INFINITY;
+    const int pidx = c / a.G;
+    const int qh = kvh * a.G + (c - pidx * a.G);
+    return a.lse_tok ? a.lse[(int64_t)(rq.tok_off + pos) * a.Hq + qh] * 1.4426950408889634f
+                     : a.lse[(int64_t)(rq.tok_off + pidx) * a.Hq + qh];
+  };
+
   double acc64[16];
   float acc32[16];
 #pragma unroll
@@ -551,49 +596,41 @@ __global__ __launch_bounds__(256, 2) void colsum_mfma_kernel(ColsumK a) {
     acc32[e] = 0.f;
   }
   int pending = 0;
-  // Column chunks of 32 are software-pipelined: the Q rows and denominators of the next chunk and
-  // the probe positions of the one after are loaded while the current chunk is computed.
-  auto col_pos = [&](int cc) -> int {
-    const int c = cc + l32;
-    return c < ncols ? probe[c / a.G] : -1;
-  };
-  auto load_chunk = [&](int cc, int pos, bf16x8_t (&qv)[D / 16], float& lse2) {
-    const int c = cc + l32;
-    const bool valid = c < ncols;
-    const int pidx = valid ? c / a.G : 0;
-    const int h = valid ? c - pidx * a.G : 0;
-    const int qh = kvh * a.G + h;
-    lse2 = !valid ? INFINITY
-                  : a.lse_tok ? a.lse[(int64_t)(rq.tok_off + pos) * a.Hq + qh] * 1.4426950408889634f
-                              : a.lse[(int64_t)(rq.tok_off + pidx) * a.Hq + qh];
-    const uint16_t* qp = a.q + ((int64_t)(rq.tok_off + (valid ? pos : 0)) * a.Hq + qh) * D + hg * 8;
-#pragma unroll
-    for (int st = 0; st < D / 16; ++st) {
-      uint4 v = valid ? *(const uint4*)(qp + 16 * st) : make_uint4(0, 0, 0, 0);
-      qv[st] = __builtin_bit_cast(bf16x8_t, v);
-    }
-  };
-  int c0 = lo * a.G;
-  int pos_cur = col_pos(c0);
-  int pos_nxt = col_pos(c0 + 32);
-  bf16x8_t qcur[D / 16], qnxt[D / 16];
-  float lse_cur = INFINITY, lse_nxt = INFINITY;
-  if (c0 < ncols) load_chunk(c0, pos_cur, qcur, lse_cur);
-  for (; c0 < ncols; c0 += 32) {
-    const int pos_nn = col_pos(c0 + 64);
-    if (c0 + 32 < ncols) load_chunk(c0 + 32, pos_nxt, qnxt, lse_nxt);
+  // prologue: chunk 0 in LDS, chunk 1 in registers, positions of chunk 2 on the way
+  int pl1 = ld_pos(1);
+  uint4 q0 = ld_q(0, ld_pos(0));
+  uint4 q1 = ld_q(1, pl1);
+  int pl2 = ld_pos(2);
+  int pc0 = cm_pos(0);
+  float lc0 = cm_lse(0, pc0);
+  int pc1 = cm_pos(1);
+  st_q(0, q0);
+  __syncthreads();
+  for (int k = 0; k < nch; ++k) {
+    // chunk k+1 into the other buffer (last read in iteration k-1); loads for chunk k+2
+    st_q(k + 1, q1);
+    q1 = ld_q(k + 2, pl2);
+    pl2 = ld_pos(k + 3);
+    const float lc1 = cm_lse(k + 1, pc1);
+    const int pc2 = cm_pos(k + 2);
+    // S^T of chunk k
+    const char* qb = qs[k & 1];
     f32x16_t s = {};
 #pragma unroll
-    for (int st = 0; st < D / 16; ++st) s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka[st], qcur[st], s, 0, 0, 0);
+    for (int st = 0; st < D / 16; ++st) {
+      const int c = 2 * st + hg;
+      const bf16x8_t b = *(const bf16x8_t*)(qb + l32 * ROWB + ((c ^ (l32 & (NCH - 1))) << 4));
+      s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka[st], b, s, 0, 0, 0);
+    }
     // the chunk's first column (lane 0's) has the smallest row; no mask when it sees all 32 keys
-    const int first_pos = __builtin_amdgcn_readfirstlane(pos_cur);
+    const int first_pos = __builtin_amdgcn_readfirstlane(pc0);
     const bool need_mask = first_pos < jw + 31;
 #pragma unroll
     for (int e = 0; e < 16; ++e) {
-      float p = __builtin_amdgcn_exp2f(s[e] * a.scale_log2 - lse_cur);
+      float p = __builtin_amdgcn_exp2f(s[e] * a.scale_log2 - lc0);
       if (need_mask) {
         const int key = jw + (e >> 2) * 8 + hg * 4 + (e & 3);
-        p = key <= pos_cur ? p : 0.f;
+        p = key <= pc0 ? p : 0.f;
       }
       acc32[e] += p;
     }
@@ -605,11 +642,10 @@ __global__ __launch_bounds__(256, 2) void colsum_mfma_kernel(ColsumK a) {
       }
       pending = 0;
     }
-#pragma unroll
-    for (int st = 0; st < D / 16; ++st) qcur[st] = qnxt[st];
-    lse_cur = lse_nxt;
-    pos_cur = pos_nxt;
-    pos_nxt = pos_nn;
+    pc0 = pc1;
+    lc0 = lc1;
+    pc1 = pc2;
+    __syncthreads();
   }
 #pragma unroll
   for (int e = 0; e < 16; ++e) acc64[e] += (double)acc32[e];
@@ -692,11 +728,11 @@ hipError_t launch_colsum(const sx_plan* p, const void* q, const void* kc, const 
   a.G = a.Hq / a.Hkv;
   a.scale_log2 = p->scale * 1.4426950408889634f;
   a.n_req = p->n_req;
-  const dim3 grid((unsigned)(((p->max_T + 127) / 128) * a.Hkv * p->n_req));
+  const dim3 grid((unsigned)(((p->max_T + CS_KEYS - 1) / CS_KEYS) * a.Hkv * p->n_req));
   if (p->desc.head_dim == 128)
-    hipLaunchKernelGGL(colsum_mfma_kernel<128>, grid, dim3(256), 0, s, a);
+    hipLaunchKernelGGL(colsum_mfma_kernel<128>, grid, dim3(512), 0, s, a);
   else
-    hipLaunchKernelGGL(colsum_mfma_kernel<64>, grid, dim3(256), 0, s, a);
+    hipLaunchKernelGGL(colsum_mfma_kernel<64>, grid, dim3(512), 0, s, a);
   return hipGetLastError();
 }
 
