@@ -50,6 +50,8 @@ def parse():
     ap.add_argument("--score-passes", type=int, choices=(1, 2), default=1,
                     help="Sparse-Q scoring in hybrid stacks: 1 = denominators from the boundary layer's full "
                          "attention (exact-logit variant), 2 = own log-sum-exp pass")
+    ap.add_argument("--separate-kv", action="store_true",
+                    help="sparse layers: re-alignment and the KV write of R as two passes instead of one")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
                     help="also run a plain device copy of BYTES bytes (reference for HBM byte counters)")
     ap.add_argument("--record-traffic", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
@@ -69,6 +71,8 @@ KERNELS = {
     "head_reduce_kernel": ("sx_sparseq_score", "k_copy.hip"),
     "realign_kernel": ("sx_rope_realign", "k_copy.hip"),
     "scatter_kernel": ("sx_kv_scatter", "k_copy.hip"),
+    "realign_scatter_kernel": ("sx_realign_scatter", "k_copy.hip"),
+    "mark_rows_kernel": ("sx_realign_scatter", "k_copy.hip"),
     "topk_kernel": ("sx_topk_select", "k_topk.hip"),
 }
 
@@ -94,8 +98,10 @@ def record_traffic(fetch_csv, write_csv, workload):
             v = float(r["Counter_Value"])
             if "copyBuffer" in r["Kernel_Name"]:
                 copy.append((int(r["Grid_Size"]), v))
+            name = re.sub(r"\s", "", r["Kernel_Name"])
             for sym in KERNELS:
-                if sym.replace(" ", "") in re.sub(r"\s", "", r["Kernel_Name"]):
+                # whole identifier only (scatter_kernel is also the tail of realign_scatter_kernel)
+                if re.search(r"(?<![A-Za-z0-9_])" + re.escape(sym.replace(" ", "")), name):
                     acc.setdefault(sym, []).append(v)
         return acc, max(copy)[1] if copy else None
 
@@ -240,11 +246,20 @@ def main():
         tm.run("sx_topk_select", lambda: sx.topk_select(plan, scores, ratio, rows, n_rows))
         for l in range(max(nfull, 0), L):
             tl = layers[l]
-            if not (nfull == 0 and l == 0):
+            if nfull == 0 and l == 0:
+                # the selecting layer's cache is already re-aligned: only R's fresh rows remain
+                tm.run("sx_kv_scatter", lambda: sx.kv_scatter(plan, tl["k"], tl["v"], tl["kc"], tl["vc"], rows=rows,
+                                                              n_rows=n_rows, max_rows=max_rows))
+            elif args.separate_kv:
                 tm.run("sx_rope_realign",
                        lambda: sx.rope_realign(plan, tl["k_src"], tl["v_src"], tl["kc"], tl["vc"]))
-            tm.run("sx_kv_scatter", lambda: sx.kv_scatter(plan, tl["k"], tl["v"], tl["kc"], tl["vc"], rows=rows,
-                                                          n_rows=n_rows, max_rows=max_rows))
+                tm.run("sx_kv_scatter", lambda: sx.kv_scatter(plan, tl["k"], tl["v"], tl["kc"], tl["vc"], rows=rows,
+                                                              n_rows=n_rows, max_rows=max_rows))
+            else:
+                # one pass: each slot gets either its fresh row (token in R) or its re-aligned cached row
+                tm.run("sx_realign_scatter",
+                       lambda: sx.realign_scatter(plan, tl["k_src"], tl["v_src"], tl["k"], tl["v"], rows, n_rows,
+                                                  max_rows, tl["kc"], tl["vc"]))
             tm.run("sx_sparse_attn", lambda: sx.sparse_attn(plan, tl["q"], rows, n_rows, max_rows, tl["kc"], tl["vc"],
                                                             out))
 
@@ -295,9 +310,16 @@ def main():
         "sx_topk_select": ("latency", 5.0 * T),
     }
     # KV write: all rows in the full layers, R in the sparse layers (and I_nr in a selecting layer)
-    n_scatter_rows = nfull * T + (L - nfull) * n_R + (info["n_nonreused"] if nfull == 0 else 0)
-    n_scatter_launches = nfull + (L - nfull) + (1 if nfull == 0 else 0)
-    work["sx_kv_scatter"] = ("hbm", 4.0 * row_bytes * n_scatter_rows / n_scatter_launches)
+    n_sparse = L - nfull
+    n_sep = n_sparse if args.separate_kv else (1 if nfull == 0 else 0)   # sparse layers with a separate write
+    n_scatter_rows = nfull * T + n_sep * n_R + (info["n_nonreused"] if nfull == 0 else 0)
+    n_scatter_launches = nfull + n_sep + (1 if nfull == 0 else 0)
+    if n_scatter_launches:
+        work["sx_kv_scatter"] = ("hbm", 4.0 * row_bytes * n_scatter_rows / n_scatter_launches)
+    # one-pass re-alignment + write: every reused token's slot plus the uncached tokens of R, each
+    # read once and written once (K and V)
+    n_R_uncached = int(sum(np.count_nonzero(~req.cached_mask()[Rr]) for req, Rr in zip(w.requests, R)))
+    work["sx_realign_scatter"] = ("hbm", 4.0 * row_bytes * (info["n_reused"] + n_R_uncached))
     peak = PEAK_BF16_TFLOPS if w.dtype == "bf16" else PEAK_F32_TFLOPS
     kernels = {}
     for name, k in kern.items():
@@ -339,7 +361,8 @@ def main():
         "vs_baseline": None, "dtype": w.dtype, "data": "synthetic (seeded N(0,1) inputs, layout rules of the workload)",
         "config": {"workload": f"{w.name}: {w.description}", "tokens": T, "layers": L, "full_layers": nfull,
                    "ratio": ratio, "recompute_rows": n_R, "k": int(k_total), "q_heads": Hq, "kv_heads": Hkv,
-                   "head_dim": d, "requests": len(w.requests), "score_passes": args.score_passes},
+                   "head_dim": d, "requests": len(w.requests), "score_passes": args.score_passes,
+                   "kv_write": "separate" if args.separate_kv else "one-pass"},
         "kernels": kernels, "roofline": roof, "cpu_baseline": cpu,
     }
     print(json.dumps(res), flush=True)

@@ -164,6 +164,18 @@ sx_status sx_kv_scatter(const sx_plan* plan, const void* k_new, const void* v_ne
                         const int32_t* n_rows, int32_t max_rows, void* k_cache, void* v_cache,
                         void* stream);
 
+/* Algorithm 1 steps 6 and 19-20 in one pass for a layer whose recompute set R is known (the
+ * sparse layers of a hybrid stack reuse the boundary layer's R, Section 3.4): the cache slot of
+ * every listed row of request r gets k_new/v_new (bit-exact, as sx_kv_scatter), the slot of every
+ * other reused token gets its re-aligned cached K and V (as sx_rope_realign); other tokens are not
+ * touched.  Same result as sx_rope_realign followed by sx_kv_scatter with the same rows, but each
+ * slot is read and written once.  rows/n_rows/max_rows as in sx_kv_scatter (rows required);
+ * src_k/src_v may be NULL only when no segment is cached.  Keeps a row-set mark per token in plan
+ * scratch, so calls sharing a plan must be stream-ordered. */
+sx_status sx_realign_scatter(const sx_plan* plan, const void* src_k, const void* src_v, const void* k_new,
+                             const void* v_new, const int32_t* rows, const int32_t* n_rows, int32_t max_rows,
+                             void* k_cache, void* v_cache, void* stream);
+
 /* Eq. sparseq-attn and Eq. sparseq-score with the cross-head sum of Section 3.2:
  *   scores[off_r + j] = sum_h sum_{i in P_r, i >= j} softmax_j(scale * q[i,h] . K[j, h/(Hq/Hkv)])
  * over the probe rows P_r = I_nr U S_tail of request r, reading keys from k_cache (whatever the

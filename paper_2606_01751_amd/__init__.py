@@ -23,7 +23,8 @@ import os
 from typing import Optional, Sequence
 
 __all__ = [
-    "LIB_PATH", "SxError", "lib", "LayerDesc", "Plan", "rope_realign", "kv_scatter", "sparseq_score",
+    "LIB_PATH", "SxError", "lib", "LayerDesc", "Plan", "rope_realign", "kv_scatter", "realign_scatter",
+    "sparseq_score",
     "topk_select", "sparse_attn", "full_attn", "F32", "BF16", "ROPE_NEOX", "ROPE_GPTJ", "EXPORTED",
 ]
 
@@ -35,8 +36,8 @@ SX_OK, SX_EINVAL, SX_ESHAPE, SX_EUNSUPPORTED, SX_EHIP, SX_ENOMEM = 0, -1, -2, -3
 
 EXPORTED = (
     "sx_plan_create", "sx_plan_destroy", "sx_plan_get_info", "sx_plan_budget", "sx_plan_nonreused_rows",
-    "sx_rope_realign", "sx_kv_scatter", "sx_sparseq_score", "sx_topk_select", "sx_sparse_attn",
-    "sx_full_attn", "sx_last_error", "sx_version",
+    "sx_rope_realign", "sx_kv_scatter", "sx_realign_scatter", "sx_sparseq_score", "sx_topk_select",
+    "sx_sparse_attn", "sx_full_attn", "sx_last_error", "sx_version",
 )
 
 
@@ -94,6 +95,7 @@ def lib() -> ctypes.CDLL:
         L.sx_plan_nonreused_rows.argtypes = [VP, P(VP), P(VP), P(I32)]
         L.sx_rope_realign.argtypes = [VP, VP, VP, VP, VP, VP]
         L.sx_kv_scatter.argtypes = [VP, VP, VP, VP, VP, I32, VP, VP, VP]
+        L.sx_realign_scatter.argtypes = [VP, VP, VP, VP, VP, VP, VP, I32, VP, VP, VP]
         L.sx_sparseq_score.argtypes = [VP, VP, VP, VP, VP, VP]
         L.sx_topk_select.argtypes = [VP, VP, D, VP, VP, VP]
         L.sx_sparse_attn.argtypes = [VP, VP, VP, VP, I32, VP, VP, VP, VP]
@@ -210,6 +212,12 @@ def kv_scatter(plan: Plan, k_new, v_new, k_cache, v_cache, rows=None, n_rows=Non
                stream=None):
     _check(lib().sx_kv_scatter(plan.handle, _ptr(k_new), _ptr(v_new), _ptr(rows), _ptr(n_rows), int(max_rows),
                                _ptr(k_cache), _ptr(v_cache), _stream(stream)))
+
+
+def realign_scatter(plan: Plan, src_k, src_v, k_new, v_new, rows, n_rows, max_rows: int, k_cache, v_cache,
+                    stream=None):
+    _check(lib().sx_realign_scatter(plan.handle, _ptr(src_k), _ptr(src_v), _ptr(k_new), _ptr(v_new), _ptr(rows),
+                                    _ptr(n_rows), int(max_rows), _ptr(k_cache), _ptr(v_cache), _stream(stream)))
 
 
 def sparseq_score(plan: Plan, q, k_cache, scores, lse_in=None, stream=None):

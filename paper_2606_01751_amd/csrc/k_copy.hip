@@ -136,6 +136,99 @@ __global__ __launch_bounds__(256) void scatter_kernel(const ReqDev* __restrict__
   vc[dst] = v_new[src];
 }
 
+// Marks the listed rows of every request with the call's generation number (no clearing pass:
+// a token belongs to the current row set iff its mark equals the generation).
+__global__ __launch_bounds__(256) void mark_rows_kernel(const ReqDev* __restrict__ reqs, const int32_t* __restrict__ rows,
+                                                        const int32_t* __restrict__ n_rows, int max_rows,
+                                                        uint32_t* __restrict__ mark, uint32_t gen) {
+  const ReqDev rq = reqs[blockIdx.y];
+  const int idx = blockIdx.x * blockDim.x + threadIdx.x;
+  if (idx >= max_rows || idx >= n_rows[blockIdx.y]) return;
+  const int t = rows[rq.tok_off + idx];
+  if (t >= 0 && t < rq.T) mark[rq.tok_off + t] = gen;
+}
+
+__global__ __launch_bounds__(256) void fill_u32_kernel(uint32_t* __restrict__ p, int64_t n, uint32_t v) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n) p[i] = v;
+}
+
+// Re-alignment and KV write in one pass (Algorithm 1 steps 6 and 19-20 for a sparse layer whose
+// row set R is known): every token's cache slot is written once -- the fresh K/V row if the token
+// is in R, else the re-aligned cached row if the token is reused; other tokens are not touched.
+// Work unit as in realign_kernel: VEC RoPE pairs of one head plus 32 bytes of V; with d = 128 and
+// 8 KV heads a wavefront is exactly one token, so the branch is uniform.
+template <int D, bool BF16, bool NEOX>
+__global__ __launch_bounds__(256) void realign_scatter_kernel(
+    const int32_t* __restrict__ tok_slot, const int32_t* __restrict__ tok_ra, const RealignRow* __restrict__ ra,
+    const float2* __restrict__ cs, const uint32_t* __restrict__ mark, uint32_t gen, int64_t total,
+    const void* __restrict__ src_k_, const void* __restrict__ src_v_, const void* __restrict__ k_new_,
+    const void* __restrict__ v_new_, void* __restrict__ kc_, void* __restrict__ vc_, int Hkv) {
+  constexpr int ESZ = BF16 ? 2 : 4;
+  constexpr int VEC = 16 / ESZ;
+  constexpr int UPH = D / (2 * VEC);
+  char* kc = (char*)kc_;
+  char* vc = (char*)vc_;
+  const int units = Hkv * UPH;
+  const int64_t g = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const int64_t tok = g / units;
+  if (tok >= total) return;
+  const int u = (int)(g - tok * units);
+  const int head = u / UPH;
+  const int ui = u - head * UPH;
+  int64_t e0, e1;
+  if constexpr (NEOX) {
+    e0 = (int64_t)ui * VEC;
+    e1 = e0 + D / 2;
+  } else {
+    e0 = (int64_t)ui * 2 * VEC;
+    e1 = e0 + VEC;
+  }
+  const int64_t v0 = (int64_t)ui * 2 * VEC;
+  const int64_t dof = pool_off(tok_slot[tok], head, Hkv, D) * ESZ;
+  if (mark[tok] == gen) {
+    // fresh row of a token in R (bit-exact copy)
+    const char* kn = (const char*)k_new_ + (tok * Hkv + head) * D * ESZ;
+    const char* vn = (const char*)v_new_ + (tok * Hkv + head) * D * ESZ;
+    *(uint4*)(kc + dof + e0 * ESZ) = *(const uint4*)(kn + e0 * ESZ);
+    *(uint4*)(kc + dof + e1 * ESZ) = *(const uint4*)(kn + e1 * ESZ);
+    *(uint4*)(vc + dof + v0 * ESZ) = *(const uint4*)(vn + v0 * ESZ);
+    *(uint4*)(vc + dof + (v0 + VEC) * ESZ) = *(const uint4*)(vn + (v0 + VEC) * ESZ);
+    return;
+  }
+  const int32_t ri = tok_ra[tok];
+  if (ri < 0) return;   // uncached and not listed: left as it is
+  const RealignRow rr = ra[ri];
+  const char* src_k = (const char*)src_k_;
+  const char* src_v = (const char*)src_v_;
+  const int64_t so = pool_off(rr.src_slot, head, Hkv, D) * ESZ;
+  const uint4 ka = *(const uint4*)(src_k + so + e0 * ESZ);
+  const uint4 kb = *(const uint4*)(src_k + so + e1 * ESZ);
+  const uint4 va = *(const uint4*)(src_v + so + v0 * ESZ);
+  const uint4 vb = *(const uint4*)(src_v + so + (v0 + VEC) * ESZ);
+  const float2* csr = cs + (int64_t)rr.cs_row * (D / 2) + (int64_t)ui * VEC;
+  float2 c[VEC];
+#pragma unroll
+  for (int e = 0; e < VEC; ++e) c[e] = csr[e];
+  float fa[VEC], fb[VEC], ya[VEC], yb[VEC];
+  unpack<BF16>(ka, fa);
+  unpack<BF16>(kb, fb);
+  if constexpr (NEOX) {
+#pragma unroll
+    for (int e = 0; e < VEC; ++e) rot(fa[e], fb[e], c[e].x, c[e].y, ya[e], yb[e]);
+  } else {
+#pragma unroll
+    for (int e = 0; e < VEC / 2; ++e) {
+      rot(fa[2 * e], fa[2 * e + 1], c[e].x, c[e].y, ya[2 * e], ya[2 * e + 1]);
+      rot(fb[2 * e], fb[2 * e + 1], c[VEC / 2 + e].x, c[VEC / 2 + e].y, yb[2 * e], yb[2 * e + 1]);
+    }
+  }
+  *(uint4*)(kc + dof + e0 * ESZ) = pack<BF16>(ya);
+  *(uint4*)(kc + dof + e1 * ESZ) = pack<BF16>(yb);
+  *(uint4*)(vc + dof + v0 * ESZ) = va;
+  *(uint4*)(vc + dof + (v0 + VEC) * ESZ) = vb;
+}
+
 // scores[i] = sum over KV heads h (in order) of colsum[h][i], rounded once to float32.
 __global__ __launch_bounds__(256) void head_reduce_kernel(const double* __restrict__ colsum, int64_t total, int Hkv,
                                                           float* __restrict__ scores) {
@@ -183,6 +276,46 @@ hipError_t launch_scatter(const sx_plan* p, const void* k_new, const void* v_new
   hipLaunchKernelGGL(scatter_kernel, grid, dim3(256), 0, s, p->d_req, p->d_bt, rows, n_rows, (const uint4*)k_new,
                      (const uint4*)v_new, (uint4*)kc, (uint4*)vc, p->desc.n_kv_heads, upr, uph);
   return hipGetLastError();
+}
+
+template <int D, bool BF16, bool NEOX>
+hipError_t realign_scatter_dispatch(const sx_plan* p, const void* sk, const void* sv, const void* kn,
+                                   const void* vn, void* kc, void* vc, uint32_t gen, hipStream_t s) {
+  constexpr int VEC = BF16 ? 8 : 4;
+  const int units = p->desc.n_kv_heads * (D / (2 * VEC));
+  const int64_t threads = p->total * units;
+  hipLaunchKernelGGL((realign_scatter_kernel<D, BF16, NEOX>), dim3((unsigned)((threads + 255) / 256)), dim3(256), 0,
+                     s, p->d_tok_slot, p->d_tok_ra, p->d_ra, p->d_cs, p->d_rmark, gen, p->total, sk, sv, kn, vn, kc,
+                     vc, p->desc.n_kv_heads);
+  return hipGetLastError();
+}
+
+hipError_t launch_realign_scatter(const sx_plan* p, const void* sk, const void* sv, const void* kn, const void* vn,
+                                  const int32_t* rows, const int32_t* n_rows, int32_t max_rows, void* kc, void* vc,
+                                  uint32_t gen, bool clear_marks, hipStream_t s) {
+  if (clear_marks) {
+    hipLaunchKernelGGL(fill_u32_kernel, dim3((unsigned)((p->total + 255) / 256)), dim3(256), 0, s, p->d_rmark,
+                       p->total, 0u);
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  if (max_rows > 0) {
+    hipLaunchKernelGGL(mark_rows_kernel, dim3((unsigned)((max_rows + 255) / 256), (unsigned)p->n_req), dim3(256), 0,
+                       s, p->d_req, rows, n_rows, max_rows, p->d_rmark, gen);
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  const bool bf16 = p->desc.dtype == SX_BF16;
+  const bool neox = p->desc.rope_style == SX_ROPE_NEOX;
+#define SX_RS(D_, B_, N_) return realign_scatter_dispatch<D_, B_, N_>(p, sk, sv, kn, vn, kc, vc, gen, s)
+  if (p->desc.head_dim == 128) {
+    if (bf16) { if (neox) SX_RS(128, true, true); else SX_RS(128, true, false); }
+    else { if (neox) SX_RS(128, false, true); else SX_RS(128, false, false); }
+  } else {
+    if (bf16) { if (neox) SX_RS(64, true, true); else SX_RS(64, true, false); }
+    else { if (neox) SX_RS(64, false, true); else SX_RS(64, false, false); }
+  }
+#undef SX_RS
 }
 
 hipError_t launch_head_reduce(const sx_plan* p, float* scores, hipStream_t s) {

@@ -85,8 +85,8 @@ sx_status dev_upload(sx_plan* p, T** ptr, const std::vector<T>& host) {
 
 void free_plan(sx_plan* p) {
   if (!p) return;
-  void* bufs[] = {p->d_req, p->d_bt, p->d_ra, p->d_cs, p->d_probe, p->d_nr,
-                  p->d_n_nr, p->d_n_probe, p->d_flags, p->d_lse, p->d_colsum};
+  void* bufs[] = {p->d_req, p->d_bt, p->d_ra, p->d_cs, p->d_probe, p->d_nr, p->d_n_nr, p->d_n_probe,
+                  p->d_flags, p->d_tok_slot, p->d_tok_ra, p->d_rmark, p->d_lse, p->d_colsum};
   for (void* b : bufs)
     if (b) (void)hipFree(b);
   delete p;
@@ -185,6 +185,7 @@ sx_status sx_plan_create(const sx_layer_desc* desc, const sx_request* requests, 
   std::vector<int32_t> probe((size_t)total, 0), nr((size_t)total, 0);
   std::vector<int32_t> n_nr(n_requests), n_probe(n_requests);
   std::vector<uint8_t> flags((size_t)total, 0);
+  std::vector<int32_t> tok_slot((size_t)total, 0), tok_ra((size_t)total, -1);
   std::vector<double> theta(d / 2);
   for (int i = 0; i < d / 2; ++i) theta[i] = std::pow(desc->rope_base, -2.0 * i / d);
   int64_t off = 0;
@@ -198,6 +199,7 @@ sx_status sx_plan_create(const sx_layer_desc* desc, const sx_request* requests, 
     h.bt_off = (int32_t)bt_all.size();
     const int nblk = (T + b - 1) / b;
     bt_all.insert(bt_all.end(), q.block_table, q.block_table + nblk);
+    for (int t = 0; t < T; ++t) tok_slot[off + t] = q.block_table[t / b] * b + (t % b);
     uint8_t* fl = flags.data() + off;
     const sx_segment* last = nullptr;
     for (int m = 0; m < q.n_segments; ++m) {
@@ -217,6 +219,7 @@ sx_status sx_plan_create(const sx_layer_desc* desc, const sx_request* requests, 
         row.dst_slot = q.block_table[tok / b] * b + (tok % b);
         row.cs_row = cs_rows;
         row.pad = 0;
+        tok_ra[off + tok] = (int32_t)ra.size();
         ra.push_back(row);
       }
       ++cs_rows;
@@ -273,6 +276,9 @@ sx_status sx_plan_create(const sx_layer_desc* desc, const sx_request* requests, 
   if (st == SX_OK) st = dev_upload(p, &p->d_n_nr, n_nr);
   if (st == SX_OK) st = dev_upload(p, &p->d_n_probe, n_probe);
   if (st == SX_OK) st = dev_upload(p, &p->d_flags, flags);
+  if (st == SX_OK) st = dev_upload(p, &p->d_tok_slot, tok_slot);
+  if (st == SX_OK) st = dev_upload(p, &p->d_tok_ra, tok_ra);
+  if (st == SX_OK) st = dev_upload(p, &p->d_rmark, std::vector<uint32_t>((size_t)total, 0u));
   if (st == SX_OK) st = dev_alloc(p, &p->d_lse, (size_t)total * desc->n_q_heads);
   if (st == SX_OK) st = dev_alloc(p, &p->d_colsum, (size_t)total * desc->n_kv_heads);
   if (st != SX_OK) {
@@ -355,6 +361,25 @@ sx_status sx_kv_scatter(const sx_plan* p, const void* k_new, const void* v_new, 
   return check_launch(sx::launch_scatter(p, k_new, v_new, rows, n_rows, rows ? max_rows : p->max_T, k_cache,
                                          v_cache, (hipStream_t)stream),
                       "sx_kv_scatter launch");
+}
+
+sx_status sx_realign_scatter(const sx_plan* p, const void* src_k, const void* src_v, const void* k_new,
+                             const void* v_new, const int32_t* rows, const int32_t* n_rows, int32_t max_rows,
+                             void* k_cache, void* v_cache, void* stream) {
+  if (!p) return fail(SX_EINVAL, "plan is NULL");
+  if (!k_new || !v_new || !k_cache || !v_cache || !rows || !n_rows) return fail(SX_EINVAL, "NULL argument");
+  if (p->n_realign > 0 && (!src_k || !src_v)) return fail(SX_EINVAL, "NULL source pool");
+  if (max_rows < 0) return fail(SX_EINVAL, "max_rows must be >= 0");
+  if (p->total == 0) return SX_OK;
+  // a new generation for this call's row set; on wrap-around every mark is cleared first
+  bool clear = false;
+  if (++p->rgen == 0) {
+    p->rgen = 1;
+    clear = true;
+  }
+  return check_launch(sx::launch_realign_scatter(p, src_k, src_v, k_new, v_new, rows, n_rows, max_rows, k_cache,
+                                                 v_cache, p->rgen, clear, (hipStream_t)stream),
+                      "sx_realign_scatter launch");
 }
 
 sx_status sx_sparseq_score(const sx_plan* p, const void* q, const void* k_cache, const float* lse_in, float* scores,

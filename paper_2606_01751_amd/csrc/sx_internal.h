@@ -66,6 +66,10 @@ struct sx_plan {
   int32_t* d_n_nr = nullptr;      // [n_req]
   int32_t* d_n_probe = nullptr;   // [n_req]
   uint8_t* d_flags = nullptr;     // [sum T]
+  int32_t* d_tok_slot = nullptr;  // [sum T] destination slot (block * b + slot) of every token
+  int32_t* d_tok_ra = nullptr;    // [sum T] index of the token's re-alignment row, -1 if uncached
+  uint32_t* d_rmark = nullptr;    // [sum T] row-set generation marks (sx_realign_scatter)
+  mutable uint32_t rgen = 0;      // last generation used
   float* d_lse = nullptr;         // scratch [sum T][Hq]
   double* d_colsum = nullptr;     // scratch [Hkv][sum T]
 };
@@ -78,6 +82,11 @@ hipError_t launch_realign(const sx_plan* p, const void* src_k, const void* src_v
 hipError_t launch_scatter(const sx_plan* p, const void* k_new, const void* v_new, const int32_t* rows,
                           const int32_t* n_rows, int32_t max_rows, void* kc, void* vc, hipStream_t s);
 hipError_t launch_head_reduce(const sx_plan* p, float* scores, hipStream_t s);
+// fused re-alignment + KV write: marks the rows with `gen` (after clearing every mark when
+// clear_marks), then writes every token's slot once
+hipError_t launch_realign_scatter(const sx_plan* p, const void* sk, const void* sv, const void* kn, const void* vn,
+                                  const int32_t* rows, const int32_t* n_rows, int32_t max_rows, void* kc, void* vc,
+                                  uint32_t gen, bool clear_marks, hipStream_t s);
 hipError_t launch_topk(const sx_plan* p, const float* scores, double ratio, int32_t* rows, int32_t* n_rows,
                        hipStream_t s);
 

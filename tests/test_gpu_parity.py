@@ -112,6 +112,49 @@ def test_scatter_matches_oracle(name, w):
 
 
 @pytest.mark.parametrize("name,w", CASES, ids=IDS)
+def test_fused_realign_scatter_matches_oracle(name, w):
+    """One pass of re-alignment + KV write equals sx_rope_realign followed by sx_kv_scatter (bit-exact)
+    and the oracle's pools, for three row sets in a row on one plan: I_nr plus a random third of the
+    tokens, a smaller random set that leaves some uncached tokens out (their slots stay untouched),
+    and the empty set (re-alignment only)."""
+    log(f"[realign_scatter] {name}")
+    t = W.layer_tensors(w, 0)
+    g = GpuLayer(w, t)
+    ref = GpuLayer(w, t)
+    rng = np.random.default_rng(17)
+    offs = w.token_offsets
+    big = [np.unique(np.concatenate([O.nonreuse_positions(r.n_tokens, r.segments),
+                                     rng.choice(r.n_tokens, size=r.n_tokens // 3, replace=False)]))
+           for r in w.requests]
+    small = [np.sort(rng.choice(r.n_tokens, size=max(1, r.n_tokens // 7), replace=False)) for r in w.requests]
+    empty = [np.zeros(0, np.int64) for _ in w.requests]
+    tol = 1e-2 if w.dtype == "bf16" else 1e-5
+    for label, sets in (("I_nr + third", big), ("seventh", small), ("empty", empty)):
+        m = max(len(s) for s in sets)
+        for x in (g, ref):
+            x.k_cache.fill_(CANARY)
+            x.v_cache.fill_(CANARY)
+            x.set_rows(sets)
+        sx.realign_scatter(g.plan, g.t["k_src"], g.t["v_src"], g.t["k"], g.t["v"], g.rows, g.n_rows, m,
+                           g.k_cache, g.v_cache)
+        ref.realign()
+        sx.kv_scatter(ref.plan, ref.t["k"], ref.t["v"], ref.k_cache, ref.v_cache, rows=ref.rows, n_rows=ref.n_rows,
+                      max_rows=m)
+        torch.cuda.synchronize()
+        gk, gv = host(g.k_cache), host(g.v_cache)
+        assert np.array_equal(gk, host(ref.k_cache)), label
+        assert np.array_equal(gv, host(ref.v_cache)), label
+        kp, vp = oracle_pool(w), oracle_pool(w)
+        for r, req in enumerate(w.requests):
+            O.realign_request(req, w, t["k_src"], t["v_src"], kp, vp)
+            O.scatter_rows(req, w, sets[r], t["k"][offs[r]:offs[r + 1]], t["v"][offs[r]:offs[r + 1]], kp, vp)
+        err = np.abs(gk - kp).max()
+        log(f"  {label}: K max-abs {err:.3g}")
+        assert err <= tol, label
+        assert np.array_equal(gv, vp), label
+
+
+@pytest.mark.parametrize("name,w", CASES, ids=IDS)
 def test_full_attention_matches_oracle(name, w):
     log(f"[full_attn] {name}")
     t = W.layer_tensors(w, 0)
