@@ -102,15 +102,14 @@ def test_c3_boundary_selection_and_layers():
     assert err <= 2e-2
     del q, k, v, kc, vc, out, t
 
-    # first sparse layer: re-alignment, KV write of R, sparse attention of R
+    # first sparse layer as the stack runs it: one-pass re-alignment + KV write of R, sparse attention of R
     layer += 1
     log(f"[c3] generating layer {layer}")
     t = W.layer_tensors(w, layer)
     q, k, v, ks, vs = (dev(t[n], w) for n in ("q", "k", "v", "k_src", "v_src"))
     kc, vc = _pool(w, dt), _pool(w, dt)
     out = torch.zeros_like(q)
-    sx.rope_realign(plan, ks, vs, kc, vc)
-    sx.kv_scatter(plan, k, v, kc, vc, rows=rows, n_rows=n_rows, max_rows=max_rows)
+    sx.realign_scatter(plan, ks, vs, k, v, rows, n_rows, max_rows, kc, vc)
     sx.sparse_attn(plan, q, rows, n_rows, max_rows, kc, vc, out)
     torch.cuda.synchronize()
     kp = np.zeros((w.n_dst_blocks, w.n_kv_heads, w.block_size, w.head_dim), np.float32)
