@@ -50,8 +50,10 @@ def parse():
     ap.add_argument("--score-passes", type=int, choices=(1, 2), default=1,
                     help="Sparse-Q scoring in hybrid stacks: 1 = denominators from the boundary layer's full "
                          "attention (exact-logit variant), 2 = own log-sum-exp pass")
-    ap.add_argument("--separate-kv", action="store_true",
-                    help="sparse layers: re-alignment and the KV write of R as two passes instead of one")
+    ap.add_argument("--kv-write", choices=("per-layer", "all-layers", "separate"), default="per-layer",
+                    help="sparse layers' re-alignment + KV write of R: one pass per layer just before its "
+                         "attention (default; the attention then finds part of the cache in the Infinity Cache), "
+                         "one pass for all sparse layers after the selection, or two passes per layer")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
                     help="also run a plain device copy of BYTES bytes (reference for HBM byte counters)")
     ap.add_argument("--record-traffic", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
@@ -72,7 +74,7 @@ KERNELS = {
     "realign_kernel": ("sx_rope_realign", "k_copy.hip"),
     "scatter_kernel": ("sx_kv_scatter", "k_copy.hip"),
     "realign_scatter_kernel": ("sx_realign_scatter", "k_copy.hip"),
-    "mark_rows_kernel": ("sx_realign_scatter", "k_copy.hip"),
+    "mark_rows_kernel": ("sx_realign_scatter", "k_copy.hip"),   # (also sx_realign_scatter_layers)
     "topk_kernel": ("sx_topk_select", "k_topk.hip"),
 }
 
@@ -221,6 +223,8 @@ def main():
     log(f"inputs resident in HBM ({torch.cuda.memory_allocated() / 2**30:.1f} GiB) in {time.time() - t0:.1f}s")
 
     tm = Timers(torch)
+    sparse_kv = [(tl["k_src"], tl["v_src"], tl["k"], tl["v"], tl["kc"], tl["vc"])
+                 for l, tl in enumerate(layers) if l >= nfull and not (nfull == 0 and l == 0)]
 
     def step():
         for l in range(nfull):
@@ -244,13 +248,19 @@ def main():
                                                             lse_in=lse if (nfull > 0 and args.score_passes == 1)
                                                             else None))
         tm.run("sx_topk_select", lambda: sx.topk_select(plan, scores, ratio, rows, n_rows))
+        if args.kv_write == "all-layers" and sparse_kv:
+            # every sparse layer's cache in one call (two launches of at most 16 layers)
+            tm.run("sx_realign_scatter_layers",
+                   lambda: sx.realign_scatter_layers(plan, sparse_kv, rows, n_rows, max_rows))
         for l in range(max(nfull, 0), L):
             tl = layers[l]
             if nfull == 0 and l == 0:
                 # the selecting layer's cache is already re-aligned: only R's fresh rows remain
                 tm.run("sx_kv_scatter", lambda: sx.kv_scatter(plan, tl["k"], tl["v"], tl["kc"], tl["vc"], rows=rows,
                                                               n_rows=n_rows, max_rows=max_rows))
-            elif args.separate_kv:
+            elif args.kv_write == "all-layers":
+                pass
+            elif args.kv_write == "separate":
                 tm.run("sx_rope_realign",
                        lambda: sx.rope_realign(plan, tl["k_src"], tl["v_src"], tl["kc"], tl["vc"]))
                 tm.run("sx_kv_scatter", lambda: sx.kv_scatter(plan, tl["k"], tl["v"], tl["kc"], tl["vc"], rows=rows,
@@ -311,7 +321,7 @@ def main():
     }
     # KV write: all rows in the full layers, R in the sparse layers (and I_nr in a selecting layer)
     n_sparse = L - nfull
-    n_sep = n_sparse if args.separate_kv else (1 if nfull == 0 else 0)   # sparse layers with a separate write
+    n_sep = n_sparse if args.kv_write == "separate" else (1 if nfull == 0 else 0)   # sparse layers with a separate write
     n_scatter_rows = nfull * T + n_sep * n_R + (info["n_nonreused"] if nfull == 0 else 0)
     n_scatter_launches = nfull + n_sep + (1 if nfull == 0 else 0)
     if n_scatter_launches:
@@ -320,6 +330,7 @@ def main():
     # read once and written once (K and V)
     n_R_uncached = int(sum(np.count_nonzero(~req.cached_mask()[Rr]) for req, Rr in zip(w.requests, R)))
     work["sx_realign_scatter"] = ("hbm", 4.0 * row_bytes * (info["n_reused"] + n_R_uncached))
+    work["sx_realign_scatter_layers"] = ("hbm", len(sparse_kv) * work["sx_realign_scatter"][1])
     peak = PEAK_BF16_TFLOPS if w.dtype == "bf16" else PEAK_F32_TFLOPS
     kernels = {}
     for name, k in kern.items():
@@ -362,7 +373,7 @@ def main():
         "config": {"workload": f"{w.name}: {w.description}", "tokens": T, "layers": L, "full_layers": nfull,
                    "ratio": ratio, "recompute_rows": n_R, "k": int(k_total), "q_heads": Hq, "kv_heads": Hkv,
                    "head_dim": d, "requests": len(w.requests), "score_passes": args.score_passes,
-                   "kv_write": "separate" if args.separate_kv else "one-pass"},
+                   "kv_write": args.kv_write},
         "kernels": kernels, "roofline": roof, "cpu_baseline": cpu,
     }
     print(json.dumps(res), flush=True)

@@ -176,6 +176,26 @@ sx_status sx_realign_scatter(const sx_plan* plan, const void* src_k, const void*
                              const void* v_new, const int32_t* rows, const int32_t* n_rows, int32_t max_rows,
                              void* k_cache, void* v_cache, void* stream);
 
+/* Device buffers of one layer for sx_realign_scatter_layers (same meaning as the arguments of
+ * sx_realign_scatter). */
+typedef struct {
+  const void* src_k;
+  const void* src_v;
+  const void* k_new;
+  const void* v_new;
+  void* k_cache;
+  void* v_cache;
+} sx_layer_kv;
+
+/* sx_realign_scatter for n_layers layers that share the plan and the row set R (the sparse layers
+ * of a hybrid stack after the boundary selection, Section 3.4), batched into as few launches as
+ * possible, as the paper re-aligns a whole batch's reused blocks at once (Section 3.1, Algorithm 1
+ * step 6).  `layers` is a HOST array of n_layers entries, read during the call only; the buffers
+ * it names are device memory.  Each entry is validated as in sx_realign_scatter; n_layers == 0 is
+ * a no-op. */
+sx_status sx_realign_scatter_layers(const sx_plan* plan, int32_t n_layers, const sx_layer_kv* layers,
+                                    const int32_t* rows, const int32_t* n_rows, int32_t max_rows, void* stream);
+
 /* Eq. sparseq-attn and Eq. sparseq-score with the cross-head sum of Section 3.2:
  *   scores[off_r + j] = sum_h sum_{i in P_r, i >= j} softmax_j(scale * q[i,h] . K[j, h/(Hq/Hkv)])
  * over the probe rows P_r = I_nr U S_tail of request r, reading keys from k_cache (whatever the

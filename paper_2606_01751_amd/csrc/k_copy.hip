@@ -153,27 +153,36 @@ __global__ __launch_bounds__(256) void fill_u32_kernel(uint32_t* __restrict__ p,
   if (i < n) p[i] = v;
 }
 
-// Re-alignment and KV write in one pass (Algorithm 1 steps 6 and 19-20 for a sparse layer whose
-// row set R is known): every token's cache slot is written once -- the fresh K/V row if the token
-// is in R, else the re-aligned cached row if the token is reused; other tokens are not touched.
-// Work unit as in realign_kernel: VEC RoPE pairs of one head plus 32 bytes of V; with d = 128 and
-// 8 KV heads a wavefront is exactly one token, so the branch is uniform.
+// Per-layer pointers of one launch of the one-pass re-alignment + KV write, passed by value.
+constexpr int kLayersPerLaunch = 16;
+struct LayerTable {
+  sx_layer_kv l[kLayersPerLaunch];
+};
+
+// Re-alignment and KV write in one pass (Algorithm 1 steps 6 and 19-20 for sparse layers whose row
+// set R is known): every token's cache slot is written once -- the fresh K/V row if the token is
+// in R, else the re-aligned cached row if the token is reused; other tokens are not touched.
+// blockIdx.y selects the layer.  Work unit as in realign_kernel: VEC RoPE pairs of one head plus
+// 32 bytes of V; with d = 128 and 8 KV heads a wavefront is exactly one token, so the branch is
+// uniform.
 template <int D, bool BF16, bool NEOX>
 __global__ __launch_bounds__(256) void realign_scatter_kernel(
     const int32_t* __restrict__ tok_slot, const int32_t* __restrict__ tok_ra, const RealignRow* __restrict__ ra,
     const float2* __restrict__ cs, const uint32_t* __restrict__ mark, uint32_t gen, int64_t total,
-    const void* __restrict__ src_k_, const void* __restrict__ src_v_, const void* __restrict__ k_new_,
-    const void* __restrict__ v_new_, void* __restrict__ kc_, void* __restrict__ vc_, int Hkv) {
+    const LayerTable tab, int Hkv) {
   constexpr int ESZ = BF16 ? 2 : 4;
   constexpr int VEC = 16 / ESZ;
   constexpr int UPH = D / (2 * VEC);
-  char* kc = (char*)kc_;
-  char* vc = (char*)vc_;
-  const int units = Hkv * UPH;
-  const int64_t g = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  const int64_t tok = g / units;
-  if (tok >= total) return;
-  const int u = (int)(g - tok * units);
+  const sx_layer_kv& lay = tab.l[blockIdx.y];
+  char* kc = (char*)lay.k_cache;
+  char* vc = (char*)lay.v_cache;
+  // 32-bit indexing: the host guarantees total * units < 2^31
+  const uint32_t units = (uint32_t)(Hkv * UPH);
+  const uint32_t g = blockIdx.x * blockDim.x + threadIdx.x;
+  const uint32_t tok32 = g / units;
+  if (tok32 >= (uint32_t)total) return;
+  const int64_t tok = tok32;
+  const int u = (int)(g - tok32 * units);
   const int head = u / UPH;
   const int ui = u - head * UPH;
   int64_t e0, e1;
@@ -188,8 +197,8 @@ __global__ __launch_bounds__(256) void realign_scatter_kernel(
   const int64_t dof = pool_off(tok_slot[tok], head, Hkv, D) * ESZ;
   if (mark[tok] == gen) {
     // fresh row of a token in R (bit-exact copy)
-    const char* kn = (const char*)k_new_ + (tok * Hkv + head) * D * ESZ;
-    const char* vn = (const char*)v_new_ + (tok * Hkv + head) * D * ESZ;
+    const char* kn = (const char*)lay.k_new + (tok * Hkv + head) * D * ESZ;
+    const char* vn = (const char*)lay.v_new + (tok * Hkv + head) * D * ESZ;
     *(uint4*)(kc + dof + e0 * ESZ) = *(const uint4*)(kn + e0 * ESZ);
     *(uint4*)(kc + dof + e1 * ESZ) = *(const uint4*)(kn + e1 * ESZ);
     *(uint4*)(vc + dof + v0 * ESZ) = *(const uint4*)(vn + v0 * ESZ);
@@ -199,8 +208,8 @@ __global__ __launch_bounds__(256) void realign_scatter_kernel(
   const int32_t ri = tok_ra[tok];
   if (ri < 0) return;   // uncached and not listed: left as it is
   const RealignRow rr = ra[ri];
-  const char* src_k = (const char*)src_k_;
-  const char* src_v = (const char*)src_v_;
+  const char* src_k = (const char*)lay.src_k;
+  const char* src_v = (const char*)lay.src_v;
   const int64_t so = pool_off(rr.src_slot, head, Hkv, D) * ESZ;
   const uint4 ka = *(const uint4*)(src_k + so + e0 * ESZ);
   const uint4 kb = *(const uint4*)(src_k + so + e1 * ESZ);
@@ -279,20 +288,27 @@ hipError_t launch_scatter(const sx_plan* p, const void* k_new, const void* v_new
 }
 
 template <int D, bool BF16, bool NEOX>
-hipError_t realign_scatter_dispatch(const sx_plan* p, const void* sk, const void* sv, const void* kn,
-                                   const void* vn, void* kc, void* vc, uint32_t gen, hipStream_t s) {
+hipError_t realign_scatter_dispatch(const sx_plan* p, int32_t n_layers, const sx_layer_kv* layers, uint32_t gen,
+                                   hipStream_t s) {
   constexpr int VEC = BF16 ? 8 : 4;
   const int units = p->desc.n_kv_heads * (D / (2 * VEC));
   const int64_t threads = p->total * units;
-  hipLaunchKernelGGL((realign_scatter_kernel<D, BF16, NEOX>), dim3((unsigned)((threads + 255) / 256)), dim3(256), 0,
-                     s, p->d_tok_slot, p->d_tok_ra, p->d_ra, p->d_cs, p->d_rmark, gen, p->total, sk, sv, kn, vn, kc,
-                     vc, p->desc.n_kv_heads);
-  return hipGetLastError();
+  for (int32_t l0 = 0; l0 < n_layers; l0 += kLayersPerLaunch) {
+    const int nl = n_layers - l0 < kLayersPerLaunch ? n_layers - l0 : kLayersPerLaunch;
+    LayerTable tab{};
+    for (int i = 0; i < nl; ++i) tab.l[i] = layers[l0 + i];
+    hipLaunchKernelGGL((realign_scatter_kernel<D, BF16, NEOX>), dim3((unsigned)((threads + 255) / 256), (unsigned)nl),
+                       dim3(256), 0, s, p->d_tok_slot, p->d_tok_ra, p->d_ra, p->d_cs, p->d_rmark, gen, p->total, tab,
+                       p->desc.n_kv_heads);
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  return hipSuccess;
 }
 
-hipError_t launch_realign_scatter(const sx_plan* p, const void* sk, const void* sv, const void* kn, const void* vn,
-                                  const int32_t* rows, const int32_t* n_rows, int32_t max_rows, void* kc, void* vc,
-                                  uint32_t gen, bool clear_marks, hipStream_t s) {
+hipError_t launch_realign_scatter(const sx_plan* p, int32_t n_layers, const sx_layer_kv* layers, const int32_t* rows,
+                                  const int32_t* n_rows, int32_t max_rows, uint32_t gen, bool clear_marks,
+                                  hipStream_t s) {
   if (clear_marks) {
     hipLaunchKernelGGL(fill_u32_kernel, dim3((unsigned)((p->total + 255) / 256)), dim3(256), 0, s, p->d_rmark,
                        p->total, 0u);
@@ -307,7 +323,7 @@ hipError_t launch_realign_scatter(const sx_plan* p, const void* sk, const void* 
   }
   const bool bf16 = p->desc.dtype == SX_BF16;
   const bool neox = p->desc.rope_style == SX_ROPE_NEOX;
-#define SX_RS(D_, B_, N_) return realign_scatter_dispatch<D_, B_, N_>(p, sk, sv, kn, vn, kc, vc, gen, s)
+#define SX_RS(D_, B_, N_) return realign_scatter_dispatch<D_, B_, N_>(p, n_layers, layers, gen, s)
   if (p->desc.head_dim == 128) {
     if (bf16) { if (neox) SX_RS(128, true, true); else SX_RS(128, true, false); }
     else { if (neox) SX_RS(128, false, true); else SX_RS(128, false, false); }

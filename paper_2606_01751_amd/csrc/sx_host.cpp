@@ -363,23 +363,38 @@ sx_status sx_kv_scatter(const sx_plan* p, const void* k_new, const void* v_new, 
                       "sx_kv_scatter launch");
 }
 
-sx_status sx_realign_scatter(const sx_plan* p, const void* src_k, const void* src_v, const void* k_new,
-                             const void* v_new, const int32_t* rows, const int32_t* n_rows, int32_t max_rows,
-                             void* k_cache, void* v_cache, void* stream) {
+sx_status sx_realign_scatter_layers(const sx_plan* p, int32_t n_layers, const sx_layer_kv* layers,
+                                    const int32_t* rows, const int32_t* n_rows, int32_t max_rows, void* stream) {
   if (!p) return fail(SX_EINVAL, "plan is NULL");
-  if (!k_new || !v_new || !k_cache || !v_cache || !rows || !n_rows) return fail(SX_EINVAL, "NULL argument");
-  if (p->n_realign > 0 && (!src_k || !src_v)) return fail(SX_EINVAL, "NULL source pool");
+  if (n_layers < 0) return fail(SX_EINVAL, "n_layers must be >= 0");
+  if (n_layers > 0 && !layers) return fail(SX_EINVAL, "layers is NULL");
+  if (!rows || !n_rows) return fail(SX_EINVAL, "NULL row list");
   if (max_rows < 0) return fail(SX_EINVAL, "max_rows must be >= 0");
-  if (p->total == 0) return SX_OK;
+  for (int32_t l = 0; l < n_layers; ++l) {
+    const sx_layer_kv& x = layers[l];
+    if (!x.k_new || !x.v_new || !x.k_cache || !x.v_cache) return fail(SX_EINVAL, "layer %d: NULL tensor", l);
+    if (p->n_realign > 0 && (!x.src_k || !x.src_v)) return fail(SX_EINVAL, "layer %d: NULL source pool", l);
+  }
+  if (p->total == 0 || n_layers == 0) return SX_OK;
+  const int64_t units = (int64_t)p->desc.n_kv_heads * p->desc.head_dim * (p->desc.dtype == SX_BF16 ? 2 : 4) / 32;
+  if (p->total * units >= ((int64_t)1 << 31))
+    return fail(SX_EUNSUPPORTED, "%lld tokens x %lld units exceed one launch", (long long)p->total, (long long)units);
   // a new generation for this call's row set; on wrap-around every mark is cleared first
   bool clear = false;
   if (++p->rgen == 0) {
     p->rgen = 1;
     clear = true;
   }
-  return check_launch(sx::launch_realign_scatter(p, src_k, src_v, k_new, v_new, rows, n_rows, max_rows, k_cache,
-                                                 v_cache, p->rgen, clear, (hipStream_t)stream),
+  return check_launch(sx::launch_realign_scatter(p, n_layers, layers, rows, n_rows, max_rows, p->rgen, clear,
+                                                 (hipStream_t)stream),
                       "sx_realign_scatter launch");
+}
+
+sx_status sx_realign_scatter(const sx_plan* p, const void* src_k, const void* src_v, const void* k_new,
+                             const void* v_new, const int32_t* rows, const int32_t* n_rows, int32_t max_rows,
+                             void* k_cache, void* v_cache, void* stream) {
+  const sx_layer_kv one{src_k, src_v, k_new, v_new, k_cache, v_cache};
+  return sx_realign_scatter_layers(p, 1, &one, rows, n_rows, max_rows, stream);
 }
 
 sx_status sx_sparseq_score(const sx_plan* p, const void* q, const void* k_cache, const float* lse_in, float* scores,

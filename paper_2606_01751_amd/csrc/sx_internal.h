@@ -82,11 +82,12 @@ hipError_t launch_realign(const sx_plan* p, const void* src_k, const void* src_v
 hipError_t launch_scatter(const sx_plan* p, const void* k_new, const void* v_new, const int32_t* rows,
                           const int32_t* n_rows, int32_t max_rows, void* kc, void* vc, hipStream_t s);
 hipError_t launch_head_reduce(const sx_plan* p, float* scores, hipStream_t s);
-// fused re-alignment + KV write: marks the rows with `gen` (after clearing every mark when
-// clear_marks), then writes every token's slot once
-hipError_t launch_realign_scatter(const sx_plan* p, const void* sk, const void* sv, const void* kn, const void* vn,
-                                  const int32_t* rows, const int32_t* n_rows, int32_t max_rows, void* kc, void* vc,
-                                  uint32_t gen, bool clear_marks, hipStream_t s);
+// fused re-alignment + KV write of n_layers layers (host array of per-layer pointers): marks the
+// rows with `gen` (after clearing every mark when clear_marks), then writes every token's slot of
+// every layer once
+hipError_t launch_realign_scatter(const sx_plan* p, int32_t n_layers, const sx_layer_kv* layers, const int32_t* rows,
+                                  const int32_t* n_rows, int32_t max_rows, uint32_t gen, bool clear_marks,
+                                  hipStream_t s);
 hipError_t launch_topk(const sx_plan* p, const float* scores, double ratio, int32_t* rows, int32_t* n_rows,
                        hipStream_t s);
 

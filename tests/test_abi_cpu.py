@@ -107,6 +107,7 @@ def test_null_arguments_are_rejected():
     assert L.sx_sparse_attn(None, None, None, None, 1, None, None, None, None) == sx.SX_EINVAL
     assert L.sx_kv_scatter(None, None, None, None, None, 1, None, None, None) == sx.SX_EINVAL
     assert L.sx_realign_scatter(None, None, None, None, None, None, None, 1, None, None, None) == sx.SX_EINVAL
+    assert L.sx_realign_scatter_layers(None, 1, None, None, None, 1, None) == sx.SX_EINVAL
     d = _desc()
     assert L.sx_full_attn(ctypes.byref(d), None, None, None, None, 1, 1, None, None, None) == sx.SX_EINVAL
     assert L.sx_plan_destroy(None) == sx.SX_OK

@@ -155,6 +155,45 @@ def test_fused_realign_scatter_matches_oracle(name, w):
 
 
 @pytest.mark.parametrize("name,w", CASES, ids=IDS)
+def test_realign_scatter_layers_matches_per_layer(name, w):
+    """The batched call over 18 layers (two launches of at most 16 layers) writes every layer's
+    cache exactly as 18 single-layer calls do; the first and the last layer also against the oracle."""
+    log(f"[realign_scatter_layers] {name}")
+    nl = 18
+    ts = [W.layer_tensors(w, l) for l in range(nl)]
+    g = GpuLayer(w, ts[0])
+    rng = np.random.default_rng(23)
+    sets = [np.unique(np.concatenate([O.nonreuse_positions(r.n_tokens, r.segments),
+                                      rng.choice(r.n_tokens, size=r.n_tokens // 4, replace=False)]))
+            for r in w.requests]
+    g.set_rows(sets)
+    m = max(len(s) for s in sets)
+    dt = tdtype(w)
+    lay = [{k: dev(t[k], w) for k in ("k_src", "v_src", "k", "v")} for t in ts]
+    shape = g.k_cache.shape
+    for x in lay:
+        for c in ("kc", "vc", "kc1", "vc1"):
+            x[c] = torch.full(shape, CANARY, dtype=dt, device="cuda")
+    sx.realign_scatter_layers(g.plan, [(x["k_src"], x["v_src"], x["k"], x["v"], x["kc"], x["vc"]) for x in lay],
+                              g.rows, g.n_rows, m)
+    for x in lay:
+        sx.realign_scatter(g.plan, x["k_src"], x["v_src"], x["k"], x["v"], g.rows, g.n_rows, m, x["kc1"], x["vc1"])
+    sx.realign_scatter_layers(g.plan, [], g.rows, g.n_rows, m)   # no layers: no-op
+    torch.cuda.synchronize()
+    for l, x in enumerate(lay):
+        assert torch.equal(x["kc"], x["kc1"]) and torch.equal(x["vc"], x["vc1"]), f"layer {l}"
+    offs = w.token_offsets
+    tol = 1e-2 if w.dtype == "bf16" else 1e-5
+    for l in (0, nl - 1):
+        kp, vp = oracle_pool(w), oracle_pool(w)
+        for r, req in enumerate(w.requests):
+            O.realign_request(req, w, ts[l]["k_src"], ts[l]["v_src"], kp, vp)
+            O.scatter_rows(req, w, sets[r], ts[l]["k"][offs[r]:offs[r + 1]], ts[l]["v"][offs[r]:offs[r + 1]], kp, vp)
+        assert np.abs(host(lay[l]["kc"]) - kp).max() <= tol
+        assert np.array_equal(host(lay[l]["vc"]), vp)
+
+
+@pytest.mark.parametrize("name,w", CASES, ids=IDS)
 def test_full_attention_matches_oracle(name, w):
     log(f"[full_attn] {name}")
     t = W.layer_tensors(w, 0)
