@@ -50,10 +50,12 @@ def parse():
     ap.add_argument("--score-passes", type=int, choices=(1, 2), default=1,
                     help="Sparse-Q scoring in hybrid stacks: 1 = denominators from the boundary layer's full "
                          "attention (exact-logit variant), 2 = own log-sum-exp pass")
-    ap.add_argument("--kv-write", choices=("per-layer", "all-layers", "separate"), default="per-layer",
+    ap.add_argument("--kv-write", choices=("per-layer", "per-layer-rows", "all-layers", "separate"),
+                    default="per-layer",
                     help="sparse layers' re-alignment + KV write of R: one pass per layer just before its "
-                         "attention (default; the attention then finds part of the cache in the Infinity Cache), "
-                         "one pass for all sparse layers after the selection, or two passes per layer")
+                         "attention with R as a byte mask built once per step (default; the attention then finds "
+                         "part of the cache in the Infinity Cache), the same from the row list (marks R per "
+                         "layer), one pass for all sparse layers after the selection, or two passes per layer")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
                     help="also run a plain device copy of BYTES bytes (reference for HBM byte counters)")
     ap.add_argument("--record-traffic", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
@@ -73,8 +75,10 @@ KERNELS = {
     "head_reduce_kernel": ("sx_sparseq_score", "k_copy.hip"),
     "realign_kernel": ("sx_rope_realign", "k_copy.hip"),
     "scatter_kernel": ("sx_kv_scatter", "k_copy.hip"),
-    "realign_scatter_kernel": ("sx_realign_scatter", "k_copy.hip"),
+    "realign_scatter_kernel": ("sx_realign_scatter_masked", "k_copy.hip"),   # (also the row-list variants)
     "mark_rows_kernel": ("sx_realign_scatter", "k_copy.hip"),   # (also sx_realign_scatter_layers)
+    "fill_u8_kernel": ("sx_rows_mask", "k_copy.hip"),
+    "mask_rows_kernel": ("sx_rows_mask", "k_copy.hip"),
     "topk_kernel": ("sx_topk_select", "k_topk.hip"),
 }
 
@@ -213,6 +217,7 @@ def main():
         layers.append(tl)
     out = torch.empty((T, Hq, d), dtype=dt, device="cuda")
     lse = torch.empty((T, Hq), dtype=torch.float32, device="cuda")   # boundary layer's denominators
+    rmask = torch.zeros(T, dtype=torch.uint8, device="cuda")           # R as a byte mask
     scores = torch.zeros(T, dtype=torch.float32, device="cuda")
     rows = torch.zeros(T, dtype=torch.int32, device="cuda")
     n_rows = torch.zeros(len(w.requests), dtype=torch.int32, device="cuda")
@@ -248,6 +253,8 @@ def main():
                                                             lse_in=lse if (nfull > 0 and args.score_passes == 1)
                                                             else None))
         tm.run("sx_topk_select", lambda: sx.topk_select(plan, scores, ratio, rows, n_rows))
+        if args.kv_write == "per-layer" and L > max(nfull, 1):
+            tm.run("sx_rows_mask", lambda: sx.rows_mask(plan, rows, n_rows, max_rows, rmask))
         if args.kv_write == "all-layers" and sparse_kv:
             # every sparse layer's cache in one call (two launches of at most 16 layers)
             tm.run("sx_realign_scatter_layers",
@@ -265,8 +272,12 @@ def main():
                        lambda: sx.rope_realign(plan, tl["k_src"], tl["v_src"], tl["kc"], tl["vc"]))
                 tm.run("sx_kv_scatter", lambda: sx.kv_scatter(plan, tl["k"], tl["v"], tl["kc"], tl["vc"], rows=rows,
                                                               n_rows=n_rows, max_rows=max_rows))
-            else:
+            elif args.kv_write == "per-layer":
                 # one pass: each slot gets either its fresh row (token in R) or its re-aligned cached row
+                tm.run("sx_realign_scatter_masked",
+                       lambda: sx.realign_scatter_masked(plan, tl["k_src"], tl["v_src"], tl["k"], tl["v"], rmask,
+                                                         tl["kc"], tl["vc"]))
+            else:
                 tm.run("sx_realign_scatter",
                        lambda: sx.realign_scatter(plan, tl["k_src"], tl["v_src"], tl["k"], tl["v"], rows, n_rows,
                                                   max_rows, tl["kc"], tl["vc"]))
@@ -330,7 +341,9 @@ def main():
     # read once and written once (K and V)
     n_R_uncached = int(sum(np.count_nonzero(~req.cached_mask()[Rr]) for req, Rr in zip(w.requests, R)))
     work["sx_realign_scatter"] = ("hbm", 4.0 * row_bytes * (info["n_reused"] + n_R_uncached))
+    work["sx_realign_scatter_masked"] = work["sx_realign_scatter"]
     work["sx_realign_scatter_layers"] = ("hbm", len(sparse_kv) * work["sx_realign_scatter"][1])
+    work["sx_rows_mask"] = ("latency", T + 4.0 * n_R)
     peak = PEAK_BF16_TFLOPS if w.dtype == "bf16" else PEAK_F32_TFLOPS
     kernels = {}
     for name, k in kern.items():

@@ -196,6 +196,26 @@ typedef struct {
 sx_status sx_realign_scatter_layers(const sx_plan* plan, int32_t n_layers, const sx_layer_kv* layers,
                                     const int32_t* rows, const int32_t* n_rows, int32_t max_rows, void* stream);
 
+/* Per-token byte mask of a row list (the recompute set R that sx_topk_select writes), for
+ * sx_realign_scatter_masked: mask[off_r + t] = 1 for every listed row t of request r
+ * (rows[off_r .. off_r + min(n_rows[r], max_rows))), 0 for every other token of the plan.
+ * mask is caller-owned DEVICE memory of sum T bytes; rows/n_rows/max_rows as in sx_kv_scatter.
+ * Listed values outside [0, T_r) are ignored.  Two kernels on `stream`, no host sync. */
+sx_status sx_rows_mask(const sx_plan* plan, const int32_t* rows, const int32_t* n_rows, int32_t max_rows,
+                       uint8_t* mask, void* stream);
+
+/* sx_realign_scatter with R given as a per-token byte mask (sx_rows_mask): the slot of every token
+ * with mask[off_r + t] != 0 gets k_new/v_new (bit-exact), the slot of every other reused token its
+ * re-aligned cached K and V (Section 3.1, Algorithm 1 steps 6 and 19-20); other tokens are not
+ * touched.  One kernel, each slot read and written once.  The mask is built once for the sparse
+ * layers that share R (Section 3.4), so no per-layer marking pass is needed, and nothing of the
+ * plan is written: calls sharing a plan may run concurrently on different streams when their
+ * caches differ.  mask: DEVICE [sum T] bytes; src_k/src_v may be NULL only when no segment is
+ * cached. */
+sx_status sx_realign_scatter_masked(const sx_plan* plan, const void* src_k, const void* src_v, const void* k_new,
+                                    const void* v_new, const uint8_t* mask, void* k_cache, void* v_cache,
+                                    void* stream);
+
 /* Eq. sparseq-attn and Eq. sparseq-score with the cross-head sum of Section 3.2:
  *   scores[off_r + j] = sum_h sum_{i in P_r, i >= j} softmax_j(scale * q[i,h] . K[j, h/(Hq/Hkv)])
  * over the probe rows P_r = I_nr U S_tail of request r, reading keys from k_cache (whatever the

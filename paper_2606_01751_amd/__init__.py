@@ -24,7 +24,7 @@ from typing import Optional, Sequence
 
 __all__ = [
     "LIB_PATH", "SxError", "lib", "LayerDesc", "Plan", "rope_realign", "kv_scatter", "realign_scatter",
-    "realign_scatter_layers", "sparseq_score",
+    "realign_scatter_layers", "rows_mask", "realign_scatter_masked", "sparseq_score",
     "topk_select", "sparse_attn", "full_attn", "F32", "BF16", "ROPE_NEOX", "ROPE_GPTJ", "EXPORTED",
 ]
 
@@ -36,7 +36,8 @@ SX_OK, SX_EINVAL, SX_ESHAPE, SX_EUNSUPPORTED, SX_EHIP, SX_ENOMEM = 0, -1, -2, -3
 
 EXPORTED = (
     "sx_plan_create", "sx_plan_destroy", "sx_plan_get_info", "sx_plan_budget", "sx_plan_nonreused_rows",
-    "sx_rope_realign", "sx_kv_scatter", "sx_realign_scatter", "sx_realign_scatter_layers", "sx_sparseq_score", "sx_topk_select",
+    "sx_rope_realign", "sx_kv_scatter", "sx_realign_scatter", "sx_realign_scatter_layers", "sx_rows_mask",
+    "sx_realign_scatter_masked", "sx_sparseq_score", "sx_topk_select",
     "sx_sparse_attn", "sx_full_attn", "sx_last_error", "sx_version",
 )
 
@@ -97,6 +98,8 @@ def lib() -> ctypes.CDLL:
         L.sx_kv_scatter.argtypes = [VP, VP, VP, VP, VP, I32, VP, VP, VP]
         L.sx_realign_scatter.argtypes = [VP, VP, VP, VP, VP, VP, VP, I32, VP, VP, VP]
         L.sx_realign_scatter_layers.argtypes = [VP, I32, VP, VP, VP, I32, VP]
+        L.sx_rows_mask.argtypes = [VP, VP, VP, I32, VP, VP]
+        L.sx_realign_scatter_masked.argtypes = [VP, VP, VP, VP, VP, VP, VP, VP, VP]
         L.sx_sparseq_score.argtypes = [VP, VP, VP, VP, VP, VP]
         L.sx_topk_select.argtypes = [VP, VP, D, VP, VP, VP]
         L.sx_sparse_attn.argtypes = [VP, VP, VP, VP, I32, VP, VP, VP, VP]
@@ -232,6 +235,16 @@ def realign_scatter_layers(plan: Plan, layers, rows, n_rows, max_rows: int, stre
         arr[i] = _LayerKV(*(_ptr(x) for x in t))
     _check(lib().sx_realign_scatter_layers(plan.handle, len(layers), ctypes.cast(arr, ctypes.c_void_p), _ptr(rows),
                                            _ptr(n_rows), int(max_rows), _stream(stream)))
+
+
+def rows_mask(plan: Plan, rows, n_rows, max_rows: int, mask, stream=None):
+    """mask (uint8, sum T) = 1 on the listed rows, 0 elsewhere."""
+    _check(lib().sx_rows_mask(plan.handle, _ptr(rows), _ptr(n_rows), int(max_rows), _ptr(mask), _stream(stream)))
+
+
+def realign_scatter_masked(plan: Plan, src_k, src_v, k_new, v_new, mask, k_cache, v_cache, stream=None):
+    _check(lib().sx_realign_scatter_masked(plan.handle, _ptr(src_k), _ptr(src_v), _ptr(k_new), _ptr(v_new),
+                                           _ptr(mask), _ptr(k_cache), _ptr(v_cache), _stream(stream)))
 
 
 def sparseq_score(plan: Plan, q, k_cache, scores, lse_in=None, stream=None):

@@ -153,6 +153,22 @@ __global__ __launch_bounds__(256) void fill_u32_kernel(uint32_t* __restrict__ p,
   if (i < n) p[i] = v;
 }
 
+__global__ __launch_bounds__(256) void fill_u8_kernel(uint8_t* __restrict__ p, int64_t n, uint8_t v) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n) p[i] = v;
+}
+
+// Sets mask[off_r + t] = 1 for every listed row t of every request (the mask was cleared first).
+__global__ __launch_bounds__(256) void mask_rows_kernel(const ReqDev* __restrict__ reqs, const int32_t* __restrict__ rows,
+                                                        const int32_t* __restrict__ n_rows, int max_rows,
+                                                        uint8_t* __restrict__ mask) {
+  const ReqDev rq = reqs[blockIdx.y];
+  const int idx = blockIdx.x * blockDim.x + threadIdx.x;
+  if (idx >= max_rows || idx >= n_rows[blockIdx.y]) return;
+  const int t = rows[rq.tok_off + idx];
+  if (t >= 0 && t < rq.T) mask[rq.tok_off + t] = 1;
+}
+
 // Per-layer pointers of one launch of the one-pass re-alignment + KV write, passed by value.
 constexpr int kLayersPerLaunch = 16;
 struct LayerTable {
@@ -165,11 +181,13 @@ struct LayerTable {
 // blockIdx.y selects the layer.  Work unit as in realign_kernel: VEC RoPE pairs of one head plus
 // 32 bytes of V; with d = 128 and 8 KV heads a wavefront is exactly one token, so the branch is
 // uniform.
-template <int D, bool BF16, bool NEOX>
+// Membership of a token in R: MASK = a caller's byte mask (nonzero = in R), else the plan's
+// generation marks (mark == gen).
+template <int D, bool BF16, bool NEOX, bool MASK>
 __global__ __launch_bounds__(256) void realign_scatter_kernel(
     const int32_t* __restrict__ tok_slot, const int32_t* __restrict__ tok_ra, const RealignRow* __restrict__ ra,
-    const float2* __restrict__ cs, const uint32_t* __restrict__ mark, uint32_t gen, int64_t total,
-    const LayerTable tab, int Hkv) {
+    const float2* __restrict__ cs, const uint32_t* __restrict__ mark, const uint8_t* __restrict__ sel, uint32_t gen,
+    int64_t total, const LayerTable tab, int Hkv) {
   constexpr int ESZ = BF16 ? 2 : 4;
   constexpr int VEC = 16 / ESZ;
   constexpr int UPH = D / (2 * VEC);
@@ -195,7 +213,7 @@ __global__ __launch_bounds__(256) void realign_scatter_kernel(
   }
   const int64_t v0 = (int64_t)ui * 2 * VEC;
   const int64_t dof = pool_off(tok_slot[tok], head, Hkv, D) * ESZ;
-  if (mark[tok] == gen) {
+  if (MASK ? sel[tok] != 0 : mark[tok] == gen) {
     // fresh row of a token in R (bit-exact copy)
     const char* kn = (const char*)lay.k_new + (tok * Hkv + head) * D * ESZ;
     const char* vn = (const char*)lay.v_new + (tok * Hkv + head) * D * ESZ;
@@ -289,7 +307,7 @@ hipError_t launch_scatter(const sx_plan* p, const void* k_new, const void* v_new
 
 template <int D, bool BF16, bool NEOX>
 hipError_t realign_scatter_dispatch(const sx_plan* p, int32_t n_layers, const sx_layer_kv* layers, uint32_t gen,
-                                   hipStream_t s) {
+                                   const uint8_t* sel, hipStream_t s) {
   constexpr int VEC = BF16 ? 8 : 4;
   const int units = p->desc.n_kv_heads * (D / (2 * VEC));
   const int64_t threads = p->total * units;
@@ -297,18 +315,38 @@ hipError_t realign_scatter_dispatch(const sx_plan* p, int32_t n_layers, const sx
     const int nl = n_layers - l0 < kLayersPerLaunch ? n_layers - l0 : kLayersPerLaunch;
     LayerTable tab{};
     for (int i = 0; i < nl; ++i) tab.l[i] = layers[l0 + i];
-    hipLaunchKernelGGL((realign_scatter_kernel<D, BF16, NEOX>), dim3((unsigned)((threads + 255) / 256), (unsigned)nl),
-                       dim3(256), 0, s, p->d_tok_slot, p->d_tok_ra, p->d_ra, p->d_cs, p->d_rmark, gen, p->total, tab,
-                       p->desc.n_kv_heads);
+    const dim3 grid((unsigned)((threads + 255) / 256), (unsigned)nl);
+    if (sel)
+      hipLaunchKernelGGL((realign_scatter_kernel<D, BF16, NEOX, true>), grid, dim3(256), 0, s, p->d_tok_slot,
+                         p->d_tok_ra, p->d_ra, p->d_cs, p->d_rmark, sel, gen, p->total, tab, p->desc.n_kv_heads);
+    else
+      hipLaunchKernelGGL((realign_scatter_kernel<D, BF16, NEOX, false>), grid, dim3(256), 0, s, p->d_tok_slot,
+                         p->d_tok_ra, p->d_ra, p->d_cs, p->d_rmark, sel, gen, p->total, tab, p->desc.n_kv_heads);
     const hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
   return hipSuccess;
 }
 
+hipError_t launch_rows_mask(const sx_plan* p, const int32_t* rows, const int32_t* n_rows, int32_t max_rows,
+                            uint8_t* mask, hipStream_t s) {
+  hipLaunchKernelGGL(fill_u8_kernel, dim3((unsigned)((p->total + 255) / 256)), dim3(256), 0, s, mask, p->total,
+                     (uint8_t)0);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess || max_rows <= 0) return e;
+  hipLaunchKernelGGL(mask_rows_kernel, dim3((unsigned)((max_rows + 255) / 256), (unsigned)p->n_req), dim3(256), 0, s,
+                     p->d_req, rows, n_rows, max_rows, mask);
+  return hipGetLastError();
+}
+
 hipError_t launch_realign_scatter(const sx_plan* p, int32_t n_layers, const sx_layer_kv* layers, const int32_t* rows,
                                   const int32_t* n_rows, int32_t max_rows, uint32_t gen, bool clear_marks,
-                                  hipStream_t s) {
+                                  const uint8_t* sel, hipStream_t s) {
+  if (sel) {
+    rows = nullptr;   // membership comes from the caller's mask
+    max_rows = 0;
+    clear_marks = false;
+  }
   if (clear_marks) {
     hipLaunchKernelGGL(fill_u32_kernel, dim3((unsigned)((p->total + 255) / 256)), dim3(256), 0, s, p->d_rmark,
                        p->total, 0u);
@@ -323,7 +361,7 @@ hipError_t launch_realign_scatter(const sx_plan* p, int32_t n_layers, const sx_l
   }
   const bool bf16 = p->desc.dtype == SX_BF16;
   const bool neox = p->desc.rope_style == SX_ROPE_NEOX;
-#define SX_RS(D_, B_, N_) return realign_scatter_dispatch<D_, B_, N_>(p, n_layers, layers, gen, s)
+#define SX_RS(D_, B_, N_) return realign_scatter_dispatch<D_, B_, N_>(p, n_layers, layers, gen, sel, s)
   if (p->desc.head_dim == 128) {
     if (bf16) { if (neox) SX_RS(128, true, true); else SX_RS(128, true, false); }
     else { if (neox) SX_RS(128, false, true); else SX_RS(128, false, false); }

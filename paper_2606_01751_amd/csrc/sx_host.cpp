@@ -386,8 +386,34 @@ sx_status sx_realign_scatter_layers(const sx_plan* p, int32_t n_layers, const sx
     clear = true;
   }
   return check_launch(sx::launch_realign_scatter(p, n_layers, layers, rows, n_rows, max_rows, p->rgen, clear,
-                                                 (hipStream_t)stream),
+                                                 nullptr, (hipStream_t)stream),
                       "sx_realign_scatter launch");
+}
+
+sx_status sx_rows_mask(const sx_plan* p, const int32_t* rows, const int32_t* n_rows, int32_t max_rows, uint8_t* mask,
+                       void* stream) {
+  if (!p) return fail(SX_EINVAL, "plan is NULL");
+  if (!rows || !n_rows || !mask) return fail(SX_EINVAL, "NULL argument");
+  if (max_rows < 0) return fail(SX_EINVAL, "max_rows must be >= 0");
+  if (p->total == 0) return SX_OK;
+  return check_launch(sx::launch_rows_mask(p, rows, n_rows, max_rows, mask, (hipStream_t)stream),
+                      "sx_rows_mask launch");
+}
+
+sx_status sx_realign_scatter_masked(const sx_plan* p, const void* src_k, const void* src_v, const void* k_new,
+                                    const void* v_new, const uint8_t* mask, void* k_cache, void* v_cache,
+                                    void* stream) {
+  if (!p) return fail(SX_EINVAL, "plan is NULL");
+  if (!mask) return fail(SX_EINVAL, "mask is NULL");
+  if (!k_new || !v_new || !k_cache || !v_cache) return fail(SX_EINVAL, "NULL tensor argument");
+  if (p->n_realign > 0 && (!src_k || !src_v)) return fail(SX_EINVAL, "NULL source pool");
+  if (p->total == 0) return SX_OK;
+  const int64_t units = (int64_t)p->desc.n_kv_heads * p->desc.head_dim * (p->desc.dtype == SX_BF16 ? 2 : 4) / 32;
+  if (p->total * units >= ((int64_t)1 << 31))
+    return fail(SX_EUNSUPPORTED, "%lld tokens x %lld units exceed one launch", (long long)p->total, (long long)units);
+  const sx_layer_kv one{src_k, src_v, k_new, v_new, k_cache, v_cache};
+  return check_launch(sx::launch_realign_scatter(p, 1, &one, nullptr, nullptr, 0, 0, false, mask, (hipStream_t)stream),
+                      "sx_realign_scatter_masked launch");
 }
 
 sx_status sx_realign_scatter(const sx_plan* p, const void* src_k, const void* src_v, const void* k_new,

@@ -85,9 +85,13 @@ hipError_t launch_head_reduce(const sx_plan* p, float* scores, hipStream_t s);
 // fused re-alignment + KV write of n_layers layers (host array of per-layer pointers): marks the
 // rows with `gen` (after clearing every mark when clear_marks), then writes every token's slot of
 // every layer once
+// (sel != null: membership in R from the caller's byte mask instead; rows, gen and clear_marks unused)
 hipError_t launch_realign_scatter(const sx_plan* p, int32_t n_layers, const sx_layer_kv* layers, const int32_t* rows,
                                   const int32_t* n_rows, int32_t max_rows, uint32_t gen, bool clear_marks,
-                                  hipStream_t s);
+                                  const uint8_t* sel, hipStream_t s);
+// mask[off_r + t] = 1 for every listed row t, 0 for every other token of the plan
+hipError_t launch_rows_mask(const sx_plan* p, const int32_t* rows, const int32_t* n_rows, int32_t max_rows,
+                            uint8_t* mask, hipStream_t s);
 hipError_t launch_topk(const sx_plan* p, const float* scores, double ratio, int32_t* rows, int32_t* n_rows,
                        hipStream_t s);
 

@@ -109,7 +109,9 @@ def test_c3_boundary_selection_and_layers():
     q, k, v, ks, vs = (dev(t[n], w) for n in ("q", "k", "v", "k_src", "v_src"))
     kc, vc = _pool(w, dt), _pool(w, dt)
     out = torch.zeros_like(q)
-    sx.realign_scatter(plan, ks, vs, k, v, rows, n_rows, max_rows, kc, vc)
+    mask = torch.zeros(T, dtype=torch.uint8, device="cuda")
+    sx.rows_mask(plan, rows, n_rows, max_rows, mask)
+    sx.realign_scatter_masked(plan, ks, vs, k, v, mask, kc, vc)
     sx.sparse_attn(plan, q, rows, n_rows, max_rows, kc, vc, out)
     torch.cuda.synchronize()
     kp = np.zeros((w.n_dst_blocks, w.n_kv_heads, w.block_size, w.head_dim), np.float32)

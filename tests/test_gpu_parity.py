@@ -121,6 +121,8 @@ def test_fused_realign_scatter_matches_oracle(name, w):
     t = W.layer_tensors(w, 0)
     g = GpuLayer(w, t)
     ref = GpuLayer(w, t)
+    gm = GpuLayer(w, t)     # same pass with R given as a byte mask (sx_rows_mask + sx_realign_scatter_masked)
+    mask = torch.full((w.total_tokens,), 0x55, dtype=torch.uint8, device="cuda")
     rng = np.random.default_rng(17)
     offs = w.token_offsets
     big = [np.unique(np.concatenate([O.nonreuse_positions(r.n_tokens, r.segments),
@@ -131,12 +133,15 @@ def test_fused_realign_scatter_matches_oracle(name, w):
     tol = 1e-2 if w.dtype == "bf16" else 1e-5
     for label, sets in (("I_nr + third", big), ("seventh", small), ("empty", empty)):
         m = max(len(s) for s in sets)
-        for x in (g, ref):
+        for x in (g, ref, gm):
             x.k_cache.fill_(CANARY)
             x.v_cache.fill_(CANARY)
             x.set_rows(sets)
         sx.realign_scatter(g.plan, g.t["k_src"], g.t["v_src"], g.t["k"], g.t["v"], g.rows, g.n_rows, m,
                            g.k_cache, g.v_cache)
+        sx.rows_mask(gm.plan, gm.rows, gm.n_rows, m, mask)
+        sx.realign_scatter_masked(gm.plan, gm.t["k_src"], gm.t["v_src"], gm.t["k"], gm.t["v"], mask,
+                                  gm.k_cache, gm.v_cache)
         ref.realign()
         sx.kv_scatter(ref.plan, ref.t["k"], ref.t["v"], ref.k_cache, ref.v_cache, rows=ref.rows, n_rows=ref.n_rows,
                       max_rows=m)
@@ -144,6 +149,11 @@ def test_fused_realign_scatter_matches_oracle(name, w):
         gk, gv = host(g.k_cache), host(g.v_cache)
         assert np.array_equal(gk, host(ref.k_cache)), label
         assert np.array_equal(gv, host(ref.v_cache)), label
+        want = np.zeros(w.total_tokens, np.uint8)
+        for r in range(len(w.requests)):
+            want[offs[r] + np.asarray(sets[r], np.int64)] = 1
+        assert np.array_equal(mask.cpu().numpy(), want), label
+        assert np.array_equal(host(gm.k_cache), gk) and np.array_equal(host(gm.v_cache), gv), label
         kp, vp = oracle_pool(w), oracle_pool(w)
         for r, req in enumerate(w.requests):
             O.realign_request(req, w, t["k_src"], t["v_src"], kp, vp)
