@@ -65,7 +65,7 @@ typedef __attribute__((address_space(3))) shortx4_t lds_shortx4_t;
 // Scheduling groups (instruction classes of the sched_group_barrier builtin): the next `n`
 // instructions of class `mask` are placed here, in program order of the groups.
 #define SX_SG(mask, n) __builtin_amdgcn_sched_group_barrier(mask, n, 0)
-constexpr int kSgMfma = 0x8, kSgDsRead = 0x100;
+constexpr int kSgValu = 0x2, kSgMfma = 0x8, kSgDsRead = 0x100;
 // Order of a matrix phase of NM MFMAs whose operands come from NR LDS reads each: the reads of
 // the first PRE MFMAs go first, then every MFMA is followed by the reads of the MFMA PRE places
 // later, so each read has PRE MFMAs (32 cycles each) to complete.
@@ -663,6 +663,296 @@ __global__ __launch_bounds__(512, 1) void colsum_mfma_kernel(ColsumK a) {
   }
 }
 
+// Gather of the Sparse-Q probe columns for colsum2_kernel: the query rows of every probe row
+// (all heads) and the base-2 log-sum-exp of every (probe row, query head), in probe order, so
+// that the column-sum kernel computes every address from its registers (no load chains).
+// Thread: one 16-byte piece of one (probe row, head); blockIdx.y = request.
+template <int D>
+__global__ __launch_bounds__(256) void probe_gather_kernel(const uint16_t* __restrict__ q, const float* __restrict__ lse,
+                                                           int lse_tok, const ReqDev* __restrict__ reqs,
+                                                           const int32_t* __restrict__ probe, int Hq, int Hkv,
+                                                           int64_t n_probe_total, uint16_t* __restrict__ qp,
+                                                           float* __restrict__ lse2p) {
+  constexpr int PPH = D * 2 / 16;   // 16-byte pieces per head row
+  const ReqDev rq = reqs[blockIdx.y];
+  const int64_t g = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const int64_t per_row = (int64_t)Hq * PPH;
+  const int64_t i = g / per_row;
+  if (i >= rq.n_probe) return;
+  const int rem = (int)(g - i * per_row);
+  const int h = rem / PPH;
+  const int pc = rem - h * PPH;
+  const int pos = probe[rq.tok_off + i];
+  const int64_t prow = (int64_t)rq.p_off + i;
+  ((uint4*)qp)[(prow * Hq + h) * PPH + pc] = ((const uint4*)q)[((int64_t)(rq.tok_off + pos) * Hq + h) * PPH + pc];
+  if (pc == 0) {
+    const int G = Hq / Hkv;
+    const int kvh = h / G;
+    const float l2 = lse_tok ? lse[(int64_t)(rq.tok_off + pos) * Hq + h] * 1.4426950408889634f
+                             : lse[(int64_t)(rq.tok_off + i) * Hq + h];
+    lse2p[((int64_t)kvh * (n_probe_total + kProbePad) + prow) * G + (h - kvh * G)] = l2;
+  }
+}
+
+// Sparse-Q column sums from the gathered probe columns.  Same key-stationary work split as
+// colsum_mfma_kernel (a workgroup = 256 keys of one KV head, a wave's 32 keys held as the MFMA A
+// operand), but the probe columns stream in chunks of RC probe rows x G heads (at most 64
+// columns, two 32-column MFMA groups) that move global -> LDS directly: the query rows (16 bytes
+// per lane, XOR-swizzled 16-byte chunks), the chunk's 64 log-sum-exps and its RC probe positions
+// (4 bytes per lane), triple-buffered and issued two chunks ahead.  No global load in the loop
+// feeds an address, so the loop waits only for transfers issued two chunks earlier.
+struct Colsum2K {
+  const uint16_t* k;
+  const uint16_t* qp;
+  const float* lse2p;
+  const ReqDev* reqs;
+  const int32_t* bt;
+  const int32_t* probe;
+  double* colsum;
+  int64_t total, n_probe_total;
+  int Hq, Hkv, G, RC, n_req;
+  float scale_log2;
+};
+
+template <int D>
+__global__ __launch_bounds__(512, 1) void colsum2_kernel(Colsum2K a) {
+  constexpr int NW = 8;
+  constexpr int ROWB = D * 2;                 // bytes of one query row (one column)
+  constexpr int NCH = ROWB / 16;              // 16-byte chunks per column
+  constexpr int CPP = 1024 / ROWB;            // columns per 1 KB transfer
+  constexpr int NC = 64;                      // column slots per chunk
+  constexpr int NPC = NC / CPP;               // 1 KB transfers per chunk
+  constexpr int PPW = (NPC + NW - 1) / NW;    // per wave
+  constexpr int QB = NC * ROWB;
+  constexpr int CHB = QB + 512;               // + 64 log-sum-exps + 64 positions
+  constexpr int NBUF = 3;
+  static_assert(NPC % NW == 0, "query transfers spread evenly over the waves");
+  __shared__ __attribute__((aligned(1024))) char smem[NBUF * CHB];
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int w = tid >> 6;
+  const int wu = __builtin_amdgcn_readfirstlane(w);
+  const int l32 = lane & 31;
+  const int hg = lane >> 5;
+  const int kvh = (int)(blockIdx.x % (unsigned)a.Hkv);
+  const int rest = (int)(blockIdx.x / (unsigned)a.Hkv);
+  const ReqDev rq = a.reqs[rest % a.n_req];
+  const int T = rq.T;
+  const int j0 = (rest / a.n_req) * CS_KEYS;
+  if (j0 >= T) return;
+  const int jw = j0 + w * 32;
+  const int G = a.G;
+  const int RC = a.RC;
+  const int ncol = RC * G;                    // columns of a full chunk (<= 64)
+  bf16x8_t ka[D / 16];
+  {
+    const int key = jw + l32;
+    const uint16_t* kp = nullptr;
+    if (key < T) {
+      const int32_t blk = a.bt[rq.bt_off + (key >> 4)];
+      kp = a.k + (((int64_t)blk * a.Hkv + kvh) * 16 + (key & 15)) * D + hg * 8;
+    }
+#pragma unroll
+    for (int s = 0; s < D / 16; ++s) {
+      uint4 v = kp ? *(const uint4*)(kp + 16 * s) : make_uint4(0, 0, 0, 0);
+      ka[s] = __builtin_bit_cast(bf16x8_t, v);
+    }
+  }
+  const int32_t* probe = a.probe + rq.tok_off;
+  const int np = rq.n_probe;
+  int lo = 0, hi = np;
+  while (lo < hi) {
+    const int mid = (lo + hi) >> 1;
+    if (probe[mid] < j0) lo = mid + 1; else hi = mid;
+  }
+  const int nchunk = (np - lo + RC - 1) / RC;
+  // ---- transfers of chunk k into buffer k mod 3 (this wave's share).  Rows past the request's
+  // probe rows read the zeroed padding (at most RC - 1 < kProbePad rows), so no clamping ----
+  // query pieces: slot column qc = CPP * piece + lane / NCH, physical chunk lane % NCH holding
+  // logical chunk (lane % NCH) ^ (qc mod NCH); slot columns past RC * G repeat column RC * G - 1
+  const uint16_t* q_src[PPW];
+#pragma unroll
+  for (int i = 0; i < PPW; ++i) {
+    const int qc = CPP * (wu + NW * i) + lane / NCH;
+    const int cc = min(qc, ncol - 1);
+    const int row = cc / G;
+    const int lc = (lane % NCH) ^ (qc & (NCH - 1));
+    q_src[i] = a.qp + (((int64_t)rq.p_off + lo + row) * a.Hq + kvh * G + (cc - row * G)) * D + lc * 8;
+  }
+  const int m_col = min(lane, ncol - 1);       // log-sum-exp transfer (wave NW-1): column
+  const int m_row = m_col / G;
+  const float* l_src =
+      a.lse2p + ((int64_t)kvh * (a.n_probe_total + kProbePad) + rq.p_off + lo + m_row) * G + (m_col - m_row * G);
+  const int32_t* p_src = probe + lo + lane;   // positions transfer (wave NW-2)
+  const int64_t q_step = (int64_t)RC * a.Hq * D;   // one chunk further
+  const bool lse_wave = wu == NW - 1, pos_wave = wu == NW - 2;
+  const int n_mine = PPW + (lse_wave ? 1 : 0) + (pos_wave ? 1 : 0);
+  auto dma16 = [&](const void* src, const char* dst) {
+    const uint32_t m0 = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) const char*)dst;
+    asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(src), "s"(m0) : "m0");
+  };
+  auto dma4 = [&](const void* src, const char* dst) {
+    const uint32_t m0 = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) const char*)dst;
+    asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dword %0, off" ::"v"(src), "s"(m0) : "m0");
+  };
+  auto issue = [&](int k) {
+    if (k >= nchunk) return;
+    char* b = smem + (k % NBUF) * CHB;
+#pragma unroll
+    for (int i = 0; i < PPW; ++i) dma16(q_src[i] + k * q_step, b + (wu + NW * i) * 1024);
+    if (lse_wave) dma4(l_src + k * RC * G, b + QB);
+    if (pos_wave) dma4(p_src + k * RC, b + QB + 256);
+  };
+  auto wait_vm = [&](int n) {
+    switch (n) {
+      case 0: SX_WAIT_VMCNT(0); break;
+      case 1: SX_WAIT_VMCNT(1); break;
+      case 2: SX_WAIT_VMCNT(2); break;
+      case 3: SX_WAIT_VMCNT(3); break;
+      default: SX_WAIT_VMCNT(4); break;
+    }
+  };
+  static_assert(PPW + 1 <= 4, "transfer count per chunk exceeds the wait table");
+  // chunks whose first probe row lies before the workgroup's last key may miss keys of a wave
+  // (causal mask); the later ones see all 256 keys.  Probe rows ascend, so the masked chunks come
+  // first: nmask of them.
+  int hm = lo, hx = np;
+  while (hm < hx) {
+    const int mid = (hm + hx) >> 1;
+    if (probe[mid] < j0 + CS_KEYS - 1) hm = mid + 1; else hx = mid;
+  }
+  const int nmask = min(nchunk, (hm - lo + RC - 1) / RC);
+
+  // compute lanes: column 32 gi + l32 of a chunk is probe row (32 gi + l32) / G of it
+  int c_row[2];
+#pragma unroll
+  for (int gi = 0; gi < 2; ++gi) c_row[gi] = (32 * gi + l32) / G;
+  double acc64[16];
+  float acc32[16];
+#pragma unroll
+  for (int e = 0; e < 16; ++e) {
+    acc64[e] = 0.0;
+    acc32[e] = 0.f;
+  }
+  // K must be in registers before the first transfer wait (the compiler does not count the
+  // transfers, so a later wait of its own for K would also wait for them)
+  SX_WAIT_VMCNT(0);
+  issue(0);
+  issue(1);
+  wait_vm(1 < nchunk ? n_mine : 0);
+  __syncthreads();
+  const float c2 = a.scale_log2;
+  // S^T of column group gi of the chunk in buffer b
+  auto s_group = [&](const char* b, int gi) -> f32x16_t {
+    f32x16_t r = {};
+    const int c = 32 * gi + l32;
+#pragma unroll
+    for (int st = 0; st < D / 16; ++st) {
+      const int ci = 2 * st + hg;
+      const bf16x8_t bq = *(const bf16x8_t*)(b + c * ROWB + ((ci ^ (c & (NCH - 1))) << 4));
+      r = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka[st], bq, r, 0, 0, 0);
+    }
+    return r;
+  };
+  // column metadata of group gi of chunk k (buffer b): base-2 log-sum-exp (+inf past the chunk,
+  // so those columns add 0) and probe position
+  struct Meta {
+    float l2;
+    int pos;
+  };
+  auto meta = [&](const char* b, int k, int gi) -> Meta {
+    const float* lseb = (const float*)(b + QB);
+    const int* posb = (const int*)(b + QB + 256);
+    const int nvalid = min(RC, np - (lo + k * RC)) * G;
+    const int c = 32 * gi + l32;
+    const bool valid = c < nvalid;
+    return Meta{valid ? lseb[c] : INFINITY, valid ? posb[c_row[gi]] : -1};
+  };
+  auto accumulate = [&](const f32x16_t& sv, const Meta& m, auto masked) {
+#pragma unroll
+    for (int e = 0; e < 16; ++e) {
+      float p = __builtin_amdgcn_exp2f(__builtin_fmaf(sv[e], c2, -m.l2));
+      if constexpr (decltype(masked)::value) {
+        const int key = jw + (e >> 2) * 8 + hg * 4 + (e & 3);
+        p = key <= m.pos ? p : 0.f;
+      }
+      acc32[e] += p;
+    }
+  };
+  // Software pipeline inside the wave: the MFMAs of one column group run while the vector ALU
+  // takes the exponentials of the previous group.  Iteration k: [S(k, 1) | sums of (k, 0)],
+  // barrier (chunk k + 1 has landed), [S(k + 1, 0) | sums of (k, 1)].  Past the last chunk the
+  // products read a stale buffer whose columns are all masked (never used).
+  auto interleave = [&](auto masked) {
+    constexpr int nv = decltype(masked)::value ? 10 : 6;   // vector instructions per MFMA
+    SX_SG(kSgDsRead, D / 16);
+#pragma unroll
+    for (int i = 0; i < D / 16; ++i) {
+      SX_SG(kSgMfma, 1);
+      SX_SG(kSgValu, nv);
+    }
+  };
+  f32x16_t s0 = {}, s1;
+  Meta m0{}, m1{};
+  if (nchunk > 0) {
+    m0 = meta(smem, 0, 0);
+    m1 = meta(smem, 0, 1);
+    s0 = s_group(smem, 0);
+  }
+  // one chunk; `phase` is k mod 3 when known at compile time (the buffer bases then fold into the
+  // LDS reads' immediate offsets), else -1
+  auto body = [&](int k, auto masked, auto phase) {
+    constexpr int PH = decltype(phase)::value;
+    issue(k + 2);
+    const char* b = smem + (PH >= 0 ? PH : k % NBUF) * CHB;
+    s1 = s_group(b, 1);
+    accumulate(s0, m0, masked);
+    interleave(masked);
+    const Meta m1k = m1;
+    wait_vm(k + 2 < nchunk ? n_mine : 0);   // this wave's transfers of chunk k + 1 have landed
+    __syncthreads();
+    const char* bn = smem + (PH >= 0 ? (PH + 1) % NBUF : (k + 1) % NBUF) * CHB;
+    m0 = meta(bn, k + 1, 0);
+    m1 = meta(bn, k + 1, 1);
+    s0 = s_group(bn, 0);
+    accumulate(s1, m1k, masked);
+    interleave(masked);
+    if ((k & 3) == 3) {
+#pragma unroll
+      for (int e = 0; e < 16; ++e) {
+        acc64[e] += (double)acc32[e];
+        acc32[e] = 0.f;
+      }
+    }
+  };
+  using dyn = std::integral_constant<int, -1>;
+  using p0 = std::integral_constant<int, 0>;
+  using p1 = std::integral_constant<int, 1>;
+  using p2 = std::integral_constant<int, 2>;
+  int k = 0;
+  for (; k < nmask; ++k) body(k, std::true_type{}, dyn{});
+  for (; k < nchunk && k % NBUF != 0; ++k) body(k, std::false_type{}, dyn{});
+  for (; k + NBUF <= nchunk; k += NBUF) {
+    body(k, std::false_type{}, p0{});
+    body(k + 1, std::false_type{}, p1{});
+    body(k + 2, std::false_type{}, p2{});
+  }
+  for (; k < nchunk; ++k) body(k, std::false_type{}, dyn{});
+#pragma unroll
+  for (int e = 0; e < 16; ++e) acc64[e] += (double)acc32[e];
+#pragma unroll
+  for (int e = 0; e < 16; ++e)
+#pragma unroll
+    for (int o = 1; o < 32; o <<= 1) acc64[e] += __shfl_xor(acc64[e], o, 64);
+  if (l32 == 0) {
+#pragma unroll
+    for (int e = 0; e < 16; ++e) {
+      const int key = jw + (e >> 2) * 8 + hg * 4 + (e & 3);
+      if (key < T) a.colsum[(int64_t)kvh * a.total + rq.tok_off + key] = acc64[e];
+    }
+  }
+}
+
 template <int D, bool PAGED, bool PV>
 hipError_t launch_mfma(const AttnLaunch& L, hipStream_t s) {
   AttnK a{};
@@ -713,6 +1003,47 @@ hipError_t launch_attn_dense(const AttnLaunch& a, hipStream_t s) {
 hipError_t launch_colsum(const sx_plan* p, const void* q, const void* kc, const float* lse, int lse_tok,
                          hipStream_t s) {
   if (p->desc.dtype == SX_F32) return launch_colsum_f32(p, q, kc, lse, lse_tok, s);
+  const int G = p->desc.n_q_heads / p->desc.n_kv_heads;
+  if (G <= 64 && p->d_qp) {
+    // gather the probe columns, then the column sums from them
+    const int D = p->desc.head_dim;
+    const int64_t threads = (int64_t)p->max_probe * p->desc.n_q_heads * (D * 2 / 16);
+    if (threads > 0) {
+      const dim3 gg((unsigned)((threads + 255) / 256), (unsigned)p->n_req);
+      if (D == 128)
+        hipLaunchKernelGGL(probe_gather_kernel<128>, gg, dim3(256), 0, s, (const uint16_t*)q, lse, lse_tok, p->d_req,
+                           p->d_probe, p->desc.n_q_heads, p->desc.n_kv_heads, p->n_probe, (uint16_t*)p->d_qp,
+                           p->d_lse2p);
+      else
+        hipLaunchKernelGGL(probe_gather_kernel<64>, gg, dim3(256), 0, s, (const uint16_t*)q, lse, lse_tok, p->d_req,
+                           p->d_probe, p->desc.n_q_heads, p->desc.n_kv_heads, p->n_probe, (uint16_t*)p->d_qp,
+                           p->d_lse2p);
+      const hipError_t e = hipGetLastError();
+      if (e != hipSuccess) return e;
+    }
+    Colsum2K c{};
+    c.k = (const uint16_t*)kc;
+    c.qp = (const uint16_t*)p->d_qp;
+    c.lse2p = p->d_lse2p;
+    c.reqs = p->d_req;
+    c.bt = p->d_bt;
+    c.probe = p->d_probe;
+    c.colsum = p->d_colsum;
+    c.total = p->total;
+    c.n_probe_total = p->n_probe;
+    c.Hq = p->desc.n_q_heads;
+    c.Hkv = p->desc.n_kv_heads;
+    c.G = G;
+    c.RC = 64 / G;
+    c.n_req = p->n_req;
+    c.scale_log2 = p->scale * 1.4426950408889634f;
+    const dim3 grid((unsigned)(((p->max_T + CS_KEYS - 1) / CS_KEYS) * c.Hkv * p->n_req));
+    if (D == 128)
+      hipLaunchKernelGGL(colsum2_kernel<128>, grid, dim3(512), 0, s, c);
+    else
+      hipLaunchKernelGGL(colsum2_kernel<64>, grid, dim3(512), 0, s, c);
+    return hipGetLastError();
+  }
   ColsumK a{};
   a.q = (const uint16_t*)q;
   a.k = (const uint16_t*)kc;

@@ -86,7 +86,8 @@ sx_status dev_upload(sx_plan* p, T** ptr, const std::vector<T>& host) {
 void free_plan(sx_plan* p) {
   if (!p) return;
   void* bufs[] = {p->d_req, p->d_bt, p->d_ra, p->d_cs, p->d_probe, p->d_nr, p->d_n_nr, p->d_n_probe,
-                  p->d_flags, p->d_tok_slot, p->d_tok_ra, p->d_rmark, p->d_lse, p->d_colsum};
+                  p->d_flags, p->d_tok_slot, p->d_tok_ra, p->d_rmark, p->d_lse, p->d_colsum,
+                  p->d_qp, p->d_lse2p};
   for (void* b : bufs)
     if (b) (void)hipFree(b);
   delete p;
@@ -182,7 +183,9 @@ sx_status sx_plan_create(const sx_layer_desc* desc, const sx_request* requests, 
   std::vector<int32_t> bt_all;
   std::vector<sx::RealignRow> ra;
   std::vector<float2> cs;
-  std::vector<int32_t> probe((size_t)total, 0), nr((size_t)total, 0);
+  // the probe list carries kProbePad zero entries past the last request: the column-sum kernel
+  // reads whole chunks of probe rows without clamping
+  std::vector<int32_t> probe((size_t)total + sx::kProbePad, 0), nr((size_t)total, 0);
   std::vector<int32_t> n_nr(n_requests), n_probe(n_requests);
   std::vector<uint8_t> flags((size_t)total, 0);
   std::vector<int32_t> tok_slot((size_t)total, 0), tok_ra((size_t)total, -1);
@@ -252,7 +255,7 @@ sx_status sx_plan_create(const sx_layer_desc* desc, const sx_request* requests, 
     h.n_nr = cnt_nr;
     h.n_base = cnt_base;
     p->reqs.push_back(h);
-    rdev[r] = sx::ReqDev{h.T, h.tok_off, h.bt_off, h.n_reuse, h.n_probe, h.n_nr, h.n_base, 0};
+    rdev[r] = sx::ReqDev{h.T, h.tok_off, h.bt_off, h.n_reuse, h.n_probe, h.n_nr, h.n_base, (int32_t)p->n_probe};
     n_nr[r] = cnt_nr;
     n_probe[r] = cnt_probe;
     p->n_reuse += cnt_reuse;
@@ -281,6 +284,20 @@ sx_status sx_plan_create(const sx_layer_desc* desc, const sx_request* requests, 
   if (st == SX_OK) st = dev_upload(p, &p->d_rmark, std::vector<uint32_t>((size_t)total, 0u));
   if (st == SX_OK) st = dev_alloc(p, &p->d_lse, (size_t)total * desc->n_q_heads);
   if (st == SX_OK) st = dev_alloc(p, &p->d_colsum, (size_t)total * desc->n_kv_heads);
+  if (st == SX_OK && desc->dtype == SX_BF16) {
+    // gathered probe columns, kProbePad zeroed rows past the last probe row (per KV head for the
+    // log-sum-exps) so that a chunk read past the end stays in bounds and finite
+    const size_t rows = (size_t)p->n_probe + sx::kProbePad;
+    uint16_t* qp = nullptr;
+    st = dev_alloc(p, &qp, rows * desc->n_q_heads * d);
+    p->d_qp = qp;
+    if (st == SX_OK) st = dev_alloc(p, &p->d_lse2p, rows * desc->n_q_heads);
+    if (st == SX_OK) {
+      hipError_t e = hipMemset(p->d_qp, 0, rows * desc->n_q_heads * d * sizeof(uint16_t));
+      if (e == hipSuccess) e = hipMemset(p->d_lse2p, 0, rows * desc->n_q_heads * sizeof(float));
+      if (e != hipSuccess) st = hip_fail(e, "hipMemset (plan scratch)");
+    }
+  }
   if (st != SX_OK) {
     std::string keep = g_err;
     free_plan(p);

@@ -13,6 +13,7 @@ namespace sx {
 
 constexpr int kBlock = 16;     // paged-cache block size supported by the kernels
 constexpr int kTail = 64;      // tail-fallback rows (Section 3.2)
+constexpr int kProbePad = 64;  // padding rows past the probe lists and gathered probe columns
 
 // Per-request device metadata.
 struct ReqDev {
@@ -23,7 +24,7 @@ struct ReqDev {
   int32_t n_probe;  // |I_nr U S_tail|: Sparse-Q rows
   int32_t n_nr;     // |I_nr|
   int32_t n_base;   // |I_nr U S_ov U S_tail|
-  int32_t pad;
+  int32_t p_off;    // first probe row of the request in the concatenation of all probe rows
 };
 
 // One reused token of the re-alignment pass.  Slots are pool-wide: block * kBlock + slot.
@@ -72,6 +73,8 @@ struct sx_plan {
   mutable uint32_t rgen = 0;      // last generation used
   float* d_lse = nullptr;         // scratch [sum T][Hq]
   double* d_colsum = nullptr;     // scratch [Hkv][sum T]
+  void* d_qp = nullptr;           // scratch [n_probe][Hq][d]: query rows of the probe rows (bf16 plans)
+  float* d_lse2p = nullptr;       // scratch [Hkv][n_probe][Hq / Hkv]: their base-2 log-sum-exp
 };
 
 namespace sx {
