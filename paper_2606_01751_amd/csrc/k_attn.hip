@@ -214,11 +214,12 @@ __global__ __launch_bounds__(512, 1) void attn_mfma_kernel(AttnK a) {
   // declares no memory clobber, which keeps the read-only index loads on the scalar unit.
   auto dma16 = [&](const void* src, const char* dst) {
     const uint32_t m0 = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) const char*)dst;
-    asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(src), "s"(m0) : "m0");
+    asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(src), "s"(m0) : "m0", "memory");
   };
   auto dma16_sb = [&](const uint16_t* sbase, uint32_t voffset, const char* dst) {
     const uint32_t m0 = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) const char*)dst;
-    asm volatile("s_mov_b32 m0, %2\n\tglobal_load_lds_dwordx4 %0, %1" ::"v"(voffset), "s"(sbase), "s"(m0) : "m0");
+    asm volatile("s_mov_b32 m0, %2\n\tglobal_load_lds_dwordx4 %0, %1" ::"v"(voffset), "s"(sbase), "s"(m0)
+                 : "m0", "memory");
   };
   // per-lane byte offsets of the transfers inside a (block, head) run; tiles start at multiples
   // of 64 keys, so they are the same for every tile
@@ -369,22 +370,36 @@ __global__ __launch_bounds__(512, 1) void attn_mfma_kernel(AttnK a) {
   const int tk = (lane & 15) >> 2;
   const int tc = lane & 3;
   // O^T += V^T P^T
+  // Lane part of the V^T read offsets, one per 32-dim tile: row 4 (tg >> 1) + tk of an 8-row
+  // group, dims 32 dt + 16 (tg & 1) + 4 tc .. +3 (16-byte chunk, 8-byte half).  The swizzle
+  // depends on the row only through row mod 4 = tk, so rows 16 kk + 8 h add a constant.
+  int vtr_off[D / 32];
+#pragma unroll
+  for (int dt = 0; dt < D / 32; ++dt) {
+    const int dchunk = 4 * dt + 2 * (tg & 1) + (tc >> 1);
+    vtr_off[dt] = (4 * (tg >> 1) + tk) * ROWB + ((dchunk ^ v_swz<NCH>(tk)) << 4) + (tc & 1) * 8;
+  }
   auto pv_body = [&](const char* Vb) {
     if constexpr (PV) {
+      // one base address per 32-dim tile for this tile's buffer (the empty asm keeps the compiler
+      // from re-associating the sums into one precomputed register per read); every read then
+      // adds its row constant as an immediate offset
+      uint32_t vbase[D / 32];
+#pragma unroll
+      for (int dt = 0; dt < D / 32; ++dt) {
+        vbase[dt] = (uint32_t)(uintptr_t)(lds_shortx4_t*)(Vb) + (uint32_t)vtr_off[dt];
+        asm volatile("" : "+v"(vbase[dt]));
+      }
 #pragma unroll
       for (int kk = 0; kk < 4; ++kk)
 #pragma unroll
         for (int dt = 0; dt < D / 32; ++dt) {
-          // dims 32 dt + 16 (tg & 1) + 4 tc .. +3 -> 16-byte chunk, 8-byte half
-          const int dchunk = 4 * dt + 2 * (tg & 1) + (tc >> 1);
-          const int dhalf = (tc & 1) * 8;
           shortx4_t h2[2];
 #pragma unroll
           for (int h = 0; h < 2; ++h) {
             // slots 8 hg + 4h + k <-> key 16 kk + 8 h + 4 hg + k (the P^T operand order)
-            const int rr = 16 * kk + 8 * h + 4 * (tg >> 1) + tk;
-            const int off = rr * ROWB + ((dchunk ^ v_swz<NCH>(rr)) << 4) + dhalf;
-            h2[h] = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_shortx4_t*)(Vb + off));
+            h2[h] = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+                (lds_shortx4_t*)(uintptr_t)(vbase[dt] + (uint32_t)((16 * kk + 8 * h) * ROWB)));
           }
           const bf16x8_t va = __builtin_bit_cast(
               bf16x8_t, make_uint4(__builtin_bit_cast(uint2, h2[0]).x, __builtin_bit_cast(uint2, h2[0]).y,
@@ -789,11 +804,11 @@ __global__ __launch_bounds__(512, 1) void colsum2_kernel(Colsum2K a) {
   const int n_mine = PPW + (lse_wave ? 1 : 0) + (pos_wave ? 1 : 0);
   auto dma16 = [&](const void* src, const char* dst) {
     const uint32_t m0 = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) const char*)dst;
-    asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(src), "s"(m0) : "m0");
+    asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(src), "s"(m0) : "m0", "memory");
   };
   auto dma4 = [&](const void* src, const char* dst) {
     const uint32_t m0 = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) const char*)dst;
-    asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dword %0, off" ::"v"(src), "s"(m0) : "m0");
+    asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dword %0, off" ::"v"(src), "s"(m0) : "m0", "memory");
   };
   auto issue = [&](int k) {
     if (k >= nchunk) return;
