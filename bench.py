@@ -71,7 +71,9 @@ KERNELS = {
     "attn_mfma_kernel<128, false, true>": ("sx_full_attn", "k_attn.hip"),
     # two-pass scoring only (layers without a preceding full layer)
     "attn_mfma_kernel<128, true, false>": ("sx_sparseq_score", "k_attn.hip"),
-    "colsum_mfma_kernel<128>": ("sx_sparseq_score", "k_attn.hip"),
+    "colsum_mfma_kernel<128>": ("sx_sparseq_score", "k_attn.hip"),   # query heads per KV head > 64 only
+    "colsum2_kernel<128>": ("sx_sparseq_score", "k_attn.hip"),
+    "probe_gather_kernel<128>": ("sx_sparseq_score", "k_attn.hip"),
     "head_reduce_kernel": ("sx_sparseq_score", "k_copy.hip"),
     "realign_kernel": ("sx_rope_realign", "k_copy.hip"),
     "scatter_kernel": ("sx_kv_scatter", "k_copy.hip"),
