@@ -56,6 +56,12 @@ def parse():
                          "attention with R as a byte mask built once per step (default; the attention then finds "
                          "part of the cache in the Infinity Cache), the same from the row list (marks R per "
                          "layer), one pass for all sparse layers after the selection, or two passes per layer")
+    ap.add_argument("--layer-body", action="store_true",
+                    help="run every sparse layer as a whole layer (Algorithm 1 steps 19-22): RMSNorm, Q/K/V "
+                         "projections of the rows of R, RoPE, KV write, sparse attention, output projection + "
+                         "residual, RMSNorm, SwiGLU feed-forward + residual, with random weights of a Llama-3-8B "
+                         "layer (hidden 4096, feed-forward 14336); the value is then whole-layer throughput")
+    ap.add_argument("--ffn", type=int, default=14336, help="feed-forward size of --layer-body")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
                     help="also run a plain device copy of BYTES bytes (reference for HBM byte counters)")
     ap.add_argument("--record-traffic", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
@@ -229,6 +235,59 @@ def main():
     torch.cuda.synchronize()
     log(f"inputs resident in HBM ({torch.cuda.memory_allocated() / 2**30:.1f} GiB) in {time.time() - t0:.1f}s")
 
+    H, F, eps = Hq * d, args.ffn, 1e-5
+    body = None
+    if args.layer_body:
+        # per sparse layer: its own random weights (~N(0, 1/fan_in), bf16); one hidden-state buffer
+        # carried from layer to layer; per-step scratch for the intermediates
+        gen = torch.Generator(device="cuda")
+        gen.manual_seed(args.seed + 12345)
+
+        def lin(o, i):
+            return (torch.randn((o, i), generator=gen, device="cuda", dtype=torch.float32) / math.sqrt(i)).to(dt)
+
+        def norm_w():
+            return (1 + 0.1 * torch.randn(H, generator=gen, device="cuda", dtype=torch.float32)).to(dt)
+        body = {"w": [], "hidden": torch.randn((T, H), generator=gen, device="cuda", dtype=torch.float32).to(dt)}
+        for l in range(nfull, L):
+            body["w"].append({"ln1": norm_w(), "wq": lin(Hq * d, H), "wk": lin(Hkv * d, H), "wv": lin(Hkv * d, H),
+                              "wo": lin(H, Hq * d), "ln2": norm_w(), "wgu": lin(2 * F, H), "wd": lin(H, F)})
+        z = lambda *shape: torch.zeros(shape, dtype=dt, device="cuda")
+        body.update({"x1": z(T, H), "att": z(T, Hq, d), "h1": z(T, H), "x2": z(T, H), "gu": z(T, 2 * F),
+                     "a": z(T, F)})
+        torch.cuda.synchronize()
+        log(f"layer body: {len(body['w'])} layers of weights ({torch.cuda.memory_allocated() / 2**30:.1f} GiB resident)")
+
+    def sparse_layer_body(l, tl):
+        """Algorithm 1 steps 19-22 for sparse layer l on the rows of R: the fresh Q/K/V of R are
+        projected into the layer's token-indexed q/k/v buffers, the hidden states of R updated in
+        place."""
+        wl = body["w"][l - nfull]
+        hid = body["hidden"]
+        tm.run("sx_rmsnorm_rows", lambda: sx.rmsnorm_rows(plan, rows, n_rows, max_rows, hid, wl["ln1"], eps, body["x1"],
+                                                          x_by_token=True))
+        tm.run("sx_gemm_rows qkv", lambda: (sx.gemm_rows(plan, rows, n_rows, max_rows, body["x1"], wl["wq"], tl["q"],
+                                                         y_by_token=True),
+                                            sx.gemm_rows(plan, rows, n_rows, max_rows, body["x1"], wl["wk"], tl["k"],
+                                                         y_by_token=True),
+                                            sx.gemm_rows(plan, rows, n_rows, max_rows, body["x1"], wl["wv"], tl["v"],
+                                                         y_by_token=True)))
+        tm.run("sx_rope_rows", lambda: sx.rope_rows(plan, rows, n_rows, max_rows, tl["q"], tl["k"]))
+        tm.run("sx_realign_scatter_masked",
+               lambda: sx.realign_scatter_masked(plan, tl["k_src"], tl["v_src"], tl["k"], tl["v"], rmask, tl["kc"],
+                                                 tl["vc"]))
+        tm.run("sx_sparse_attn", lambda: sx.sparse_attn(plan, tl["q"], rows, n_rows, max_rows, tl["kc"], tl["vc"],
+                                                        body["att"]))
+        tm.run("sx_gemm_rows o", lambda: sx.gemm_rows(plan, rows, n_rows, max_rows, body["att"].view(T, H), wl["wo"],
+                                                      body["h1"], residual=hid, y_by_token=True))
+        tm.run("sx_rmsnorm_rows", lambda: sx.rmsnorm_rows(plan, rows, n_rows, max_rows, body["h1"], wl["ln2"], eps,
+                                                          body["x2"], x_by_token=True))
+        tm.run("sx_gemm_rows gate_up", lambda: sx.gemm_rows(plan, rows, n_rows, max_rows, body["x2"], wl["wgu"],
+                                                            body["gu"]))
+        tm.run("sx_silu_mul_rows", lambda: sx.silu_mul_rows(plan, n_rows, max_rows, body["gu"], body["a"]))
+        tm.run("sx_gemm_rows down", lambda: sx.gemm_rows(plan, rows, n_rows, max_rows, body["a"], wl["wd"], hid,
+                                                         residual=body["h1"], y_by_token=True))
+
     tm = Timers(torch)
     sparse_kv = [(tl["k_src"], tl["v_src"], tl["k"], tl["v"], tl["kc"], tl["vc"])
                  for l, tl in enumerate(layers) if l >= nfull and not (nfull == 0 and l == 0)]
@@ -255,7 +314,7 @@ def main():
                                                             lse_in=lse if (nfull > 0 and args.score_passes == 1)
                                                             else None))
         tm.run("sx_topk_select", lambda: sx.topk_select(plan, scores, ratio, rows, n_rows))
-        if args.kv_write == "per-layer" and L > max(nfull, 1):
+        if (args.kv_write == "per-layer" or args.layer_body) and L > max(nfull, 1):
             tm.run("sx_rows_mask", lambda: sx.rows_mask(plan, rows, n_rows, max_rows, rmask))
         if args.kv_write == "all-layers" and sparse_kv:
             # every sparse layer's cache in one call (two launches of at most 16 layers)
@@ -263,6 +322,9 @@ def main():
                    lambda: sx.realign_scatter_layers(plan, sparse_kv, rows, n_rows, max_rows))
         for l in range(max(nfull, 0), L):
             tl = layers[l]
+            if args.layer_body and l >= nfull and not (nfull == 0 and l == 0):
+                sparse_layer_body(l, tl)
+                continue
             if nfull == 0 and l == 0:
                 # the selecting layer's cache is already re-aligned: only R's fresh rows remain
                 tm.run("sx_kv_scatter", lambda: sx.kv_scatter(plan, tl["k"], tl["v"], tl["kc"], tl["vc"], rows=rows,
@@ -346,6 +408,14 @@ def main():
     work["sx_realign_scatter_masked"] = work["sx_realign_scatter"]
     work["sx_realign_scatter_layers"] = ("hbm", len(sparse_kv) * work["sx_realign_scatter"][1])
     work["sx_rows_mask"] = ("latency", T + 4.0 * n_R)
+    # layer body: matrix products 2 |R| k n, per launch (the q/k/v entry times three launches)
+    work["sx_gemm_rows qkv"] = ("mfma", 2.0 * n_R * H * (Hq + 2 * Hkv) * d)
+    work["sx_gemm_rows o"] = ("mfma", 2.0 * n_R * Hq * d * H)
+    work["sx_gemm_rows gate_up"] = ("mfma", 2.0 * n_R * H * 2 * F)
+    work["sx_gemm_rows down"] = ("mfma", 2.0 * n_R * F * H)
+    work["sx_rmsnorm_rows"] = ("hbm", 2.0 * n_R * H * esz + H * esz)
+    work["sx_rope_rows"] = ("hbm", 4.0 * n_R * (Hq + Hkv) * d * esz)
+    work["sx_silu_mul_rows"] = ("hbm", 3.0 * n_R * F * esz)
     peak = PEAK_BF16_TFLOPS if w.dtype == "bf16" else PEAK_F32_TFLOPS
     kernels = {}
     for name, k in kern.items():
@@ -379,7 +449,7 @@ def main():
 
     value = T * L / (ms_per_step / 1e3)
     cpu = None
-    if not args.no_cpu_baseline:
+    if not args.no_cpu_baseline and not args.layer_body:
         cpu = cpu_baseline(w, layers, R, nfull, L, ratio, torch)
     res = {
         "metric": METRIC, "value": round(value, 1), "unit": "tokens/s", "n_gpus": 1, "steps": args.steps,
@@ -388,7 +458,8 @@ def main():
         "config": {"workload": f"{w.name}: {w.description}", "tokens": T, "layers": L, "full_layers": nfull,
                    "ratio": ratio, "recompute_rows": n_R, "k": int(k_total), "q_heads": Hq, "kv_heads": Hkv,
                    "head_dim": d, "requests": len(w.requests), "score_passes": args.score_passes,
-                   "kv_write": args.kv_write},
+                   "kv_write": args.kv_write, "layer_body": bool(args.layer_body),
+                   **({"hidden": H, "ffn": F} if args.layer_body else {})},
         "kernels": kernels, "roofline": roof, "cpu_baseline": cpu,
     }
     print(json.dumps(res), flush=True)

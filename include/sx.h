@@ -255,6 +255,48 @@ sx_status sx_full_attn(const sx_layer_desc* desc, const void* q, const void* k, 
                        const int32_t* cu_seqlens, int32_t n_requests, int32_t max_seqlen, void* out,
                        float* lse, void* stream);
 
+/* ------------------------------------------------------------------------------------------
+ * Row-sparse layer body (Algorithm 1 steps 19 and 22): the projections, normalisations and the
+ * feed-forward module evaluated only on the rows of R, as the paper does after the boundary
+ * layer.  bfloat16 plans only (SX_EUNSUPPORTED otherwise); float32 arithmetic inside, bfloat16
+ * results rounded to nearest even.
+ *
+ * Rows: for request r, rows[off_r + n] for n < n_rows[r] (the row-list layout of sx_topk_select;
+ * max_rows >= every n_rows[r], at most the longest request).  An operand row is addressed
+ *   by slot  (`*_by_token` = 0): row off_r + n of a [sum T][...] array -- compact per request,
+ *            the layout of sx_sparse_attn's output;
+ *   by token (`*_by_token` = 1): row off_r + rows[off_r + n] -- the request's token rows, the
+ *            layout of fresh q/k/v and of hidden states.
+ * Every tensor is caller-owned DEVICE memory; rows not listed are neither read nor written.
+ * ------------------------------------------------------------------------------------------ */
+
+/* y[row] = x[row] . w^T (+ residual[row]): x [..][k], w [n][k] (the weight of a linear layer,
+ * k contiguous), y and residual [..][n]; residual (nullable) is addressed like y and may be y
+ * itself (in-place residual add).  k a multiple of 64, n a multiple of 256.  Matrix cores,
+ * float32 accumulation. */
+sx_status sx_gemm_rows(const sx_plan* plan, const int32_t* rows, const int32_t* n_rows, int32_t max_rows,
+                       const void* x, int32_t x_by_token, const void* w, int32_t k, int32_t n,
+                       const void* residual, void* y, int32_t y_by_token, void* stream);
+
+/* RMSNorm: y[row] = x[row] / sqrt(mean_j x[row][j]^2 + eps) * gamma, rows of h elements
+ * (h a multiple of 8), gamma [h]; the sum of squares is float32 in a fixed order. */
+sx_status sx_rmsnorm_rows(const sx_plan* plan, const int32_t* rows, const int32_t* n_rows, int32_t max_rows,
+                          const void* x, int32_t x_by_token, const void* gamma, float eps, int32_t h, void* y,
+                          int32_t y_by_token, void* stream);
+
+/* RoPE of fresh query and key rows, in place, at each listed token's position in the new
+ * sequence (new_pos of its segment + offset): q [sum T][Hq][d], k [sum T][Hkv][d], addressed by
+ * token.  Pairs and frequencies as in sx_rope_realign (angle and cos/sin in float64, rounded to
+ * float32; rotation in float32 without contraction). */
+sx_status sx_rope_rows(const sx_plan* plan, const int32_t* rows, const int32_t* n_rows, int32_t max_rows, void* q,
+                       void* k, void* stream);
+
+/* SwiGLU activation, by slot: y[row][j] = silu(g) * u with g = gate_up[row][j],
+ * u = gate_up[row][f + j], silu(g) = g / (1 + e^-g); gate_up [sum T][2f], y [sum T][f]
+ * (f a multiple of 8). */
+sx_status sx_silu_mul_rows(const sx_plan* plan, const int32_t* n_rows, int32_t max_rows, const void* gate_up,
+                           int32_t f, void* y, void* stream);
+
 /* Text of the last non-OK status returned to this thread ("" if none). */
 const char* sx_last_error(void);
 

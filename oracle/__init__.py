@@ -44,7 +44,7 @@ __all__ = [
     "rope_rotate", "to_bf16", "store", "realign_request", "scatter_rows", "gather_tokens",
     "tail_fallback", "overflow_positions", "probe_positions", "budget", "topk_keys",
     "recompute_set", "sparseq_scores", "attention_rows", "full_attention", "softmax_scale",
-    "sparse_layer", "full_layer",
+    "sparse_layer", "full_layer", "rmsnorm", "linear", "rope_at_positions", "silu_mul", "layer_body",
 ]
 
 
@@ -425,3 +425,83 @@ def full_layer(w, tensors: dict, rows_sample=None) -> dict:
         rows = None if rows_sample is None else rows_sample[r]
         out.append(full_attention(q, k, v, scale, rows))
     return {"out": out, "k_pool": kp, "v_pool": vp}
+
+
+# ---------------------------------------------------------------------------------------------
+# Row-sparse layer body (Algorithm 1 step 19: project Q/K/V only for the tokens of R; step 22:
+# update the hidden states only on R, then the output projection, residual path, normalisation
+# and feed-forward module on those rows).  The paper does not fix the block architecture; the
+# reading used is the Llama-3 block of the workloads: pre-normalisation with RMSNorm, linear
+# maps without bias, RoPE on the fresh queries and keys at their positions in the new sequence,
+# and a SwiGLU feed-forward module.  Everything is float64 from the stored input values; where a
+# result is stored (bfloat16), `store` rounds it.
+# ---------------------------------------------------------------------------------------------
+
+def rmsnorm(x: np.ndarray, gamma: np.ndarray, eps: float) -> np.ndarray:
+    """x / sqrt(mean(x^2) + eps) * gamma over the last axis, float64."""
+    x = np.asarray(x, dtype=np.float64)
+    ms = np.mean(x * x, axis=-1, keepdims=True)
+    return x / np.sqrt(ms + eps) * np.asarray(gamma, dtype=np.float64)
+
+
+def linear(x: np.ndarray, w: np.ndarray, residual=None) -> np.ndarray:
+    """x w^T (+ residual) with w stored [out][in] (a linear layer's weight), float64."""
+    y = np.asarray(x, dtype=np.float64) @ np.asarray(w, dtype=np.float64).T
+    return y if residual is None else y + np.asarray(residual, dtype=np.float64)
+
+
+def rope_at_positions(x: np.ndarray, positions, base: float, style: str = "neox") -> np.ndarray:
+    """RoPE of fresh rows [n][H][d] at their positions: row i is rotated by R_{positions[i]}
+    (the rotation of rope_rotate with shift = position, i.e. from position 0), float32."""
+    x = np.asarray(x, dtype=np.float32)
+    out = np.empty_like(x)
+    for i, p in enumerate(np.asarray(positions, dtype=np.int64)):
+        out[i] = rope_rotate(x[i], int(p), base, style)
+    return out
+
+
+def silu_mul(gate_up: np.ndarray) -> np.ndarray:
+    """SwiGLU: silu(g) * u for rows [g (f) | u (f)], silu(g) = g / (1 + e^-g), float64."""
+    gu = np.asarray(gate_up, dtype=np.float64)
+    f = gu.shape[-1] // 2
+    g, u = gu[..., :f], gu[..., f:]
+    return g / (1.0 + np.exp(-g)) * u
+
+
+def layer_body(w, hidden: np.ndarray, R: np.ndarray, weights: dict, src_k, src_v, eps: float) -> dict:
+    """One sparse layer of a single request on the rows of R (Algorithm 1 steps 19-22).
+
+    hidden: the request's [T][H] input hidden states; weights: ln1 [H], wq [Hq d][H],
+    wk / wv [Hkv d][H], wo [H][Hq d], ln2 [H], wgu [2F][H], wd [H][F].  The cache of the layer
+    holds the re-aligned cached K/V of reused tokens (step 20) and the freshly projected K/V of
+    the rows of R (step 19).  Intermediates are stored in the workload's type (bfloat16) where
+    the GPU path stores them.  Returns the new hidden states of R and the intermediates."""
+    req = w.requests[0]
+    T = req.n_tokens
+    Hq, Hkv, d = w.n_q_heads, w.n_kv_heads, w.head_dim
+    R = np.asarray(R, dtype=np.int64)
+    dt = w.dtype
+    x1 = store(rmsnorm(hidden[R], weights["ln1"], eps), dt)
+    q = store(linear(x1, weights["wq"]), dt).reshape(len(R), Hq, d)
+    k = store(linear(x1, weights["wk"]), dt).reshape(len(R), Hkv, d)
+    v = store(linear(x1, weights["wv"]), dt).reshape(len(R), Hkv, d)
+    _, pos, _ = token_layout(T, req.segments)
+    q = store(rope_at_positions(q, pos[R], w.rope_base, w.rope_style), dt)
+    k = store(rope_at_positions(k, pos[R], w.rope_base, w.rope_style), dt)
+    kp, vp = _empty_pool(w), _empty_pool(w)
+    realign_request(req, w, src_k, src_v, kp, vp)
+    k_tok = np.zeros((T, Hkv, d), np.float32)
+    v_tok = np.zeros((T, Hkv, d), np.float32)
+    k_tok[R], v_tok[R] = k, v
+    scatter_rows(req, w, R, k_tok, v_tok, kp, vp)
+    q_tok = np.zeros((T, Hq, d), np.float32)
+    q_tok[R] = q
+    att = store(attention_rows(q_tok, gather_tokens(req, w, kp), gather_tokens(req, w, vp), R,
+                               softmax_scale(d)), dt).reshape(len(R), Hq * d)
+    h1 = store(linear(att, weights["wo"], hidden[R]), dt)
+    x2 = store(rmsnorm(h1, weights["ln2"], eps), dt)
+    gu = store(linear(x2, weights["wgu"]), dt)
+    a = store(silu_mul(gu), dt)
+    h2 = store(linear(a, weights["wd"], h1), dt)
+    return {"x1": x1, "q": q, "k": k, "v": v, "att": att, "h1": h1, "x2": x2, "gu": gu, "a": a, "h2": h2,
+            "k_pool": kp, "v_pool": vp}

@@ -25,7 +25,8 @@ from typing import Optional, Sequence
 __all__ = [
     "LIB_PATH", "SxError", "lib", "LayerDesc", "Plan", "rope_realign", "kv_scatter", "realign_scatter",
     "realign_scatter_layers", "rows_mask", "realign_scatter_masked", "sparseq_score",
-    "topk_select", "sparse_attn", "full_attn", "F32", "BF16", "ROPE_NEOX", "ROPE_GPTJ", "EXPORTED",
+    "topk_select", "sparse_attn", "full_attn", "gemm_rows", "rmsnorm_rows", "rope_rows", "silu_mul_rows",
+    "F32", "BF16", "ROPE_NEOX", "ROPE_GPTJ", "EXPORTED",
 ]
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libsx.so")
@@ -38,7 +39,8 @@ EXPORTED = (
     "sx_plan_create", "sx_plan_destroy", "sx_plan_get_info", "sx_plan_budget", "sx_plan_nonreused_rows",
     "sx_rope_realign", "sx_kv_scatter", "sx_realign_scatter", "sx_realign_scatter_layers", "sx_rows_mask",
     "sx_realign_scatter_masked", "sx_sparseq_score", "sx_topk_select",
-    "sx_sparse_attn", "sx_full_attn", "sx_last_error", "sx_version",
+    "sx_sparse_attn", "sx_full_attn", "sx_gemm_rows", "sx_rmsnorm_rows", "sx_rope_rows", "sx_silu_mul_rows",
+    "sx_last_error", "sx_version",
 )
 
 
@@ -104,6 +106,11 @@ def lib() -> ctypes.CDLL:
         L.sx_topk_select.argtypes = [VP, VP, D, VP, VP, VP]
         L.sx_sparse_attn.argtypes = [VP, VP, VP, VP, I32, VP, VP, VP, VP]
         L.sx_full_attn.argtypes = [P(LayerDesc), VP, VP, VP, VP, I32, I32, VP, VP, VP]
+        F = ctypes.c_float
+        L.sx_gemm_rows.argtypes = [VP, VP, VP, I32, VP, I32, VP, I32, I32, VP, VP, I32, VP]
+        L.sx_rmsnorm_rows.argtypes = [VP, VP, VP, I32, VP, I32, VP, F, I32, VP, I32, VP]
+        L.sx_rope_rows.argtypes = [VP, VP, VP, I32, VP, VP, VP]
+        L.sx_silu_mul_rows.argtypes = [VP, VP, I32, VP, I32, VP, VP]
         for name in EXPORTED:
             if name in ("sx_last_error", "sx_version"):
                 getattr(L, name).restype = ctypes.c_char_p
@@ -265,3 +272,32 @@ def full_attn(desc: LayerDesc, q, k, v, cu_seqlens, n_requests: int, max_seqlen:
               stream=None):
     _check(lib().sx_full_attn(ctypes.byref(desc), _ptr(q), _ptr(k), _ptr(v), _ptr(cu_seqlens), int(n_requests),
                               int(max_seqlen), _ptr(out), _ptr(lse), _stream(stream)))
+
+
+# ---- row-sparse layer body (rows of R only; see include/sx.h) ----
+
+def gemm_rows(plan: Plan, rows, n_rows, max_rows: int, x, w, y, residual=None, x_by_token=False,
+              y_by_token=False, stream=None):
+    """y[row] = x[row] @ w.T (+ residual[row]); w is [n][k]."""
+    n, k = int(w.shape[0]), int(w.shape[1])
+    _check(lib().sx_gemm_rows(plan.handle, _ptr(rows), _ptr(n_rows), int(max_rows), _ptr(x), int(bool(x_by_token)),
+                              _ptr(w), k, n, _ptr(residual), _ptr(y), int(bool(y_by_token)), _stream(stream)))
+
+
+def rmsnorm_rows(plan: Plan, rows, n_rows, max_rows: int, x, gamma, eps: float, y, x_by_token=False,
+                 y_by_token=False, stream=None):
+    h = int(gamma.shape[0])
+    _check(lib().sx_rmsnorm_rows(plan.handle, _ptr(rows), _ptr(n_rows), int(max_rows), _ptr(x),
+                                 int(bool(x_by_token)), _ptr(gamma), float(eps), h, _ptr(y), int(bool(y_by_token)),
+                                 _stream(stream)))
+
+
+def rope_rows(plan: Plan, rows, n_rows, max_rows: int, q, k, stream=None):
+    _check(lib().sx_rope_rows(plan.handle, _ptr(rows), _ptr(n_rows), int(max_rows), _ptr(q), _ptr(k),
+                              _stream(stream)))
+
+
+def silu_mul_rows(plan: Plan, n_rows, max_rows: int, gate_up, y, stream=None):
+    f = int(y.shape[-1])
+    _check(lib().sx_silu_mul_rows(plan.handle, _ptr(n_rows), int(max_rows), _ptr(gate_up), f, _ptr(y),
+                                  _stream(stream)))

@@ -1,0 +1,371 @@
+// Row-sparse layer body (Algorithm 1 steps 19 and 22): the projections, normalisations and the
+// feed-forward module evaluated on the rows of the recompute set R only.
+//
+//   gemm_rows_kernel     Y[row] = X[row] W^T (+ residual[row]): bfloat16 operands, float32
+//                        accumulation on v_mfma_f32_32x32x16_bf16, W stored [n][k] (k contiguous,
+//                        the layout of a linear layer's weight)
+//   rmsnorm_rows_kernel  Y[row] = X[row] / sqrt(mean(X[row]^2) + eps) * gamma
+//   rope_rows_kernel     RoPE of fresh query / key rows at their positions in the new sequence
+//   silu_mul_rows_kernel Y[row] = silu(G[row]) * U[row] for a gate|up product [row][2f]
+//
+// Rows: for request r, the listed rows n < n_rows[r] of the row-list layout.  An operand row is
+// addressed by slot (off_r + n: compact per request, like the sparse attention output) or by
+// token (off_r + rows[off_r + n]: the request's token rows, like fresh Q/K/V and hidden states).
+#include "sx_device.h"
+#include "sx_internal.h"
+
+namespace sx {
+namespace {
+
+typedef float f32x2_t __attribute__((ext_vector_type(2)));
+
+// s_waitcnt with vmcnt <= n (n < 16), expcnt and lgkmcnt left unconstrained (gfx9 encoding).
+#define SX_WAIT_VMCNT(n) __builtin_amdgcn_s_waitcnt(((n) & 0xF) | (0x7 << 4) | (0xF << 8))
+
+__device__ __forceinline__ int64_t row_index(const ReqDev& rq, const int32_t* rows, int n, bool by_token) {
+  return by_token ? (int64_t)rq.tok_off + rows[rq.tok_off + n] : (int64_t)rq.tok_off + n;
+}
+
+// ---------------------------------------------------------------------------------------------
+// GEMM on listed rows.  Computed transposed, Y^T = W X^T: the MFMA A operand is a 32 x 16 slice of
+// W (32 output features), the B operand a 16 x 32 slice of X^T (32 rows), so each lane owns one
+// row of the result and writes 4 consecutive features per store.
+// Workgroup tile: 256 features x 256 rows, 64 of k per stage; 8 waves as 4 (features) x 2 (rows),
+// a wave owns 64 features x 128 rows (2 x 4 accumulators of 32 x 32).  Both operand tiles move
+// global -> LDS directly (16 bytes per lane), double-buffered; rows of 128 bytes with their eight
+// 16-byte chunks XOR-swizzled by (row / 2) mod 8, conflict-free for the 16-byte operand reads.
+// ---------------------------------------------------------------------------------------------
+constexpr int GBN = 256, GBM = 256, GBK = 64;
+constexpr int GTILE = 256 * GBK * 2;            // bytes of one operand tile (32 KB)
+
+struct GemmRowsK {
+  const ReqDev* reqs;
+  const int32_t* rows;
+  const int32_t* n_rows;
+  const uint16_t* x;
+  const uint16_t* w;
+  const uint16_t* res;
+  uint16_t* y;
+  int K, N, n_req, m_tiles, x_tok, y_tok;
+};
+
+__global__ __launch_bounds__(512, 1) void gemm_rows_kernel(GemmRowsK a) {
+  constexpr int NW = 8;
+  __shared__ __attribute__((aligned(1024))) char smem[2 * 2 * GTILE];   // [stage][W | X]
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wu = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int l32 = lane & 31;
+  const int hg = lane >> 5;
+  // grid: row tile fastest (consecutive workgroups share a W panel), then feature tile
+  const int n_mt = a.n_req * a.m_tiles;
+  const int mt_all = (int)(blockIdx.x % (unsigned)n_mt);
+  const int nt = (int)(blockIdx.x / (unsigned)n_mt);
+  const int r = mt_all / a.m_tiles;
+  const int m0 = (mt_all - r * a.m_tiles) * GBM;
+  const ReqDev rq = a.reqs[r];
+  const int nr = a.n_rows[r];
+  if (m0 >= nr) return;
+  const int n0 = nt * GBN;
+  const int K = a.K;
+
+  // ---- transfers: piece q (1 KB) of a tile holds rows 8q .. 8q + 7; lane l fills row 8q + l / 8,
+  // physical chunk l % 8 with logical chunk (l % 8) ^ ((row / 2) mod 8).  A wave moves pieces
+  // wu + 8 i (i < 4) of both tiles. ----
+  const uint16_t* w_src[4];
+  const uint16_t* x_src[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int row = 8 * (wu + NW * i) + lane / 8;
+    const int lc = (lane & 7) ^ ((row >> 1) & 7);
+    w_src[i] = a.w + (int64_t)(n0 + row) * K + lc * 8;
+    const int m = min(m0 + row, nr - 1);   // rows past the request's last read a valid row
+    x_src[i] = a.x + row_index(rq, a.rows, m, a.x_tok) * K + lc * 8;
+  }
+  const uint32_t smem_lds = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) char*)smem;
+  auto dma16 = [&](const void* src, uint32_t lds) {
+    const uint32_t m0r = __builtin_amdgcn_readfirstlane(lds);
+    asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(src), "s"(m0r) : "m0", "memory");
+  };
+  auto issue = [&](int t) {   // stage t into buffer t mod 2
+    const uint32_t base = smem_lds + (uint32_t)((t & 1) * 2 * GTILE);
+    const int k0 = t * GBK;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      dma16(w_src[i] + k0, base + (uint32_t)((wu + NW * i) * 1024));
+      dma16(x_src[i] + k0, base + (uint32_t)(GTILE + (wu + NW * i) * 1024));
+    }
+  };
+
+  // ---- operand reads: row 32 j + l32 of a tile, logical chunk 2 s + hg at physical chunk
+  // (2 s + hg) ^ ((l32 / 2) mod 8): the lane part depends on s only, the tile row block adds a
+  // constant (an immediate offset) ----
+  const int wn = wu & 3, wm = wu >> 2;
+  uint32_t lane_off[GBK / 16];
+#pragma unroll
+  for (int s = 0; s < GBK / 16; ++s)
+    lane_off[s] = (uint32_t)(l32 * 128 + ((((2 * s + hg) ^ ((l32 >> 1) & 7))) << 4));
+  f32x16_t acc[2][4];
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
+
+  const int nk = K / GBK;
+  // the row indices above are compiler-visible loads: complete before the first transfer wait
+  SX_WAIT_VMCNT(0);
+  issue(0);
+  SX_WAIT_VMCNT(0);
+  __syncthreads();
+  for (int t = 0; t < nk; ++t) {
+    if (t + 1 < nk) issue(t + 1);
+    // stage t: per 16-wide k slice s, 2 W slices (features) x 4 X slices (rows) -> 8 MFMAs.  One
+    // base register per slice s and matrix (the empty asm keeps the sums from being re-associated
+    // into one precomputed register per read)
+    const uint32_t sb = smem_lds + (uint32_t)((t & 1) * 2 * GTILE);
+    uint32_t wb[GBK / 16], xb[GBK / 16];
+#pragma unroll
+    for (int s = 0; s < GBK / 16; ++s) {
+      wb[s] = sb + lane_off[s] + (uint32_t)(wn * 64 * 128);
+      xb[s] = sb + (uint32_t)GTILE + lane_off[s] + (uint32_t)(wm * 128 * 128);
+      asm volatile("" : "+v"(wb[s]), "+v"(xb[s]));
+    }
+#pragma unroll
+    for (int s = 0; s < GBK / 16; ++s) {
+      bf16x8_t fw[2], fx[4];
+#pragma unroll
+      for (int i = 0; i < 2; ++i)
+        fw[i] = *(const __attribute__((address_space(3))) bf16x8_t*)(uintptr_t)(wb[s] + (uint32_t)(i * 32 * 128));
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+        fx[j] = *(const __attribute__((address_space(3))) bf16x8_t*)(uintptr_t)(xb[s] + (uint32_t)(j * 32 * 128));
+#pragma unroll
+      for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fw[i], fx[j], acc[i][j], 0, 0, 0);
+    }
+    SX_WAIT_VMCNT(0);   // this wave's transfers of stage t + 1 have landed
+    __syncthreads();
+  }
+
+  // ---- epilogue: lane owns row 32 j + l32 of the wave's rows; value e of accumulator (i, j) is
+  // feature 32 i + 8 (e / 4) + 4 hg + e % 4 of the wave's features ----
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const int m = m0 + wm * 128 + 32 * j + l32;
+    if (m >= nr) continue;
+    const int64_t yr = row_index(rq, a.rows, m, a.y_tok);
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        const int n = n0 + wn * 64 + 32 * i + 8 * g + 4 * hg;
+        float v[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) v[e] = acc[i][j][4 * g + e];
+        if (a.res) {
+          const uint2 rv = *(const uint2*)(a.res + yr * a.N + n);
+          v[0] += bf16_lo(rv.x);
+          v[1] += bf16_hi(rv.x);
+          v[2] += bf16_lo(rv.y);
+          v[3] += bf16_hi(rv.y);
+        }
+        uint2 o;
+        o.x = pack_bf16x2(v[0], v[1]);
+        o.y = pack_bf16x2(v[2], v[3]);
+        *(uint2*)(a.y + yr * a.N + n) = o;
+      }
+  }
+}
+
+// ---------------------------------------------------------------------------------------------
+// RMSNorm of listed rows: one wave per row, float32 sum of squares in a fixed order.
+// ---------------------------------------------------------------------------------------------
+__global__ __launch_bounds__(256) void rmsnorm_rows_kernel(const ReqDev* __restrict__ reqs, const int32_t* __restrict__ rows,
+                                                           const int32_t* __restrict__ n_rows,
+                                                           const uint16_t* __restrict__ x, int x_tok,
+                                                           const uint16_t* __restrict__ gamma, float eps, int H,
+                                                           uint16_t* __restrict__ y, int y_tok) {
+  const ReqDev rq = reqs[blockIdx.y];
+  const int n = blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  if (n >= n_rows[blockIdx.y]) return;
+  const uint16_t* xr = x + row_index(rq, rows, n, x_tok) * H;
+  uint16_t* yr = y + row_index(rq, rows, n, y_tok) * H;
+  float ss = 0.f;
+  for (int c = lane * 8; c < H; c += 64 * 8) {
+    const uint4 v = *(const uint4*)(xr + c);
+    const uint32_t u[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const float lo = bf16_lo(u[i]), hi = bf16_hi(u[i]);
+      ss = __builtin_fmaf(lo, lo, ss);
+      ss = __builtin_fmaf(hi, hi, ss);
+    }
+  }
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) ss += __shfl_xor(ss, o, 64);
+  const float inv = 1.0f / sqrtf(ss / (float)H + eps);
+  for (int c = lane * 8; c < H; c += 64 * 8) {
+    const uint4 v = *(const uint4*)(xr + c);
+    const uint4 gv = *(const uint4*)(gamma + c);
+    const uint32_t u[4] = {v.x, v.y, v.z, v.w}, gw[4] = {gv.x, gv.y, gv.z, gv.w};
+    uint32_t o[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+      o[i] = pack_bf16x2(bf16_lo(u[i]) * inv * bf16_lo(gw[i]), bf16_hi(u[i]) * inv * bf16_hi(gw[i]));
+    *(uint4*)(yr + c) = make_uint4(o[0], o[1], o[2], o[3]);
+  }
+}
+
+// ---------------------------------------------------------------------------------------------
+// RoPE of the fresh query and key rows of listed tokens, in place.  A thread owns 8 rotation
+// pairs of one token: it forms their cos / sin once (angle and cos / sin in float64, rounded to
+// float32) and rotates those pairs in every query and key head (float32, no contraction, bf16
+// store with round to nearest even).
+// ---------------------------------------------------------------------------------------------
+template <int D, bool NEOX>
+__global__ __launch_bounds__(256) void rope_rows_kernel(const ReqDev* __restrict__ reqs, const int32_t* __restrict__ rows,
+                                                        const int32_t* __restrict__ n_rows,
+                                                        const int32_t* __restrict__ tok_pos,
+                                                        const double* __restrict__ theta, uint16_t* __restrict__ q,
+                                                        uint16_t* __restrict__ k, int Hq, int Hkv) {
+  constexpr int UPR = D / 16;   // threads per token: 8 pairs each
+  const ReqDev rq = reqs[blockIdx.y];
+  const int g = blockIdx.x * blockDim.x + threadIdx.x;
+  const int n = g / UPR;
+  const int u = g - n * UPR;
+  if (n >= n_rows[blockIdx.y]) return;
+  const int64_t t = row_index(rq, rows, n, true);
+  const double pos = (double)tok_pos[t];
+  float c[8], s[8];
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    const double phi = pos * theta[u * 8 + e];
+    c[e] = (float)cos(phi);
+    s[e] = (float)sin(phi);
+  }
+  // pair p = 8u + e: NEOX (p, p + D/2); GPT-J (2p, 2p + 1)
+  auto rotate_head = [&](uint16_t* h) {
+#pragma clang fp contract(off)
+    if constexpr (NEOX) {
+      uint4* pa = (uint4*)(h + u * 8);
+      uint4* pb = (uint4*)(h + D / 2 + u * 8);
+      const uint4 va = *pa, vb = *pb;
+      const uint32_t wa[4] = {va.x, va.y, va.z, va.w}, wb[4] = {vb.x, vb.y, vb.z, vb.w};
+      uint32_t oa[4], ob[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const float a0 = bf16_lo(wa[i]), a1 = bf16_hi(wa[i]), b0 = bf16_lo(wb[i]), b1 = bf16_hi(wb[i]);
+        const int e0 = 2 * i, e1 = 2 * i + 1;
+        oa[i] = pack_bf16x2(a0 * c[e0] - b0 * s[e0], a1 * c[e1] - b1 * s[e1]);
+        ob[i] = pack_bf16x2(b0 * c[e0] + a0 * s[e0], b1 * c[e1] + a1 * s[e1]);
+      }
+      *pa = make_uint4(oa[0], oa[1], oa[2], oa[3]);
+      *pb = make_uint4(ob[0], ob[1], ob[2], ob[3]);
+    } else {
+      uint4* pp = (uint4*)(h + u * 16);
+      const uint4 v0 = pp[0], v1 = pp[1];
+      const uint32_t w[8] = {v0.x, v0.y, v0.z, v0.w, v1.x, v1.y, v1.z, v1.w};
+      uint32_t o[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const float x1 = bf16_lo(w[e]), x2 = bf16_hi(w[e]);
+        o[e] = pack_bf16x2(x1 * c[e] - x2 * s[e], x2 * c[e] + x1 * s[e]);
+      }
+      pp[0] = make_uint4(o[0], o[1], o[2], o[3]);
+      pp[1] = make_uint4(o[4], o[5], o[6], o[7]);
+    }
+  };
+  for (int h = 0; h < Hq; ++h) rotate_head(q + (t * Hq + h) * D);
+  for (int h = 0; h < Hkv; ++h) rotate_head(k + (t * Hkv + h) * D);
+}
+
+// ---------------------------------------------------------------------------------------------
+// SwiGLU activation of listed rows (slot-indexed): gu row = [gate (f) | up (f)] -> y row (f).
+// silu(g) = g / (1 + e^-g) in float32.
+// ---------------------------------------------------------------------------------------------
+__global__ __launch_bounds__(256) void silu_mul_rows_kernel(const ReqDev* __restrict__ reqs,
+                                                            const int32_t* __restrict__ n_rows,
+                                                            const uint16_t* __restrict__ gu, int f,
+                                                            uint16_t* __restrict__ y) {
+  const ReqDev rq = reqs[blockIdx.y];
+  const int64_t g = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const int upr = f / 8;
+  const int64_t n = g / upr;
+  const int c = (int)(g - n * upr) * 8;
+  if (n >= n_rows[blockIdx.y]) return;
+  const int64_t row = (int64_t)rq.tok_off + n;
+  const uint4 gv = *(const uint4*)(gu + row * 2 * f + c);
+  const uint4 uv = *(const uint4*)(gu + row * 2 * f + f + c);
+  const uint32_t gw[4] = {gv.x, gv.y, gv.z, gv.w}, uw[4] = {uv.x, uv.y, uv.z, uv.w};
+  uint32_t o[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const float g0 = bf16_lo(gw[i]), g1 = bf16_hi(gw[i]);
+    const float s0 = g0 / (1.0f + expf(-g0)), s1 = g1 / (1.0f + expf(-g1));
+    o[i] = pack_bf16x2(s0 * bf16_lo(uw[i]), s1 * bf16_hi(uw[i]));
+  }
+  *(uint4*)(y + row * f + c) = make_uint4(o[0], o[1], o[2], o[3]);
+}
+
+}  // namespace
+
+hipError_t launch_gemm_rows(const sx_plan* p, const RowsArg& r, const void* x, int x_tok, const void* w, int k, int n,
+                            const void* res, void* y, int y_tok, hipStream_t s) {
+  GemmRowsK a{};
+  a.reqs = p->d_req;
+  a.rows = r.rows;
+  a.n_rows = r.n_rows;
+  a.x = (const uint16_t*)x;
+  a.w = (const uint16_t*)w;
+  a.res = (const uint16_t*)res;
+  a.y = (uint16_t*)y;
+  a.K = k;
+  a.N = n;
+  a.n_req = p->n_req;
+  a.m_tiles = (r.max_rows + GBM - 1) / GBM;
+  a.x_tok = x_tok;
+  a.y_tok = y_tok;
+  const int64_t blocks = (int64_t)a.m_tiles * p->n_req * (n / GBN);
+  hipLaunchKernelGGL(gemm_rows_kernel, dim3((unsigned)blocks), dim3(512), 0, s, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_rmsnorm_rows(const sx_plan* p, const RowsArg& r, const void* x, int x_tok, const void* gamma,
+                               float eps, int h, void* y, int y_tok, hipStream_t s) {
+  const dim3 grid((unsigned)((r.max_rows + 3) / 4), (unsigned)p->n_req);
+  hipLaunchKernelGGL(rmsnorm_rows_kernel, grid, dim3(256), 0, s, p->d_req, r.rows, r.n_rows, (const uint16_t*)x, x_tok,
+                     (const uint16_t*)gamma, eps, h, (uint16_t*)y, y_tok);
+  return hipGetLastError();
+}
+
+hipError_t launch_rope_rows(const sx_plan* p, const RowsArg& r, void* q, void* k, hipStream_t s) {
+  const int D = p->desc.head_dim;
+  const int64_t threads = (int64_t)r.max_rows * (D / 16);
+  const dim3 grid((unsigned)((threads + 255) / 256), (unsigned)p->n_req);
+  const bool neox = p->desc.rope_style == SX_ROPE_NEOX;
+  const int Hq = p->desc.n_q_heads, Hkv = p->desc.n_kv_heads;
+#define SX_ROPE(D_, N_)                                                                                               \
+  hipLaunchKernelGGL((rope_rows_kernel<D_, N_>), grid, dim3(256), 0, s, p->d_req, r.rows, r.n_rows, p->d_tok_pos,   \
+                     p->d_theta, (uint16_t*)q, (uint16_t*)k, Hq, Hkv)
+  if (D == 128) {
+    if (neox) SX_ROPE(128, true); else SX_ROPE(128, false);
+  } else {
+    if (neox) SX_ROPE(64, true); else SX_ROPE(64, false);
+  }
+#undef SX_ROPE
+  return hipGetLastError();
+}
+
+hipError_t launch_silu_mul_rows(const sx_plan* p, const RowsArg& r, const void* gu, int f, void* y, hipStream_t s) {
+  const int64_t threads = (int64_t)r.max_rows * (f / 8);
+  const dim3 grid((unsigned)((threads + 255) / 256), (unsigned)p->n_req);
+  hipLaunchKernelGGL(silu_mul_rows_kernel, grid, dim3(256), 0, s, p->d_req, r.n_rows, (const uint16_t*)gu, f,
+                     (uint16_t*)y);
+  return hipGetLastError();
+}
+
+}  // namespace sx

@@ -87,7 +87,7 @@ void free_plan(sx_plan* p) {
   if (!p) return;
   void* bufs[] = {p->d_req, p->d_bt, p->d_ra, p->d_cs, p->d_probe, p->d_nr, p->d_n_nr, p->d_n_probe,
                   p->d_flags, p->d_tok_slot, p->d_tok_ra, p->d_rmark, p->d_lse, p->d_colsum,
-                  p->d_qp, p->d_lse2p};
+                  p->d_qp, p->d_lse2p, p->d_tok_pos, p->d_theta};
   for (void* b : bufs)
     if (b) (void)hipFree(b);
   delete p;
@@ -188,7 +188,7 @@ sx_status sx_plan_create(const sx_layer_desc* desc, const sx_request* requests, 
   std::vector<int32_t> probe((size_t)total + sx::kProbePad, 0), nr((size_t)total, 0);
   std::vector<int32_t> n_nr(n_requests), n_probe(n_requests);
   std::vector<uint8_t> flags((size_t)total, 0);
-  std::vector<int32_t> tok_slot((size_t)total, 0), tok_ra((size_t)total, -1);
+  std::vector<int32_t> tok_slot((size_t)total, 0), tok_ra((size_t)total, -1), tok_pos((size_t)total, 0);
   std::vector<double> theta(d / 2);
   for (int i = 0; i < d / 2; ++i) theta[i] = std::pow(desc->rope_base, -2.0 * i / d);
   int64_t off = 0;
@@ -207,6 +207,7 @@ sx_status sx_plan_create(const sx_layer_desc* desc, const sx_request* requests, 
     const sx_segment* last = nullptr;
     for (int m = 0; m < q.n_segments; ++m) {
       const sx_segment& s = q.segments[m];
+      for (int j = 0; j < s.length; ++j) tok_pos[off + s.seq_start + j] = s.new_pos + j;
       if (s.seq_start <= T - 1 && T - 1 < s.seq_start + s.length) last = &s;
       if (!s.cached) continue;
       const double delta = (double)s.new_pos - (double)s.old_pos;
@@ -281,6 +282,8 @@ sx_status sx_plan_create(const sx_layer_desc* desc, const sx_request* requests, 
   if (st == SX_OK) st = dev_upload(p, &p->d_flags, flags);
   if (st == SX_OK) st = dev_upload(p, &p->d_tok_slot, tok_slot);
   if (st == SX_OK) st = dev_upload(p, &p->d_tok_ra, tok_ra);
+  if (st == SX_OK) st = dev_upload(p, &p->d_tok_pos, tok_pos);
+  if (st == SX_OK) st = dev_upload(p, &p->d_theta, theta);
   if (st == SX_OK) st = dev_upload(p, &p->d_rmark, std::vector<uint32_t>((size_t)total, 0u));
   if (st == SX_OK) st = dev_alloc(p, &p->d_lse, (size_t)total * desc->n_q_heads);
   if (st == SX_OK) st = dev_alloc(p, &p->d_colsum, (size_t)total * desc->n_kv_heads);
@@ -438,6 +441,70 @@ sx_status sx_realign_scatter(const sx_plan* p, const void* src_k, const void* sr
                              void* k_cache, void* v_cache, void* stream) {
   const sx_layer_kv one{src_k, src_v, k_new, v_new, k_cache, v_cache};
   return sx_realign_scatter_layers(p, 1, &one, rows, n_rows, max_rows, stream);
+}
+
+namespace {
+
+sx_status check_rows(const sx_plan* p, const int32_t* rows, const int32_t* n_rows, int32_t max_rows, bool need_rows) {
+  if (!p) return fail(SX_EINVAL, "plan is NULL");
+  if (p->desc.dtype != SX_BF16) return fail(SX_EUNSUPPORTED, "the layer body runs on bfloat16 plans");
+  if (!n_rows || (need_rows && !rows)) return fail(SX_EINVAL, "NULL row list");
+  if (max_rows < 0) return fail(SX_EINVAL, "max_rows must be >= 0");
+  if (max_rows > p->max_T) return fail(SX_ESHAPE, "max_rows %d exceeds the longest request (%d)", max_rows, p->max_T);
+  return SX_OK;
+}
+
+}  // namespace
+
+sx_status sx_gemm_rows(const sx_plan* p, const int32_t* rows, const int32_t* n_rows, int32_t max_rows, const void* x,
+                       int32_t x_by_token, const void* w, int32_t k, int32_t n, const void* residual, void* y,
+                       int32_t y_by_token, void* stream) {
+  sx_status st = check_rows(p, rows, n_rows, max_rows, x_by_token || y_by_token);
+  if (st != SX_OK) return st;
+  if (!x || !w || !y) return fail(SX_EINVAL, "NULL tensor argument");
+  if (k <= 0 || n <= 0 || k % 64 != 0 || n % 256 != 0)
+    return fail(SX_EUNSUPPORTED, "sx_gemm_rows needs k a multiple of 64 and n a multiple of 256 (k=%d n=%d)", k, n);
+  if (max_rows == 0) return SX_OK;
+  const sx::RowsArg r{rows, n_rows, max_rows};
+  return check_launch(sx::launch_gemm_rows(p, r, x, x_by_token != 0, w, k, n, residual, y, y_by_token != 0,
+                                           (hipStream_t)stream),
+                      "sx_gemm_rows launch");
+}
+
+sx_status sx_rmsnorm_rows(const sx_plan* p, const int32_t* rows, const int32_t* n_rows, int32_t max_rows,
+                          const void* x, int32_t x_by_token, const void* gamma, float eps, int32_t h, void* y,
+                          int32_t y_by_token, void* stream) {
+  sx_status st = check_rows(p, rows, n_rows, max_rows, x_by_token || y_by_token);
+  if (st != SX_OK) return st;
+  if (!x || !gamma || !y) return fail(SX_EINVAL, "NULL tensor argument");
+  if (h <= 0 || h % 8 != 0) return fail(SX_EUNSUPPORTED, "hidden size %d must be a positive multiple of 8", h);
+  if (!(eps > 0.0f) || !std::isfinite(eps)) return fail(SX_EINVAL, "eps must be finite and > 0");
+  if (max_rows == 0) return SX_OK;
+  const sx::RowsArg r{rows, n_rows, max_rows};
+  return check_launch(sx::launch_rmsnorm_rows(p, r, x, x_by_token != 0, gamma, eps, h, y, y_by_token != 0,
+                                              (hipStream_t)stream),
+                      "sx_rmsnorm_rows launch");
+}
+
+sx_status sx_rope_rows(const sx_plan* p, const int32_t* rows, const int32_t* n_rows, int32_t max_rows, void* q,
+                       void* k, void* stream) {
+  sx_status st = check_rows(p, rows, n_rows, max_rows, true);
+  if (st != SX_OK) return st;
+  if (!q || !k) return fail(SX_EINVAL, "NULL tensor argument");
+  if (max_rows == 0) return SX_OK;
+  const sx::RowsArg r{rows, n_rows, max_rows};
+  return check_launch(sx::launch_rope_rows(p, r, q, k, (hipStream_t)stream), "sx_rope_rows launch");
+}
+
+sx_status sx_silu_mul_rows(const sx_plan* p, const int32_t* n_rows, int32_t max_rows, const void* gate_up, int32_t f,
+                           void* y, void* stream) {
+  sx_status st = check_rows(p, nullptr, n_rows, max_rows, false);
+  if (st != SX_OK) return st;
+  if (!gate_up || !y) return fail(SX_EINVAL, "NULL tensor argument");
+  if (f <= 0 || f % 8 != 0) return fail(SX_EUNSUPPORTED, "feed-forward size %d must be a positive multiple of 8", f);
+  if (max_rows == 0) return SX_OK;
+  const sx::RowsArg r{nullptr, n_rows, max_rows};
+  return check_launch(sx::launch_silu_mul_rows(p, r, gate_up, f, y, (hipStream_t)stream), "sx_silu_mul_rows launch");
 }
 
 sx_status sx_sparseq_score(const sx_plan* p, const void* q, const void* k_cache, const float* lse_in, float* scores,

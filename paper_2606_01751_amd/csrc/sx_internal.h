@@ -73,6 +73,8 @@ struct sx_plan {
   mutable uint32_t rgen = 0;      // last generation used
   float* d_lse = nullptr;         // scratch [sum T][Hq]
   double* d_colsum = nullptr;     // scratch [Hkv][sum T]
+  int32_t* d_tok_pos = nullptr;   // [sum T] RoPE position of every token in the new sequence
+  double* d_theta = nullptr;      // [d/2] RoPE frequencies base^(-2i/d), float64
   void* d_qp = nullptr;           // scratch [n_probe][Hq][d]: query rows of the probe rows (bf16 plans)
   float* d_lse2p = nullptr;       // scratch [Hkv][n_probe][Hq / Hkv]: their base-2 log-sum-exp
 };
@@ -97,6 +99,21 @@ hipError_t launch_rows_mask(const sx_plan* p, const int32_t* rows, const int32_t
                             uint8_t* mask, hipStream_t s);
 hipError_t launch_topk(const sx_plan* p, const float* scores, double ratio, int32_t* rows, int32_t* n_rows,
                        hipStream_t s);
+
+// Row-sparse layer body (defined in k_layer.hip).  Rows are the listed rows of every request in
+// the row-list layout; an operand row is addressed by slot (off_r + n) or by token
+// (off_r + rows[off_r + n]).
+struct RowsArg {
+  const int32_t* rows;
+  const int32_t* n_rows;
+  int32_t max_rows;
+};
+hipError_t launch_gemm_rows(const sx_plan* p, const RowsArg& r, const void* x, int x_tok, const void* w, int k, int n,
+                            const void* res, void* y, int y_tok, hipStream_t s);
+hipError_t launch_rmsnorm_rows(const sx_plan* p, const RowsArg& r, const void* x, int x_tok, const void* gamma,
+                               float eps, int h, void* y, int y_tok, hipStream_t s);
+hipError_t launch_rope_rows(const sx_plan* p, const RowsArg& r, void* q, void* k, hipStream_t s);
+hipError_t launch_silu_mul_rows(const sx_plan* p, const RowsArg& r, const void* gu, int f, void* y, hipStream_t s);
 
 // Attention family.  Mode selects the query rows and the key source.
 struct AttnLaunch {

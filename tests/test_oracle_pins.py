@@ -378,7 +378,8 @@ def test_full_attention_matches_torch_sdpa():
     rng = np.random.default_rng(41)
     T, Hq, Hkv, d = 70, 8, 2, 16
     q, k, v = (rng.standard_normal((T, h, d)) for h in (Hq, Hkv, Hkv))
-    got = O.full_attention(q, k, v, 1 / math.sqrt(d))
+    # the oracle's own scale against torch's default 1/sqrt(d) (pins softmax_scale too)
+    got = O.full_attention(q, k, v, O.softmax_scale(d))
     tq = torch.from_numpy(q).permute(1, 0, 2)
     tk = torch.from_numpy(k).permute(1, 0, 2).repeat_interleave(Hq // Hkv, dim=0)
     tv = torch.from_numpy(v).permute(1, 0, 2).repeat_interleave(Hq // Hkv, dim=0)
@@ -449,3 +450,131 @@ def test_scatter_is_exact_and_local():
     others = np.setdiff1d(np.arange(95), rows)
     assert np.all(gk[others] == -3.0) and np.all(gv[others] == -3.0)
     assert (kp != -3.0).sum() == len(rows) * 8
+
+
+# ----------------------------------------------------------------------------------------------
+# Row-sparse layer body (Algorithm 1 steps 19 and 22)
+# ----------------------------------------------------------------------------------------------
+
+def test_rmsnorm_closed_form_and_invariants():
+    # [3, 4]: mean square 12.5, so the row becomes [3, 4] / sqrt(12.5)
+    y = O.rmsnorm(np.array([[3.0, 4.0]]), np.array([1.0, 1.0]), 0.0)
+    np.testing.assert_allclose(y, [[0.8485281374238571, 1.1313708498984762]], rtol=1e-15)
+    rng = np.random.default_rng(0)
+    x = rng.standard_normal((5, 64))
+    g = rng.standard_normal(64)
+    # scale invariance without eps, mean square 1 with unit gamma, gamma multiplies elementwise
+    np.testing.assert_allclose(O.rmsnorm(7.5 * x, g, 0.0), O.rmsnorm(x, g, 0.0), rtol=1e-12)
+    np.testing.assert_allclose(np.mean(O.rmsnorm(x, np.ones(64), 0.0) ** 2, axis=1), 1.0, rtol=1e-12)
+    np.testing.assert_allclose(O.rmsnorm(x, 2.0 * g, 0.0), 2.0 * O.rmsnorm(x, g, 0.0), rtol=1e-12)
+    # eps bounds a zero row
+    assert np.all(O.rmsnorm(np.zeros((1, 8)), np.ones(8), 1e-6) == 0.0)
+
+
+def test_linear_matches_loops_and_identity():
+    rng = np.random.default_rng(1)
+    x = rng.integers(-5, 6, size=(3, 7)).astype(np.float64)
+    w = rng.integers(-5, 6, size=(4, 7)).astype(np.float64)
+    r = rng.integers(-5, 6, size=(3, 4)).astype(np.float64)
+    loops = np.zeros((3, 4))
+    for i in range(3):
+        for j in range(4):
+            for kk in range(7):
+                loops[i, j] += x[i, kk] * w[j, kk]
+    assert np.array_equal(O.linear(x, w), loops)
+    assert np.array_equal(O.linear(x, w, r), loops + r)
+    assert np.array_equal(O.linear(x, np.eye(7)), x)
+
+
+@pytest.mark.parametrize("style", ["neox", "gptj"])
+def test_rope_at_positions_absolute_and_relative(style):
+    rng = np.random.default_rng(2)
+    d, base = 64, 1e4
+    x = rng.standard_normal((3, 2, d)).astype(np.float32)
+    # position 0 is the identity; a position p matches the complex-number absolute RoPE
+    assert np.array_equal(O.rope_at_positions(x, [0, 0, 0], base, style), x)
+    pos = [5, 300, 4097]
+    got = O.rope_at_positions(x, pos, base, style)
+    for i, p in enumerate(pos):
+        np.testing.assert_allclose(got[i], _rope_complex(x[i], p, base, style), atol=2e-5)
+    # relative property: <R_a q, R_b k> depends on a - b only
+    q = x[0, 0][None, None]
+    k = x[1, 0][None, None]
+    def dot(a, b):
+        return float(np.dot(O.rope_at_positions(q, [a], base, style)[0, 0].astype(np.float64),
+                            O.rope_at_positions(k, [b], base, style)[0, 0].astype(np.float64)))
+    assert abs(dot(10, 3) - dot(1010, 1003)) < 1e-4
+    assert abs(dot(10, 3) - dot(3, 10)) > 1e-3   # the rotation has a direction
+
+
+def test_silu_mul_closed_forms():
+    g = np.array([0.0, 1.0, 30.0, -30.0])
+    y = O.silu_mul(np.concatenate([g, np.ones(4)])[None])[0]
+    np.testing.assert_allclose(y[:2], [0.0, 1.0 / (1.0 + math.exp(-1.0))], rtol=1e-15)
+    np.testing.assert_allclose(y[2], 30.0, rtol=1e-12)      # silu(g) -> g for large g
+    assert abs(y[3]) < 1e-11                                 # -> 0 for very negative g
+    u = np.array([2.0, -3.0, 0.5, 4.0])
+    np.testing.assert_allclose(O.silu_mul(np.concatenate([g, u])[None])[0], y * u, rtol=1e-15)
+
+
+def _dense_block(hidden, wts, w, eps):
+    """The same Llama block written densely over every token, attention by the per-row causal
+    formulation (independent of the row-list routing of layer_body)."""
+    T = hidden.shape[0]
+    Hq, Hkv, d = w.n_q_heads, w.n_kv_heads, w.head_dim
+    st = lambda a: O.store(a, w.dtype)
+    x1 = st(O.rmsnorm(hidden, wts["ln1"], eps))
+    q = st(O.linear(x1, wts["wq"])).reshape(T, Hq, d)
+    k = st(O.linear(x1, wts["wk"])).reshape(T, Hkv, d)
+    v = st(O.linear(x1, wts["wv"])).reshape(T, Hkv, d)
+    pos = np.arange(T)
+    q = st(O.rope_at_positions(q, pos, w.rope_base, w.rope_style))
+    k = st(O.rope_at_positions(k, pos, w.rope_base, w.rope_style))
+    att = st(O.full_attention(q, k, v, O.softmax_scale(d))).reshape(T, Hq * d)
+    h1 = st(O.linear(att, wts["wo"], hidden))
+    x2 = st(O.rmsnorm(h1, wts["ln2"], eps))
+    a = st(O.silu_mul(st(O.linear(x2, wts["wgu"]))))
+    return st(O.linear(a, wts["wd"], h1))
+
+
+def _body_weights(rng, H, Hq, Hkv, d, F):
+    def m(o, i):
+        return O.to_bf16((rng.standard_normal((o, i)) / math.sqrt(i)).astype(np.float32))
+    return {"ln1": O.to_bf16((1 + 0.1 * rng.standard_normal(H)).astype(np.float32)), "wq": m(Hq * d, H),
+            "wk": m(Hkv * d, H), "wv": m(Hkv * d, H), "wo": m(H, Hq * d),
+            "ln2": O.to_bf16((1 + 0.1 * rng.standard_normal(H)).astype(np.float32)), "wgu": m(2 * F, H),
+            "wd": m(H, F)}
+
+
+def test_layer_body_with_every_row_equals_dense_block():
+    """No cached segment and R = every token: the row-sparse body is the plain dense block."""
+    specs = [[(40, False, 0, None)]]
+    w = W.custom_workload(specs, n_q_heads=4, n_kv_heads=2, head_dim=16, dtype="bf16", rope_base=1e4, seed=5,
+                          name="body-dense")
+    T, H = 40, 64
+    rng = np.random.default_rng(3)
+    hidden = O.to_bf16(rng.standard_normal((T, H)).astype(np.float32))
+    wts = _body_weights(rng, H, 4, 2, 16, 96)
+    t = W.layer_tensors(w, 0)
+    body = O.layer_body(w, hidden, np.arange(T), wts, t["k_src"], t["v_src"], 1e-5)
+    dense = _dense_block(hidden, wts, w, 1e-5)
+    np.testing.assert_allclose(body["h2"], dense, atol=1e-6)
+
+
+def test_layer_body_rows_depend_only_on_their_own_inputs_and_the_cache():
+    """A row of R is computed from its own hidden state and the cache: dropping other rows of R
+    from the set changes nothing for it as long as the cache is the same (here every token is
+    cached, so rows outside R read re-aligned keys either way -- except the dropped rows' own
+    slots, which is why only rows before the dropped ones are compared)."""
+    specs = [[(32, True, 3, None), (16, False, 0, None), (32, True, 50, None)]]
+    w = W.custom_workload(specs, n_q_heads=4, n_kv_heads=2, head_dim=16, dtype="bf16", rope_base=1e4, seed=6,
+                          name="body-local")
+    T, H = 80, 64
+    rng = np.random.default_rng(4)
+    hidden = O.to_bf16(rng.standard_normal((T, H)).astype(np.float32))
+    wts = _body_weights(rng, H, 4, 2, 16, 96)
+    t = W.layer_tensors(w, 0)
+    R = np.array([2, 7, 32, 40, 47, 60, 70])
+    full = O.layer_body(w, hidden, R, wts, t["k_src"], t["v_src"], 1e-5)
+    part = O.layer_body(w, hidden, R[:4], wts, t["k_src"], t["v_src"], 1e-5)
+    np.testing.assert_array_equal(full["h2"][:4], part["h2"])
