@@ -250,8 +250,9 @@ def main():
             return (1 + 0.1 * torch.randn(H, generator=gen, device="cuda", dtype=torch.float32)).to(dt)
         body = {"w": [], "hidden": torch.randn((T, H), generator=gen, device="cuda", dtype=torch.float32).to(dt)}
         for l in range(nfull, L):
-            body["w"].append({"ln1": norm_w(), "wq": lin(Hq * d, H), "wk": lin(Hkv * d, H), "wv": lin(Hkv * d, H),
-                              "wo": lin(H, Hq * d), "ln2": norm_w(), "wgu": lin(2 * F, H), "wd": lin(H, F)})
+            # wqkv stacks the query, key and value projections ([(Hq + 2 Hkv) d][H])
+            body["w"].append({"ln1": norm_w(), "wqkv": lin((Hq + 2 * Hkv) * d, H), "wo": lin(H, Hq * d),
+                              "ln2": norm_w(), "wgu": lin(2 * F, H), "wd": lin(H, F)})
         z = lambda *shape: torch.zeros(shape, dtype=dt, device="cuda")
         body.update({"x1": z(T, H), "att": z(T, Hq, d), "h1": z(T, H), "x2": z(T, H), "gu": z(T, 2 * F),
                      "a": z(T, F)})
@@ -266,12 +267,8 @@ def main():
         hid = body["hidden"]
         tm.run("sx_rmsnorm_rows", lambda: sx.rmsnorm_rows(plan, rows, n_rows, max_rows, hid, wl["ln1"], eps, body["x1"],
                                                           x_by_token=True))
-        tm.run("sx_gemm_rows qkv", lambda: (sx.gemm_rows(plan, rows, n_rows, max_rows, body["x1"], wl["wq"], tl["q"],
-                                                         y_by_token=True),
-                                            sx.gemm_rows(plan, rows, n_rows, max_rows, body["x1"], wl["wk"], tl["k"],
-                                                         y_by_token=True),
-                                            sx.gemm_rows(plan, rows, n_rows, max_rows, body["x1"], wl["wv"], tl["v"],
-                                                         y_by_token=True)))
+        tm.run("sx_gemm_rows qkv", lambda: sx.gemm_rows_split(plan, rows, n_rows, max_rows, body["x1"], wl["wqkv"],
+                                                              [tl["q"], tl["k"], tl["v"]], y_by_token=True))
         tm.run("sx_rope_rows", lambda: sx.rope_rows(plan, rows, n_rows, max_rows, tl["q"], tl["k"]))
         tm.run("sx_realign_scatter_masked",
                lambda: sx.realign_scatter_masked(plan, tl["k_src"], tl["v_src"], tl["k"], tl["v"], rmask, tl["kc"],

@@ -278,6 +278,16 @@ sx_status sx_gemm_rows(const sx_plan* plan, const int32_t* rows, const int32_t* 
                        const void* x, int32_t x_by_token, const void* w, int32_t k, int32_t n,
                        const void* residual, void* y, int32_t y_by_token, void* stream);
 
+/* The same product for a weight made of stacked parts, each written to its own output: w is
+ * [sum part_n][k] (part i = rows sum_{j<i} part_n[j] .. of w, e.g. the query, key and value
+ * projections stacked), and columns of part i land in y_parts[i], [..][part_n[i]], addressed by
+ * y_by_token like sx_gemm_rows' y.  part_n (host array of n_parts, 1 <= n_parts <= 4): positive
+ * multiples of 256; y_parts: host array of DEVICE pointers.  No residual.  One launch for all the
+ * parts, so narrow parts share the machine. */
+sx_status sx_gemm_rows_split(const sx_plan* plan, const int32_t* rows, const int32_t* n_rows, int32_t max_rows,
+                             const void* x, int32_t x_by_token, const void* w, int32_t k, int32_t n_parts,
+                             const int32_t* part_n, void* const* y_parts, int32_t y_by_token, void* stream);
+
 /* RMSNorm: y[row] = x[row] / sqrt(mean_j x[row][j]^2 + eps) * gamma, rows of h elements
  * (h a multiple of 8), gamma [h]; the sum of squares is float32 in a fixed order. */
 sx_status sx_rmsnorm_rows(const sx_plan* plan, const int32_t* rows, const int32_t* n_rows, int32_t max_rows,

@@ -39,7 +39,7 @@ EXPORTED = (
     "sx_plan_create", "sx_plan_destroy", "sx_plan_get_info", "sx_plan_budget", "sx_plan_nonreused_rows",
     "sx_rope_realign", "sx_kv_scatter", "sx_realign_scatter", "sx_realign_scatter_layers", "sx_rows_mask",
     "sx_realign_scatter_masked", "sx_sparseq_score", "sx_topk_select",
-    "sx_sparse_attn", "sx_full_attn", "sx_gemm_rows", "sx_rmsnorm_rows", "sx_rope_rows", "sx_silu_mul_rows",
+    "sx_sparse_attn", "sx_full_attn", "sx_gemm_rows", "sx_gemm_rows_split", "sx_rmsnorm_rows", "sx_rope_rows", "sx_silu_mul_rows",
     "sx_last_error", "sx_version",
 )
 
@@ -108,6 +108,7 @@ def lib() -> ctypes.CDLL:
         L.sx_full_attn.argtypes = [P(LayerDesc), VP, VP, VP, VP, I32, I32, VP, VP, VP]
         F = ctypes.c_float
         L.sx_gemm_rows.argtypes = [VP, VP, VP, I32, VP, I32, VP, I32, I32, VP, VP, I32, VP]
+        L.sx_gemm_rows_split.argtypes = [VP, VP, VP, I32, VP, I32, VP, I32, I32, P(I32), P(VP), I32, VP]
         L.sx_rmsnorm_rows.argtypes = [VP, VP, VP, I32, VP, I32, VP, F, I32, VP, I32, VP]
         L.sx_rope_rows.argtypes = [VP, VP, VP, I32, VP, VP, VP]
         L.sx_silu_mul_rows.argtypes = [VP, VP, I32, VP, I32, VP, VP]
@@ -282,6 +283,22 @@ def gemm_rows(plan: Plan, rows, n_rows, max_rows: int, x, w, y, residual=None, x
     n, k = int(w.shape[0]), int(w.shape[1])
     _check(lib().sx_gemm_rows(plan.handle, _ptr(rows), _ptr(n_rows), int(max_rows), _ptr(x), int(bool(x_by_token)),
                               _ptr(w), k, n, _ptr(residual), _ptr(y), int(bool(y_by_token)), _stream(stream)))
+
+
+def gemm_rows_split(plan: Plan, rows, n_rows, max_rows: int, x, w, ys, x_by_token=False, y_by_token=False,
+                    stream=None):
+    """One launch of y = x @ w.T for a weight of stacked parts: w is [sum n_i][k] and the columns of
+    part i go to ys[i] (its last dimension flattened: [..][n_i])."""
+    k = int(w.shape[1])
+    widths = [int(y.numel() // y.shape[0]) for y in ys]
+    if sum(widths) != int(w.shape[0]):
+        raise ValueError(f"output widths {widths} do not add up to the weight's {int(w.shape[0])} rows")
+    n = len(ys)
+    part_n = (ctypes.c_int32 * n)(*widths)
+    y_parts = (ctypes.c_void_p * n)(*[_ptr(y) for y in ys])
+    _check(lib().sx_gemm_rows_split(plan.handle, _ptr(rows), _ptr(n_rows), int(max_rows), _ptr(x),
+                                    int(bool(x_by_token)), _ptr(w), k, n, part_n, y_parts, int(bool(y_by_token)),
+                                    _stream(stream)))
 
 
 def rmsnorm_rows(plan: Plan, rows, n_rows, max_rows: int, x, gamma, eps: float, y, x_by_token=False,

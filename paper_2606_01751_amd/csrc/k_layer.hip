@@ -30,13 +30,17 @@ __device__ __forceinline__ int64_t row_index(const ReqDev& rq, const int32_t* ro
 // GEMM on listed rows.  Computed transposed, Y^T = W X^T: the MFMA A operand is a 32 x 16 slice of
 // W (32 output features), the B operand a 16 x 32 slice of X^T (32 rows), so each lane owns one
 // row of the result and writes 4 consecutive features per store.
-// Workgroup tile: 256 features x 256 rows, 64 of k per stage; 8 waves as 4 (features) x 2 (rows),
-// a wave owns 64 features x 128 rows (2 x 4 accumulators of 32 x 32).  Both operand tiles move
-// global -> LDS directly (16 bytes per lane), double-buffered; rows of 128 bytes with their eight
-// 16-byte chunks XOR-swizzled by (row / 2) mod 8, conflict-free for the 16-byte operand reads.
+// Workgroup tile: 256 features x 256 rows; 8 waves as 4 (features) x 2 (rows), a wave owns 64
+// features x 128 rows (2 x 4 accumulators of 32 x 32).  The k dimension moves in stages of BK
+// through NST LDS buffers: both operand tiles go global -> LDS directly (16 bytes per lane);
+// stage t + NST is issued once every wave has read stage t, so a stage has about NST - 1 stages
+// of compute to land.  A tile row (BK bf16) holds BK / 8 chunks of 16 bytes, XOR-swizzled per row (chunk_swz)
+// so that the rows a read instruction touches at one logical chunk hit distinct banks.
 // ---------------------------------------------------------------------------------------------
-constexpr int GBN = 256, GBM = 256, GBK = 64;
-constexpr int GTILE = 256 * GBK * 2;            // bytes of one operand tile (32 KB)
+constexpr int GBN = 256, GBM = 256;
+constexpr int kGemmMaxParts = 4;
+constexpr unsigned kGemmXcds = 8;   // XCDs of the chip, which deals workgroups round-robin
+constexpr int kSgMfma = 0x8, kSgDsRead = 0x100;   // sched_group_barrier instruction classes
 
 struct GemmRowsK {
   const ReqDev* reqs;
@@ -45,22 +49,48 @@ struct GemmRowsK {
   const uint16_t* x;
   const uint16_t* w;
   const uint16_t* res;
-  uint16_t* y;
-  int K, N, n_req, m_tiles, x_tok, y_tok;
+  uint16_t* y[kGemmMaxParts];   // output part p: columns pn[p] .. pn[p + 1] - 1, row stride pn[p + 1] - pn[p]
+  int pn[kGemmMaxParts + 1];
+  int n_parts, K, N, n_req, m_tiles, x_tok, y_tok;
 };
 
+// physical chunk of logical chunk c in tile row `row` (CH chunks per row): 16 consecutive rows
+// read at one logical chunk cover the 16 four-bank groups of a 256-byte LDS line
+template <int CH>
+__device__ __forceinline__ int chunk_swz(int c, int row) {
+  if constexpr (CH == 8) return c ^ ((row >> 1) & 7);   // 128-byte rows: two per line
+  else return c ^ ((row >> 2) & 3);                     // 64-byte rows: four per line
+}
+
+template <int BK, int NST, int GM>
 __global__ __launch_bounds__(512, 1) void gemm_rows_kernel(GemmRowsK a) {
   constexpr int NW = 8;
-  __shared__ __attribute__((aligned(1024))) char smem[2 * 2 * GTILE];   // [stage][W | X]
+  constexpr int ROWB = BK * 2;                 // bytes of one tile row
+  constexpr int CH = ROWB / 16;                // 16-byte chunks per row
+  constexpr int TILE = 256 * ROWB;             // bytes of one operand tile
+  constexpr int RPP = 1024 / ROWB;             // rows per 1 KB transfer
+  constexpr int PPW = 256 / RPP / NW;          // transfers per wave per operand tile
+  constexpr int NS = BK / 16;                  // 16-wide k slices per stage
+  __shared__ __attribute__((aligned(1024))) char smem[NST * 2 * TILE];   // [stage][W | X]
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wu = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int l32 = lane & 31;
   const int hg = lane >> 5;
-  // grid: row tile fastest (consecutive workgroups share a W panel), then feature tile
+  // tile order: groups of GM row tiles, the feature tile slowest within a group, so that a run of
+  // consecutive tile indices covers a few feature tiles x GM row tiles.  The hardware deals block b
+  // to XCD b mod 8; each XCD takes a contiguous run of tile indices, so the workgroups running
+  // together on one XCD read the same W and X k-slices through that XCD's L2.
   const int n_mt = a.n_req * a.m_tiles;
-  const int mt_all = (int)(blockIdx.x % (unsigned)n_mt);
-  const int nt = (int)(blockIdx.x / (unsigned)n_mt);
+  const int n_nt = a.N / GBN;
+  const unsigned per_xcd = gridDim.x / kGemmXcds;   // the grid is a multiple of kGemmXcds
+  const int L = (int)((blockIdx.x % kGemmXcds) * per_xcd + blockIdx.x / kGemmXcds);
+  if (L >= n_mt * n_nt) return;
+  const int grp = L / (GM * n_nt);
+  const int in_g = L - grp * GM * n_nt;
+  const int gm = min(GM, n_mt - grp * GM);
+  const int mt_all = grp * GM + in_g % gm;
+  const int nt = in_g / gm;
   const int r = mt_all / a.m_tiles;
   const int m0 = (mt_all - r * a.m_tiles) * GBM;
   const ReqDev rq = a.reqs[r];
@@ -69,15 +99,15 @@ __global__ __launch_bounds__(512, 1) void gemm_rows_kernel(GemmRowsK a) {
   const int n0 = nt * GBN;
   const int K = a.K;
 
-  // ---- transfers: piece q (1 KB) of a tile holds rows 8q .. 8q + 7; lane l fills row 8q + l / 8,
-  // physical chunk l % 8 with logical chunk (l % 8) ^ ((row / 2) mod 8).  A wave moves pieces
-  // wu + 8 i (i < 4) of both tiles. ----
-  const uint16_t* w_src[4];
-  const uint16_t* x_src[4];
+  // ---- transfers: piece q (1 KB) of a tile holds rows RPP q .. RPP q + RPP - 1; lane l fills row
+  // RPP q + l / CH, physical chunk l % CH with the logical chunk that chunk_swz maps there.  A wave
+  // moves pieces wu + 8 i (i < PPW) of both tiles. ----
+  const uint16_t* w_src[PPW];
+  const uint16_t* x_src[PPW];
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int row = 8 * (wu + NW * i) + lane / 8;
-    const int lc = (lane & 7) ^ ((row >> 1) & 7);
+  for (int i = 0; i < PPW; ++i) {
+    const int row = RPP * (wu + NW * i) + lane / CH;
+    const int lc = chunk_swz<CH>(lane % CH, row);   // (the swizzle is an involution)
     w_src[i] = a.w + (int64_t)(n0 + row) * K + lc * 8;
     const int m = min(m0 + row, nr - 1);   // rows past the request's last read a valid row
     x_src[i] = a.x + row_index(rq, a.rows, m, a.x_tok) * K + lc * 8;
@@ -87,24 +117,38 @@ __global__ __launch_bounds__(512, 1) void gemm_rows_kernel(GemmRowsK a) {
     const uint32_t m0r = __builtin_amdgcn_readfirstlane(lds);
     asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(src), "s"(m0r) : "m0", "memory");
   };
-  auto issue = [&](int t) {   // stage t into buffer t mod 2
-    const uint32_t base = smem_lds + (uint32_t)((t & 1) * 2 * GTILE);
-    const int k0 = t * GBK;
+  const int nk = K / BK;
+  auto issue = [&](int t) {   // stage t into buffer t mod NST
+    if (t >= nk) return;
+    const uint32_t base = smem_lds + (uint32_t)((t % NST) * 2 * TILE);
+    const int k0 = t * BK;
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
+    for (int i = 0; i < PPW; ++i) {
       dma16(w_src[i] + k0, base + (uint32_t)((wu + NW * i) * 1024));
-      dma16(x_src[i] + k0, base + (uint32_t)(GTILE + (wu + NW * i) * 1024));
+      dma16(x_src[i] + k0, base + (uint32_t)(TILE + (wu + NW * i) * 1024));
     }
   };
+  // wait until this wave's transfers of every stage before the n youngest have landed
+  auto wait_stages = [&](int n) {
+    switch (n * 2 * PPW) {
+      case 0: SX_WAIT_VMCNT(0); break;
+      case 2: SX_WAIT_VMCNT(2); break;
+      case 4: SX_WAIT_VMCNT(4); break;
+      case 6: SX_WAIT_VMCNT(6); break;
+      case 8: SX_WAIT_VMCNT(8); break;
+      case 10: SX_WAIT_VMCNT(10); break;
+      default: SX_WAIT_VMCNT(12); break;
+    }
+  };
+  static_assert((NST - 1) * 2 * PPW <= 12, "wait table");
+  static_assert(NS % 2 == 0, "a stage holds an even number of slices");
 
-  // ---- operand reads: row 32 j + l32 of a tile, logical chunk 2 s + hg at physical chunk
-  // (2 s + hg) ^ ((l32 / 2) mod 8): the lane part depends on s only, the tile row block adds a
-  // constant (an immediate offset) ----
+  // ---- operand reads: row 32 j + l32 of a tile, logical chunk 2 s + hg: the lane part depends on
+  // s only, the row block adds a constant (an immediate offset) ----
   const int wn = wu & 3, wm = wu >> 2;
-  uint32_t lane_off[GBK / 16];
+  uint32_t lane_off[NS];
 #pragma unroll
-  for (int s = 0; s < GBK / 16; ++s)
-    lane_off[s] = (uint32_t)(l32 * 128 + ((((2 * s + hg) ^ ((l32 >> 1) & 7))) << 4));
+  for (int s = 0; s < NS; ++s) lane_off[s] = (uint32_t)(l32 * ROWB + (chunk_swz<CH>(2 * s + hg, l32) << 4));
   f32x16_t acc[2][4];
 #pragma unroll
   for (int i = 0; i < 2; ++i)
@@ -113,60 +157,99 @@ __global__ __launch_bounds__(512, 1) void gemm_rows_kernel(GemmRowsK a) {
 #pragma unroll
       for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
 
-  const int nk = K / GBK;
+  // fragments of one 16-wide k slice, read from stage buffer `buf`: one base register per matrix
+  // (the empty asm keeps the sums from being re-associated into one register per read), the row
+  // blocks as immediate offsets
+  auto read_slice = [&](int buf, int s, bf16x8_t (&fw)[2], bf16x8_t (&fx)[4]) {
+    const uint32_t sb = smem_lds + (uint32_t)(buf * 2 * TILE);
+    uint32_t wb = sb + lane_off[s] + (uint32_t)(wn * 64 * ROWB);
+    uint32_t xb = sb + (uint32_t)TILE + lane_off[s] + (uint32_t)(wm * 128 * ROWB);
+    asm volatile("" : "+v"(wb), "+v"(xb));
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+      fw[i] = *(const __attribute__((address_space(3))) bf16x8_t*)(uintptr_t)(wb + (uint32_t)(i * 32 * ROWB));
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+      fx[j] = *(const __attribute__((address_space(3))) bf16x8_t*)(uintptr_t)(xb + (uint32_t)(j * 32 * ROWB));
+  };
+
+  // Software pipeline: the fragments of slice s + 1 are read while the MFMAs of slice s run (two
+  // register sets).  The stage barrier sits before the MFMAs of a stage's last slice: past it every
+  // wave has finished reading the stage (its buffer takes stage t + NST) and stage t + 1 has landed
+  // (its first slice is read during those MFMAs).
   // the row indices above are compiler-visible loads: complete before the first transfer wait
   SX_WAIT_VMCNT(0);
-  issue(0);
-  SX_WAIT_VMCNT(0);
+#pragma unroll
+  for (int t = 0; t < NST; ++t) issue(t);
+  wait_stages(min(NST - 1, nk - 1));   // stage 0 has landed
   __syncthreads();
-  for (int t = 0; t < nk; ++t) {
-    if (t + 1 < nk) issue(t + 1);
-    // stage t: per 16-wide k slice s, 2 W slices (features) x 4 X slices (rows) -> 8 MFMAs.  One
-    // base register per slice s and matrix (the empty asm keeps the sums from being re-associated
-    // into one precomputed register per read)
-    const uint32_t sb = smem_lds + (uint32_t)((t & 1) * 2 * GTILE);
-    uint32_t wb[GBK / 16], xb[GBK / 16];
+  bf16x8_t fw[2][2], fx[2][4];
+  auto mfma_slice = [&](int c) {
 #pragma unroll
-    for (int s = 0; s < GBK / 16; ++s) {
-      wb[s] = sb + lane_off[s] + (uint32_t)(wn * 64 * 128);
-      xb[s] = sb + (uint32_t)GTILE + lane_off[s] + (uint32_t)(wm * 128 * 128);
-      asm volatile("" : "+v"(wb[s]), "+v"(xb[s]));
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fw[c][i], fx[c][j], acc[i][j], 0, 0, 0);
+  };
+  // the scheduler would sink the reads below the MFMAs (to reuse their registers): pin one read
+  // after each of the first six MFMAs
+  auto interleave = [&]() {
+#pragma unroll
+    for (int q = 0; q < 6; ++q) {
+      __builtin_amdgcn_sched_group_barrier(kSgMfma, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(kSgDsRead, 1, 0);
     }
+    __builtin_amdgcn_sched_group_barrier(kSgMfma, 2, 0);
+  };
+  read_slice(0, 0, fw[0], fx[0]);
+  for (int t = 0; t + 1 < nk; ++t) {
 #pragma unroll
-    for (int s = 0; s < GBK / 16; ++s) {
-      bf16x8_t fw[2], fx[4];
-#pragma unroll
-      for (int i = 0; i < 2; ++i)
-        fw[i] = *(const __attribute__((address_space(3))) bf16x8_t*)(uintptr_t)(wb[s] + (uint32_t)(i * 32 * 128));
-#pragma unroll
-      for (int j = 0; j < 4; ++j)
-        fx[j] = *(const __attribute__((address_space(3))) bf16x8_t*)(uintptr_t)(xb[s] + (uint32_t)(j * 32 * 128));
-#pragma unroll
-      for (int i = 0; i < 2; ++i)
-#pragma unroll
-        for (int j = 0; j < 4; ++j) acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fw[i], fx[j], acc[i][j], 0, 0, 0);
+    for (int s = 0; s + 1 < NS; ++s) {   // NS is even: a stage starts on set 0
+      read_slice(t % NST, s + 1, fw[(s + 1) & 1], fx[(s + 1) & 1]);
+      mfma_slice(s & 1);
+      interleave();
     }
-    SX_WAIT_VMCNT(0);   // this wave's transfers of stage t + 1 have landed
+    // this wave's reads of stage t are done (the barrier alone does not wait for them) and its
+    // transfers of stage t + 1 have landed (the younger ones may be in flight)
+    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+    wait_stages(max(0, min(NST - 2, nk - 2 - t)));
     __syncthreads();
+    issue(t + NST);   // into the buffer of stage t
+    read_slice((t + 1) % NST, 0, fw[0], fx[0]);
+    mfma_slice(1);
+    interleave();
   }
+  // last stage
+#pragma unroll
+  for (int s = 0; s + 1 < NS; ++s) {
+    read_slice((nk - 1) % NST, s + 1, fw[(s + 1) & 1], fx[(s + 1) & 1]);
+    mfma_slice(s & 1);
+    interleave();
+  }
+  mfma_slice(1);
 
   // ---- epilogue: lane owns row 32 j + l32 of the wave's rows; value e of accumulator (i, j) is
-  // feature 32 i + 8 (e / 4) + 4 hg + e % 4 of the wave's features ----
+  // feature 32 i + 8 (e / 4) + 4 hg + e % 4 of the wave's features.  Part boundaries are multiples
+  // of the tile width, so the output part is the tile's. ----
+  int part = 0;
+  while (part + 1 < a.n_parts && n0 >= a.pn[part + 1]) ++part;
+  uint16_t* const yp = a.y[part];
+  const int ld = a.pn[part + 1] - a.pn[part];
+  const int c0 = n0 - a.pn[part] + wn * 64 + 4 * hg;
 #pragma unroll
   for (int j = 0; j < 4; ++j) {
     const int m = m0 + wm * 128 + 32 * j + l32;
     if (m >= nr) continue;
-    const int64_t yr = row_index(rq, a.rows, m, a.y_tok);
+    const int64_t yr = row_index(rq, a.rows, m, a.y_tok) * ld;
 #pragma unroll
     for (int i = 0; i < 2; ++i)
 #pragma unroll
       for (int g = 0; g < 4; ++g) {
-        const int n = n0 + wn * 64 + 32 * i + 8 * g + 4 * hg;
+        const int c = c0 + 32 * i + 8 * g;
         float v[4];
 #pragma unroll
         for (int e = 0; e < 4; ++e) v[e] = acc[i][j][4 * g + e];
         if (a.res) {
-          const uint2 rv = *(const uint2*)(a.res + yr * a.N + n);
+          const uint2 rv = *(const uint2*)(a.res + yr + c);
           v[0] += bf16_lo(rv.x);
           v[1] += bf16_hi(rv.x);
           v[2] += bf16_lo(rv.y);
@@ -175,10 +258,18 @@ __global__ __launch_bounds__(512, 1) void gemm_rows_kernel(GemmRowsK a) {
         uint2 o;
         o.x = pack_bf16x2(v[0], v[1]);
         o.y = pack_bf16x2(v[2], v[3]);
-        *(uint2*)(a.y + yr * a.N + n) = o;
+        *(uint2*)(yp + yr + c) = o;
       }
   }
 }
+
+#ifndef SX_GEMM_BK
+#define SX_GEMM_BK 64
+#define SX_GEMM_NST 2
+#endif
+#ifndef SX_GEMM_GM
+#define SX_GEMM_GM 8
+#endif
 
 // ---------------------------------------------------------------------------------------------
 // RMSNorm of listed rows: one wave per row, float32 sum of squares in a fixed order.
@@ -313,8 +404,9 @@ __global__ __launch_bounds__(256) void silu_mul_rows_kernel(const ReqDev* __rest
 
 }  // namespace
 
-hipError_t launch_gemm_rows(const sx_plan* p, const RowsArg& r, const void* x, int x_tok, const void* w, int k, int n,
-                            const void* res, void* y, int y_tok, hipStream_t s) {
+hipError_t launch_gemm_rows(const sx_plan* p, const RowsArg& r, const void* x, int x_tok, const void* w, int k,
+                            int n_parts, const int* part_n, void* const* ys, const void* res, int y_tok, hipStream_t s) {
+  if (n_parts < 1 || n_parts > kGemmMaxParts) return hipErrorInvalidValue;
   GemmRowsK a{};
   a.reqs = p->d_req;
   a.rows = r.rows;
@@ -322,15 +414,24 @@ hipError_t launch_gemm_rows(const sx_plan* p, const RowsArg& r, const void* x, i
   a.x = (const uint16_t*)x;
   a.w = (const uint16_t*)w;
   a.res = (const uint16_t*)res;
-  a.y = (uint16_t*)y;
+  a.n_parts = n_parts;
+  int n = 0;
+  for (int i = 0; i < n_parts; ++i) {
+    a.y[i] = (uint16_t*)ys[i];
+    a.pn[i] = n;
+    n += part_n[i];
+  }
+  a.pn[n_parts] = n;
   a.K = k;
   a.N = n;
   a.n_req = p->n_req;
   a.m_tiles = (r.max_rows + GBM - 1) / GBM;
+  constexpr int BK = SX_GEMM_BK, NST = SX_GEMM_NST, GM = SX_GEMM_GM;
   a.x_tok = x_tok;
   a.y_tok = y_tok;
-  const int64_t blocks = (int64_t)a.m_tiles * p->n_req * (n / GBN);
-  hipLaunchKernelGGL(gemm_rows_kernel, dim3((unsigned)blocks), dim3(512), 0, s, a);
+  const int64_t tiles = (int64_t)a.m_tiles * p->n_req * (n / GBN);
+  const int64_t blocks = (tiles + kGemmXcds - 1) / kGemmXcds * kGemmXcds;
+  hipLaunchKernelGGL((gemm_rows_kernel<BK, NST, GM>), dim3((unsigned)blocks), dim3(512), 0, s, a);
   return hipGetLastError();
 }
 

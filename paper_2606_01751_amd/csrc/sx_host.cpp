@@ -466,9 +466,34 @@ sx_status sx_gemm_rows(const sx_plan* p, const int32_t* rows, const int32_t* n_r
     return fail(SX_EUNSUPPORTED, "sx_gemm_rows needs k a multiple of 64 and n a multiple of 256 (k=%d n=%d)", k, n);
   if (max_rows == 0) return SX_OK;
   const sx::RowsArg r{rows, n_rows, max_rows};
-  return check_launch(sx::launch_gemm_rows(p, r, x, x_by_token != 0, w, k, n, residual, y, y_by_token != 0,
+  const int part_n[1] = {n};
+  void* const ys[1] = {y};
+  return check_launch(sx::launch_gemm_rows(p, r, x, x_by_token != 0, w, k, 1, part_n, ys, residual, y_by_token != 0,
                                            (hipStream_t)stream),
                       "sx_gemm_rows launch");
+}
+
+sx_status sx_gemm_rows_split(const sx_plan* p, const int32_t* rows, const int32_t* n_rows, int32_t max_rows,
+                             const void* x, int32_t x_by_token, const void* w, int32_t k, int32_t n_parts,
+                             const int32_t* part_n, void* const* y_parts, int32_t y_by_token, void* stream) {
+  sx_status st = check_rows(p, rows, n_rows, max_rows, x_by_token || y_by_token);
+  if (st != SX_OK) return st;
+  if (!x || !w || !part_n || !y_parts) return fail(SX_EINVAL, "NULL argument");
+  if (n_parts < 1 || n_parts > 4) return fail(SX_EINVAL, "n_parts %d outside 1..4", n_parts);
+  if (k <= 0 || k % 64 != 0) return fail(SX_EUNSUPPORTED, "sx_gemm_rows_split needs k a multiple of 64 (k=%d)", k);
+  int64_t n = 0;
+  for (int i = 0; i < n_parts; ++i) {
+    if (!y_parts[i]) return fail(SX_EINVAL, "output part %d is NULL", i);
+    if (part_n[i] <= 0 || part_n[i] % 256 != 0)
+      return fail(SX_EUNSUPPORTED, "part %d width %d is not a positive multiple of 256", i, part_n[i]);
+    n += part_n[i];
+  }
+  if (n > INT32_MAX) return fail(SX_EINVAL, "total width %lld too large", (long long)n);
+  if (max_rows == 0) return SX_OK;
+  const sx::RowsArg r{rows, n_rows, max_rows};
+  return check_launch(sx::launch_gemm_rows(p, r, x, x_by_token != 0, w, k, n_parts, part_n, y_parts, nullptr,
+                                           y_by_token != 0, (hipStream_t)stream),
+                      "sx_gemm_rows_split launch");
 }
 
 sx_status sx_rmsnorm_rows(const sx_plan* p, const int32_t* rows, const int32_t* n_rows, int32_t max_rows,

@@ -108,8 +108,11 @@ struct RowsArg {
   const int32_t* n_rows;
   int32_t max_rows;
 };
-hipError_t launch_gemm_rows(const sx_plan* p, const RowsArg& r, const void* x, int x_tok, const void* w, int k, int n,
-                            const void* res, void* y, int y_tok, hipStream_t s);
+// y = x w^T on the listed rows; w is [sum part_n][k], output part i (columns of w's rows
+// sum_{j<i} part_n[j] ..) goes to ys[i] with row stride part_n[i]; 1 <= n_parts <= 4, residual
+// (nullable) addressed like part 0
+hipError_t launch_gemm_rows(const sx_plan* p, const RowsArg& r, const void* x, int x_tok, const void* w, int k,
+                            int n_parts, const int* part_n, void* const* ys, const void* res, int y_tok, hipStream_t s);
 hipError_t launch_rmsnorm_rows(const sx_plan* p, const RowsArg& r, const void* x, int x_tok, const void* gamma,
                                float eps, int h, void* y, int y_tok, hipStream_t s);
 hipError_t launch_rope_rows(const sx_plan* p, const RowsArg& r, void* q, void* k, hipStream_t s);

@@ -82,7 +82,8 @@ def test_gemm_rows_matches_oracle(x_tok, y_tok, with_res):
 
 
 def test_gemm_rows_full_tiles_and_k_tail_shapes():
-    """Row counts that end exactly on and just past a 256-row tile, k = 64 (one stage), n = 256."""
+    """Row counts that end exactly on and just past a 256-row tile; k = 64 (one stage), 128 (two)
+    and 1024; n = 256 (one feature tile) and 768."""
     specs = [[(512, False, 0, None)], [(257, False, 0, None)]]
     w = W.custom_workload(specs, n_q_heads=8, n_kv_heads=2, head_dim=128, dtype="bf16", rope_base=5e5, seed=3,
                           name="gemm-edges")
@@ -90,7 +91,7 @@ def test_gemm_rows_full_tiles_and_k_tail_shapes():
     per = [np.arange(512), np.arange(257)]
     rows = torch.from_numpy(np.concatenate([per[0], per[1]]).astype(np.int32)).cuda()
     n_rows = torch.tensor([512, 257], dtype=torch.int32, device="cuda")
-    for K, N in ((64, 256), (1024, 768)):
+    for K, N in ((64, 256), (128, 512), (1024, 768)):
         x = _bf16(rng, (w.total_tokens, K))
         wt = _bf16(rng, (N, K), 1 / math.sqrt(K))
         plan = sx.Plan(desc_of(w), w.requests, w.n_dst_blocks, w.n_src_blocks)
@@ -101,6 +102,54 @@ def test_gemm_rows_full_tiles_and_k_tail_shapes():
         mag = np.abs(x).astype(np.float64) @ np.abs(wt).astype(np.float64).T
         assert np.all(np.abs(host(y) - ref) <= BF16_ULP * np.abs(ref) + 1e-5 * mag + 1e-6), (K, N)
         plan.close()
+
+
+@pytest.mark.parametrize("x_tok,y_tok", [(True, True), (False, False)])
+def test_gemm_rows_split_matches_oracle(x_tok, y_tok):
+    """Stacked query / key / value weights in one launch: each output part equals the product with
+    its own block of rows of the weight."""
+    log(f"[gemm_rows_split] x_tok={x_tok} y_tok={y_tok}")
+    w = _ragged_workload()
+    rng = np.random.default_rng(14)
+    per, rows, n_rows, m = _rows(w, rng, 0.5)
+    K, widths, tot = 256, (512, 256, 256), w.total_tokens
+    x = _bf16(rng, (tot, K))
+    wt = _bf16(rng, (sum(widths), K), 1 / math.sqrt(K))
+    plan = sx.Plan(desc_of(w), w.requests, w.n_dst_blocks, w.n_src_blocks)
+    ys = [torch.full((tot, n), CANARY, dtype=torch.bfloat16, device="cuda") for n in widths]
+    sx.gemm_rows_split(plan, rows, n_rows, m, dev(x, w), dev(wt, w), ys, x_by_token=x_tok, y_by_token=y_tok)
+    torch.cuda.synchronize()
+    start = 0
+    for n, y in zip(widths, ys):
+        got = host(y)
+        wp = wt[start:start + n]
+        touched = np.zeros(tot, bool)
+        for r in range(len(w.requests)):
+            xi, yi = _index(w, per, r, x_tok), _index(w, per, r, y_tok)
+            ref = O.linear(x[xi], wp)
+            mag = np.abs(x[xi]).astype(np.float64) @ np.abs(wp).astype(np.float64).T
+            err = np.abs(got[yi] - ref)
+            assert np.all(err <= BF16_ULP * np.abs(ref) + 1e-5 * mag + 1e-6), f"part at {start}, request {r}"
+            touched[yi] = True
+        assert np.all(got[~touched] == CANARY), "rows that are not listed were written"
+        start += n
+    plan.close()
+
+
+def test_gemm_rows_split_rejects_bad_parts():
+    w = _ragged_workload()
+    plan = sx.Plan(desc_of(w), w.requests, w.n_dst_blocks, w.n_src_blocks)
+    rows = torch.zeros(w.total_tokens, dtype=torch.int32, device="cuda")
+    n_rows = torch.zeros(3, dtype=torch.int32, device="cuda")
+    x = torch.zeros((w.total_tokens, 128), dtype=torch.bfloat16, device="cuda")
+    wt = torch.zeros((384, 128), dtype=torch.bfloat16, device="cuda")
+    ys = [torch.zeros((w.total_tokens, n), dtype=torch.bfloat16, device="cuda") for n in (256, 128)]
+    with pytest.raises(sx.SxError) as e:
+        sx.gemm_rows_split(plan, rows, n_rows, 10, x, wt, ys)   # a part 128 wide
+    assert e.value.status == sx.SX_EUNSUPPORTED
+    with pytest.raises(ValueError):
+        sx.gemm_rows_split(plan, rows, n_rows, 10, x, wt[:256], ys)   # widths add up to 384, w has 256 rows
+    plan.close()
 
 
 def test_gemm_rows_rejects_unsupported_shapes():
@@ -207,9 +256,9 @@ def run_layer_body(plan, w, rows, n_rows, max_rows, hidden, wd, src_k, src_v, kc
     Hq, Hkv, d = w.n_q_heads, w.n_kv_heads, w.head_dim
     b = bufs
     sx.rmsnorm_rows(plan, rows, n_rows, max_rows, hidden, wd["ln1"], eps, b["x1"], x_by_token=True)
-    sx.gemm_rows(plan, rows, n_rows, max_rows, b["x1"], wd["wq"], b["q"], y_by_token=True)
-    sx.gemm_rows(plan, rows, n_rows, max_rows, b["x1"], wd["wk"], b["k"], y_by_token=True)
-    sx.gemm_rows(plan, rows, n_rows, max_rows, b["x1"], wd["wv"], b["v"], y_by_token=True)
+    # the query, key and value projections in one launch (wd["wqkv"] stacks wq, wk, wv)
+    sx.gemm_rows_split(plan, rows, n_rows, max_rows, b["x1"], wd["wqkv"], [b["q"], b["k"], b["v"]],
+                       y_by_token=True)
     sx.rope_rows(plan, rows, n_rows, max_rows, b["q"], b["k"])
     sx.rows_mask(plan, rows, n_rows, max_rows, b["mask"])
     sx.realign_scatter_masked(plan, src_k, src_v, b["k"], b["v"], b["mask"], kc, vc)
@@ -253,6 +302,7 @@ def test_layer_body_matches_oracle():
     rows[:len(R)] = torch.from_numpy(R.astype(np.int32)).cuda()
     n_rows = torch.tensor([len(R)], dtype=torch.int32, device="cuda")
     wd = {kk: dev(v, w) for kk, v in wts.items()}
+    wd["wqkv"] = dev(np.concatenate([wts["wq"], wts["wk"], wts["wv"]]), w)
     shape = (w.n_dst_blocks, Hkv, w.block_size, d)
     kc = torch.full(shape, CANARY, dtype=torch.bfloat16, device="cuda")
     vc = torch.full(shape, CANARY, dtype=torch.bfloat16, device="cuda")
