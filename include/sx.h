@@ -66,7 +66,8 @@ enum {
   SX_ESHAPE = -2,        /* inconsistent sizes (heads, block ids out of range, ...) */
   SX_EUNSUPPORTED = -3,  /* valid but not implemented (head_dim, block_size, dtype) */
   SX_EHIP = -4,          /* a HIP runtime call failed */
-  SX_ENOMEM = -6         /* device allocation failed */
+  SX_ENOMEM = -6,        /* device allocation failed */
+  SX_EFULL = -7          /* the block pool cannot hold the request (sx_cache_schedule) */
 };
 
 enum { SX_F32 = 0, SX_BF16 = 1 };

@@ -255,6 +255,10 @@ class BlockCache:
         if r.committed:
             raise ValueError("request already committed")
         b = self.block_size
+        publish = [(int(s), int(n), bytes(e), bool(f)) for s, n, e, f in publish]
+        for s, n, _, _ in publish:
+            if s < 0 or n <= 0 or s % b or n % b or s + n > len(r.tokens):
+                raise ValueError("published spans must be block aligned and inside the request")
         for blk in r.src_blocks:
             self._put(blk)
         r.src_blocks = []
@@ -268,9 +272,6 @@ class BlockCache:
                 self.prefix_of[blk] = h
             parent = h
         for s, n, e, freeze in publish:
-            s, n, e = int(s), int(n), bytes(e)
-            if s < 0 or n <= 0 or s % b or n % b or s + n > len(r.tokens):
-                raise ValueError("published spans must be block aligned and inside the request")
             for i in range(s // b, (s + n) // b):
                 blk = r.block_table[i]
                 vh = virtual_hash(r.tokens[i * b:(i + 1) * b], e)
@@ -300,6 +301,8 @@ class BlockCache:
                 self.frozen[blk] = True
 
     def frozen_delete(self, blocks) -> None:
+        if len(set(blocks)) != len(blocks):
+            raise ValueError("a block is listed twice")
         for blk in blocks:
             if not self.frozen[blk]:
                 raise ValueError(f"block {blk} is not frozen")

@@ -24,6 +24,17 @@ sx_status fail(sx_status st, const char* fmt, ...) {
 
 sx_status ok() { return SX_OK; }
 
+}  // namespace
+
+namespace sx {
+sx_status report(sx_status st, const char* msg) {
+  g_err = msg;
+  return st;
+}
+}  // namespace sx
+
+namespace {
+
 sx_status hip_fail(hipError_t e, const char* what) {
   return fail(SX_EHIP, "%s: %s", what, hipGetErrorString(e));
 }

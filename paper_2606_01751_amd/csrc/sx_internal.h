@@ -103,6 +103,10 @@ hipError_t launch_topk(const sx_plan* p, const float* scores, double ratio, int3
 // Row-sparse layer body (defined in k_layer.hip).  Rows are the listed rows of every request in
 // the row-list layout; an operand row is addressed by slot (off_r + n) or by token
 // (off_r + rows[off_r + n]).
+// Sets the thread-local error message read by sx_last_error and returns st (for host-only
+// translation units without the dispatcher's helpers).
+sx_status report(sx_status st, const char* msg);
+
 struct RowsArg {
   const int32_t* rows;
   const int32_t* n_rows;
