@@ -13,6 +13,8 @@ from __future__ import annotations
 import ctypes
 from dataclasses import dataclass
 
+import numpy as np
+
 from . import SxError, lib as _lib
 
 EXPORTED = (
@@ -94,8 +96,17 @@ def _check(st: int) -> None:
 
 
 def _ints(xs):
-    xs = [int(x) for x in xs]
-    return (I32 * max(len(xs), 1))(*xs), len(xs)
+    """(pointer, count) of an int32 copy of xs; the pointer keeps the copy alive."""
+    a = np.ascontiguousarray(np.asarray(xs, dtype=np.int64).astype(np.int32) if not isinstance(xs, np.ndarray)
+                             or xs.dtype != np.int32 else xs)
+    if a.size == 0:
+        a = np.zeros(1, np.int32)
+        n = 0
+    else:
+        n = int(a.size)
+    ptr = a.ctypes.data_as(ctypes.POINTER(I32))
+    ptr._keep = a
+    return ptr, n
 
 
 def _bytes(b: bytes):

@@ -135,6 +135,8 @@ struct Sha256 {
   void update(const void* data, size_t n) {
     const uint8_t* p = (const uint8_t*)data;
     len += n;
+    if (fill == 0)
+      for (; n >= 64; n -= 64, p += 64) block(p);
     while (n > 0) {
       const size_t take = std::min(n, (size_t)(64 - fill));
       std::memcpy(buf + fill, p, take);
@@ -146,21 +148,6 @@ struct Sha256 {
         fill = 0;
       }
     }
-  }
-
-  void u32(uint32_t v) {
-    const uint8_t b[4] = {(uint8_t)v, (uint8_t)(v >> 8), (uint8_t)(v >> 16), (uint8_t)(v >> 24)};
-    update(b, 4);
-  }
-
-  void tokens(const int32_t* t, int32_t n) {
-    u32((uint32_t)n);
-    for (int32_t i = 0; i < n; ++i) u32((uint32_t)t[i]);
-  }
-
-  void key(const uint8_t* k, int32_t n) {
-    u32((uint32_t)n);
-    if (n > 0) update(k, (size_t)n);
   }
 
   void final(uint8_t* out) {
@@ -190,28 +177,44 @@ struct DigestHash {
   }
 };
 
-Digest virtual_hash(const int32_t* t, int32_t n, const uint8_t* key, int32_t key_len) {
+// The encoded message of a block hash: tag [| parent] | u32 n | n little-endian int32 | u32 key
+// length | key, assembled in one buffer and hashed with one update.
+Digest block_hash(uint8_t tag, const uint8_t* parent, const int32_t* t, int32_t n, const uint8_t* key,
+                  int32_t key_len) {
+  static const uint8_t zero[32] = {};
+  thread_local std::vector<uint8_t> msg;
+  const size_t len = 1 + (tag == 'P' ? 32 : 0) + 4 + 4 * (size_t)n + 4 + (size_t)key_len;
+  if (msg.size() < len) msg.resize(len);
+  uint8_t* p = msg.data();
+  auto put32 = [&](uint32_t v) {
+    p[0] = (uint8_t)v;
+    p[1] = (uint8_t)(v >> 8);
+    p[2] = (uint8_t)(v >> 16);
+    p[3] = (uint8_t)(v >> 24);
+    p += 4;
+  };
+  *p++ = tag;
+  if (tag == 'P') {
+    std::memcpy(p, parent ? parent : zero, 32);
+    p += 32;
+  }
+  put32((uint32_t)n);
+  for (int32_t i = 0; i < n; ++i) put32((uint32_t)t[i]);
+  put32((uint32_t)key_len);
+  if (key_len > 0) std::memcpy(p, key, (size_t)key_len);
   Sha256 s;
-  const uint8_t tag = 'V';
-  s.update(&tag, 1);
-  s.tokens(t, n);
-  s.key(key, key_len);
+  s.update(msg.data(), len);
   Digest d;
   s.final(d.data());
   return d;
 }
 
+Digest virtual_hash(const int32_t* t, int32_t n, const uint8_t* key, int32_t key_len) {
+  return block_hash('V', nullptr, t, n, key, key_len);
+}
+
 Digest prefix_hash(const uint8_t* parent, const int32_t* t, int32_t n, const uint8_t* key, int32_t key_len) {
-  static const uint8_t zero[32] = {};
-  Sha256 s;
-  const uint8_t tag = 'P';
-  s.update(&tag, 1);
-  s.update(parent ? parent : zero, 32);
-  s.tokens(t, n);
-  s.key(key, key_len);
-  Digest d;
-  s.final(d.data());
-  return d;
+  return block_hash('P', parent, t, n, key, key_len);
 }
 
 }  // namespace
