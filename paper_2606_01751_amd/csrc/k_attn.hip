@@ -256,6 +256,11 @@ __global__ __launch_bounds__(512, 1) void attn_mfma_kernel(AttnK a) {
   };
   auto ktile = [&](int t) { return kbuf + (t % NBUF) * TILEB; };
   auto vtile = [&](int t) { return vbuf + (t % NBUF) * TILEB; };
+  // the same buffers as LDS byte addresses (wave-uniform: the operand reads add a lane offset)
+  const uint32_t kbuf_lds = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) char*)kbuf;
+  const uint32_t vbuf_lds = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) char*)vbuf;
+  auto ktile_lds = [&](int t) { return kbuf_lds + (uint32_t)((t % NBUF) * TILEB); };
+  auto vtile_lds = [&](int t) { return vbuf_lds + (uint32_t)((t % NBUF) * TILEB); };
   // wait until at most n of this wave's tile transfers (the youngest) are still in flight
   auto wait_vm = [&](int n) {
     switch (n) {
@@ -272,23 +277,30 @@ __global__ __launch_bounds__(512, 1) void attn_mfma_kernel(AttnK a) {
   // ---- tile computations ----
   // S^T = K Q^T for the 64 keys of a tile (two 32-key M tiles)
   f32x16_t sacc[2];
-  auto s_body = [&](const char* Kb) {
+  // K operand addressing: lane reads row 32 mt + l32, logical chunk 2 s + hg.  The swizzle depends
+  // on the row only through l32 mod NCH, so the lane part of the address is one value per k-slice
+  // s (computed once) and the second row block adds a constant (an immediate offset).
+  int k_off[D / 16];
+#pragma unroll
+  for (int s = 0; s < D / 16; ++s) k_off[s] = l32 * ROWB + (((2 * s + hg) ^ (l32 & (NCH - 1))) << 4);
+  auto s_body = [&](uint32_t Kb) {
+    asm volatile("" : "+s"(Kb));   // opaque: one add per k-slice, no strength-reduced variants
 #pragma unroll
     for (int mt = 0; mt < 2; ++mt)
 #pragma unroll
       for (int e = 0; e < 16; ++e) sacc[mt][e] = 0.f;
 #pragma unroll
     for (int s = 0; s < D / 16; ++s) {
+      uint32_t kbase = Kb + (uint32_t)k_off[s];
+      asm volatile("" : "+v"(kbase));
 #pragma unroll
       for (int mt = 0; mt < 2; ++mt) {
-        const int rr = mt * 32 + l32;
-        const int c = 2 * s + hg;
-        const bf16x8_t ka = *(const bf16x8_t*)(Kb + rr * ROWB + ((c ^ (rr & (NCH - 1))) << 4));
+        const bf16x8_t ka = *(const __attribute__((address_space(3))) bf16x8_t*)(uintptr_t)(kbase + (uint32_t)(mt * 32 * ROWB));
         sacc[mt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka, qb[s], sacc[mt], 0, 0, 0);
       }
     }
   };
-  auto s_tile = [&](const char* Kb) {
+  auto s_tile = [&](uint32_t Kb) {
     s_body(Kb);
     sched_pipelined<D / 8, 1, 4>();
   };
@@ -379,15 +391,16 @@ __global__ __launch_bounds__(512, 1) void attn_mfma_kernel(AttnK a) {
     const int dchunk = 4 * dt + 2 * (tg & 1) + (tc >> 1);
     vtr_off[dt] = (4 * (tg >> 1) + tk) * ROWB + ((dchunk ^ v_swz<NCH>(tk)) << 4) + (tc & 1) * 8;
   }
-  auto pv_body = [&](const char* Vb) {
+  auto pv_body = [&](uint32_t Vb) {
     if constexpr (PV) {
+      asm volatile("" : "+s"(Vb));
       // one base address per 32-dim tile for this tile's buffer (the empty asm keeps the compiler
       // from re-associating the sums into one precomputed register per read); every read then
       // adds its row constant as an immediate offset
       uint32_t vbase[D / 32];
 #pragma unroll
       for (int dt = 0; dt < D / 32; ++dt) {
-        vbase[dt] = (uint32_t)(uintptr_t)(lds_shortx4_t*)(Vb) + (uint32_t)vtr_off[dt];
+        vbase[dt] = Vb + (uint32_t)vtr_off[dt];
         asm volatile("" : "+v"(vbase[dt]));
       }
 #pragma unroll
@@ -408,7 +421,7 @@ __global__ __launch_bounds__(512, 1) void attn_mfma_kernel(AttnK a) {
         }
     }
   };
-  auto pv_tile = [&](const char* Vb) {
+  auto pv_tile = [&](uint32_t Vb) {
     if constexpr (PV) {
       pv_body(Vb);
       sched_pipelined<D / 8, 2, 4>();
@@ -437,8 +450,8 @@ __global__ __launch_bounds__(512, 1) void attn_mfma_kernel(AttnK a) {
     // the wave in its matrix phase issues first: its MFMAs are not held back by the other
     // wave's softmax on the same SIMD
     __builtin_amdgcn_s_setprio(2);
-    if (j >= 1 && (j - 1) * KT <= wave_max) pv_tile(vtile(j - 1));
-    if (j < nkt && j * KT <= wave_max) s_tile(ktile(j));
+    if (j >= 1 && (j - 1) * KT <= wave_max) pv_tile(vtile_lds(j - 1));
+    if (j < nkt && j * KT <= wave_max) s_tile(ktile_lds(j));
     __builtin_amdgcn_s_setprio(0);
   };
   auto transfer_phase = [&](int j) {   // this wave's share of K(j+2) and V(j+1)
