@@ -2,7 +2,7 @@
 // feed-forward module evaluated on the rows of the recompute set R only.
 //
 //   gemm_rows_kernel     Y[row] = X[row] W^T (+ residual[row]): bfloat16 operands, float32
-//                        accumulation on v_mfma_f32_32x32x16_bf16, W stored [n][k] (k contiguous,
+//                        accumulation on v_mfma_f32_16x16x32_bf16, W stored [n][k] (k contiguous,
 //                        the layout of a linear layer's weight)
 //   rmsnorm_rows_kernel  Y[row] = X[row] / sqrt(mean(X[row]^2) + eps) * gamma
 //   rope_rows_kernel     RoPE of fresh query / key rows at their positions in the new sequence
@@ -21,21 +21,26 @@ typedef float f32x2_t __attribute__((ext_vector_type(2)));
 
 // s_waitcnt with vmcnt <= n (n < 16), expcnt and lgkmcnt left unconstrained (gfx9 encoding).
 #define SX_WAIT_VMCNT(n) __builtin_amdgcn_s_waitcnt(((n) & 0xF) | (0x7 << 4) | (0xF << 8))
+// the same for n < 64 (the counter's two high bits sit at 15:14)
+#define SX_WAIT_VMCNT6(n) \
+  __builtin_amdgcn_s_waitcnt(((n) & 0xF) | ((((n) >> 4) & 3) << 14) | (0x7 << 4) | (0xF << 8))
 
 __device__ __forceinline__ int64_t row_index(const ReqDev& rq, const int32_t* rows, int n, bool by_token) {
   return by_token ? (int64_t)rq.tok_off + rows[rq.tok_off + n] : (int64_t)rq.tok_off + n;
 }
 
 // ---------------------------------------------------------------------------------------------
-// GEMM on listed rows.  Computed transposed, Y^T = W X^T: the MFMA A operand is a 32 x 16 slice of
-// W (32 output features), the B operand a 16 x 32 slice of X^T (32 rows), so each lane owns one
-// row of the result and writes 4 consecutive features per store.
+// GEMM on listed rows.  Computed transposed, Y^T = W X^T: the MFMA A operand is a slice of W (MF
+// output features), the B operand a slice of X^T (MF rows), so each lane owns one row of the
+// result and writes 4 consecutive features per store.
 // Workgroup tile: 256 features x 256 rows; 8 waves as 4 (features) x 2 (rows), a wave owns 64
-// features x 128 rows (2 x 4 accumulators of 32 x 32).  The k dimension moves in stages of BK
+// features x 128 rows.  The default MFMA is v_mfma_f32_16x16x32_bf16 (4 x 8 accumulators of
+// 16 x 16): measured 1-12 % faster than v_mfma_f32_32x32x16_bf16 (MF = 32, 2 x 4 accumulators)
+// on the same tiles, most on the narrow products.  The k dimension moves in stages of BK
 // through NST LDS buffers: both operand tiles go global -> LDS directly (16 bytes per lane);
 // stage t + NST is issued once every wave has read stage t, so a stage has about NST - 1 stages
-// of compute to land.  A tile row (BK bf16) holds BK / 8 chunks of 16 bytes, XOR-swizzled per row (chunk_swz)
-// so that the rows a read instruction touches at one logical chunk hit distinct banks.
+// of compute to land.  A tile row (BK bf16) holds BK / 8 chunks of 16 bytes, XOR-swizzled per row
+// (chunk_swz) so that the rows a read instruction touches at one logical chunk hit distinct banks.
 // ---------------------------------------------------------------------------------------------
 constexpr int GBN = 256, GBM = 256;
 constexpr int kGemmMaxParts = 4;
@@ -62,15 +67,22 @@ __device__ __forceinline__ int chunk_swz(int c, int row) {
   else return c ^ ((row >> 2) & 3);                     // 64-byte rows: four per line
 }
 
-template <int BK, int NST, int GM>
-__global__ __launch_bounds__(512, 1) void gemm_rows_kernel(GemmRowsK a) {
-  constexpr int NW = 8;
+template <int BK, int NST, int GM, int NW, int MF>
+__global__ __launch_bounds__(NW * 64, 1) void gemm_rows_kernel(GemmRowsK a) {
+  // NW = 8: a wave owns 64 features x 128 rows (two waves per SIMD); NW = 4: 128 x 128 (one wave
+  // per SIMD, the accumulators in the AGPR half of the register file; measured about 10 % slower)
+  // MF = 32: v_mfma_f32_32x32x16_bf16 (32 x 32 blocks, k 16); MF = 16: v_mfma_f32_16x16x32_bf16
+  constexpr int WCOL = NW / 2;                 // waves across the features
+  constexpr int FI = 256 / WCOL / MF;          // MF-feature fragments per wave
+  constexpr int RJ = 128 / MF;                 // MF-row fragments per wave
+  constexpr int KM = MF == 32 ? 16 : 32;       // k per MFMA
+  typedef float accv_t __attribute__((ext_vector_type(MF == 32 ? 16 : 4)));
   constexpr int ROWB = BK * 2;                 // bytes of one tile row
   constexpr int CH = ROWB / 16;                // 16-byte chunks per row
   constexpr int TILE = 256 * ROWB;             // bytes of one operand tile
   constexpr int RPP = 1024 / ROWB;             // rows per 1 KB transfer
   constexpr int PPW = 256 / RPP / NW;          // transfers per wave per operand tile
-  constexpr int NS = BK / 16;                  // 16-wide k slices per stage
+  constexpr int NS = BK / KM;                  // k slices (one MFMA deep) per stage
   __shared__ __attribute__((aligned(1024))) char smem[NST * 2 * TILE];   // [stage][W | X]
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -131,46 +143,49 @@ __global__ __launch_bounds__(512, 1) void gemm_rows_kernel(GemmRowsK a) {
   // wait until this wave's transfers of every stage before the n youngest have landed
   auto wait_stages = [&](int n) {
     switch (n * 2 * PPW) {
-      case 0: SX_WAIT_VMCNT(0); break;
-      case 2: SX_WAIT_VMCNT(2); break;
-      case 4: SX_WAIT_VMCNT(4); break;
-      case 6: SX_WAIT_VMCNT(6); break;
-      case 8: SX_WAIT_VMCNT(8); break;
-      case 10: SX_WAIT_VMCNT(10); break;
-      default: SX_WAIT_VMCNT(12); break;
+      case 0: SX_WAIT_VMCNT6(0); break;
+      case 4: SX_WAIT_VMCNT6(4); break;
+      case 8: SX_WAIT_VMCNT6(8); break;
+      case 12: SX_WAIT_VMCNT6(12); break;
+      case 16: SX_WAIT_VMCNT6(16); break;
+      case 24: SX_WAIT_VMCNT6(24); break;
+      default: SX_WAIT_VMCNT6(32); break;
     }
   };
-  static_assert((NST - 1) * 2 * PPW <= 12, "wait table");
+  static_assert((NST - 1) * 2 * PPW <= 32 && (2 * PPW) % 4 == 0, "wait table");
   static_assert(NS % 2 == 0, "a stage holds an even number of slices");
 
   // ---- operand reads: row 32 j + l32 of a tile, logical chunk 2 s + hg: the lane part depends on
   // s only, the row block adds a constant (an immediate offset) ----
-  const int wn = wu & 3, wm = wu >> 2;
+  const int wn = wu % WCOL, wm = wu / WCOL;
+  // a lane reads row lr of each MF-row fragment, 16 bytes of k starting at chunk (KM / 8) s + cg
+  const int lr = lane % MF, cg = lane / MF;
   uint32_t lane_off[NS];
 #pragma unroll
-  for (int s = 0; s < NS; ++s) lane_off[s] = (uint32_t)(l32 * ROWB + (chunk_swz<CH>(2 * s + hg, l32) << 4));
-  f32x16_t acc[2][4];
+  for (int s = 0; s < NS; ++s)
+    lane_off[s] = (uint32_t)(lr * ROWB + (chunk_swz<CH>((KM / 8) * s + cg, lr) << 4));
+  accv_t acc[FI][RJ];
 #pragma unroll
-  for (int i = 0; i < 2; ++i)
+  for (int i = 0; i < FI; ++i)
 #pragma unroll
-    for (int j = 0; j < 4; ++j)
+    for (int j = 0; j < RJ; ++j)
 #pragma unroll
-      for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
+      for (int e = 0; e < (MF == 32 ? 16 : 4); ++e) acc[i][j][e] = 0.f;
 
   // fragments of one 16-wide k slice, read from stage buffer `buf`: one base register per matrix
   // (the empty asm keeps the sums from being re-associated into one register per read), the row
   // blocks as immediate offsets
-  auto read_slice = [&](int buf, int s, bf16x8_t (&fw)[2], bf16x8_t (&fx)[4]) {
+  auto read_slice = [&](int buf, int s, bf16x8_t (&fw)[FI], bf16x8_t (&fx)[RJ]) {
     const uint32_t sb = smem_lds + (uint32_t)(buf * 2 * TILE);
-    uint32_t wb = sb + lane_off[s] + (uint32_t)(wn * 64 * ROWB);
+    uint32_t wb = sb + lane_off[s] + (uint32_t)(wn * FI * MF * ROWB);
     uint32_t xb = sb + (uint32_t)TILE + lane_off[s] + (uint32_t)(wm * 128 * ROWB);
     asm volatile("" : "+v"(wb), "+v"(xb));
 #pragma unroll
-    for (int i = 0; i < 2; ++i)
-      fw[i] = *(const __attribute__((address_space(3))) bf16x8_t*)(uintptr_t)(wb + (uint32_t)(i * 32 * ROWB));
+    for (int i = 0; i < FI; ++i)
+      fw[i] = *(const __attribute__((address_space(3))) bf16x8_t*)(uintptr_t)(wb + (uint32_t)(i * MF * ROWB));
 #pragma unroll
-    for (int j = 0; j < 4; ++j)
-      fx[j] = *(const __attribute__((address_space(3))) bf16x8_t*)(uintptr_t)(xb + (uint32_t)(j * 32 * ROWB));
+    for (int j = 0; j < RJ; ++j)
+      fx[j] = *(const __attribute__((address_space(3))) bf16x8_t*)(uintptr_t)(xb + (uint32_t)(j * MF * ROWB));
   };
 
   // Software pipeline: the fragments of slice s + 1 are read while the MFMAs of slice s run (two
@@ -183,22 +198,27 @@ __global__ __launch_bounds__(512, 1) void gemm_rows_kernel(GemmRowsK a) {
   for (int t = 0; t < NST; ++t) issue(t);
   wait_stages(min(NST - 1, nk - 1));   // stage 0 has landed
   __syncthreads();
-  bf16x8_t fw[2][2], fx[2][4];
+  bf16x8_t fw[2][FI], fx[2][RJ];
   auto mfma_slice = [&](int c) {
 #pragma unroll
-    for (int i = 0; i < 2; ++i)
+    for (int i = 0; i < FI; ++i)
 #pragma unroll
-      for (int j = 0; j < 4; ++j) acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fw[c][i], fx[c][j], acc[i][j], 0, 0, 0);
+      for (int j = 0; j < RJ; ++j) {
+        if constexpr (MF == 32)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fw[c][i], fx[c][j], acc[i][j], 0, 0, 0);
+        else
+          acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fw[c][i], fx[c][j], acc[i][j], 0, 0, 0);
+      }
   };
   // the scheduler would sink the reads below the MFMAs (to reuse their registers): pin one read
-  // after each of the first six MFMAs
+  // after each of the first FI + RJ MFMAs
   auto interleave = [&]() {
 #pragma unroll
-    for (int q = 0; q < 6; ++q) {
+    for (int q = 0; q < FI + RJ; ++q) {
       __builtin_amdgcn_sched_group_barrier(kSgMfma, 1, 0);
       __builtin_amdgcn_sched_group_barrier(kSgDsRead, 1, 0);
     }
-    __builtin_amdgcn_sched_group_barrier(kSgMfma, 2, 0);
+    __builtin_amdgcn_sched_group_barrier(kSgMfma, FI * RJ - FI - RJ, 0);
   };
   read_slice(0, 0, fw[0], fx[0]);
   for (int t = 0; t + 1 < nk; ++t) {
@@ -230,21 +250,23 @@ __global__ __launch_bounds__(512, 1) void gemm_rows_kernel(GemmRowsK a) {
   // ---- epilogue: lane owns row 32 j + l32 of the wave's rows; value e of accumulator (i, j) is
   // feature 32 i + 8 (e / 4) + 4 hg + e % 4 of the wave's features.  Part boundaries are multiples
   // of the tile width, so the output part is the tile's. ----
+  // MF = 16: lane owns row 16 j + lr, value e of accumulator (i, j) is feature 16 i + 4 cg + e
+  static_assert(RJ * MF == 128, "two waves of rows cover the 256-row tile");
   int part = 0;
   while (part + 1 < a.n_parts && n0 >= a.pn[part + 1]) ++part;
   uint16_t* const yp = a.y[part];
   const int ld = a.pn[part + 1] - a.pn[part];
-  const int c0 = n0 - a.pn[part] + wn * 64 + 4 * hg;
+  const int c0 = n0 - a.pn[part] + wn * FI * MF + 4 * cg;
 #pragma unroll
-  for (int j = 0; j < 4; ++j) {
-    const int m = m0 + wm * 128 + 32 * j + l32;
+  for (int j = 0; j < RJ; ++j) {
+    const int m = m0 + wm * 128 + MF * j + lr;
     if (m >= nr) continue;
     const int64_t yr = row_index(rq, a.rows, m, a.y_tok) * ld;
 #pragma unroll
-    for (int i = 0; i < 2; ++i)
+    for (int i = 0; i < FI; ++i)
 #pragma unroll
-      for (int g = 0; g < 4; ++g) {
-        const int c = c0 + 32 * i + 8 * g;
+      for (int g = 0; g < (MF == 32 ? 4 : 1); ++g) {
+        const int c = c0 + MF * i + 8 * g;
         float v[4];
 #pragma unroll
         for (int e = 0; e < 4; ++e) v[e] = acc[i][j][4 * g + e];
@@ -269,6 +291,12 @@ __global__ __launch_bounds__(512, 1) void gemm_rows_kernel(GemmRowsK a) {
 #endif
 #ifndef SX_GEMM_GM
 #define SX_GEMM_GM 8
+#endif
+#ifndef SX_GEMM_NW
+#define SX_GEMM_NW 8
+#endif
+#ifndef SX_GEMM_MF
+#define SX_GEMM_MF 16
 #endif
 
 // ---------------------------------------------------------------------------------------------
@@ -426,12 +454,12 @@ hipError_t launch_gemm_rows(const sx_plan* p, const RowsArg& r, const void* x, i
   a.N = n;
   a.n_req = p->n_req;
   a.m_tiles = (r.max_rows + GBM - 1) / GBM;
-  constexpr int BK = SX_GEMM_BK, NST = SX_GEMM_NST, GM = SX_GEMM_GM;
+  constexpr int BK = SX_GEMM_BK, NST = SX_GEMM_NST, GM = SX_GEMM_GM, NW = SX_GEMM_NW, MF = SX_GEMM_MF;
   a.x_tok = x_tok;
   a.y_tok = y_tok;
   const int64_t tiles = (int64_t)a.m_tiles * p->n_req * (n / GBN);
   const int64_t blocks = (tiles + kGemmXcds - 1) / kGemmXcds * kGemmXcds;
-  hipLaunchKernelGGL((gemm_rows_kernel<BK, NST, GM>), dim3((unsigned)blocks), dim3(512), 0, s, a);
+  hipLaunchKernelGGL((gemm_rows_kernel<BK, NST, GM, NW, MF>), dim3((unsigned)blocks), dim3(NW * 64), 0, s, a);
   return hipGetLastError();
 }
 
