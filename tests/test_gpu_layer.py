@@ -339,3 +339,86 @@ def test_layer_body_matches_oracle():
     assert np.array_equal(O.gather_tokens(req, w, host(vc))[np.setdiff1d(np.arange(T), R)],
                           O.gather_tokens(req, w, ref["v_pool"])[np.setdiff1d(np.arange(T), R)])
     plan.close()
+
+
+def test_layer_body_full_size_sampled_rows():
+    """The layer body at the benchmark's size and launch configuration (the 32768-token chat stack:
+    32/8/128 heads, hidden 4096, feed-forward 14336, the 6712 rows of its stored recompute set),
+    each operation checked on 64 sampled rows against the oracle fed with the GPU's own inputs to
+    that operation (a row of every output depends only on that row of the inputs and the weights,
+    so a sampled row is an exact check).  The attention output is replaced by seeded values: the
+    attention kernels have their own full-size tests."""
+    import os
+    w = W.config(3)
+    req = w.requests[0]
+    T = req.n_tokens
+    Hq, Hkv, d, H, F, eps = w.n_q_heads, w.n_kv_heads, w.head_dim, 4096, 14336, 1e-5
+    R = np.load(os.path.join(os.path.dirname(__file__), "golden", "c3_boundary.npz"))["R"].astype(np.int64)
+    log(f"[layer_body full size] T={T} |R|={len(R)} hidden={H} ffn={F}")
+    rng = np.random.default_rng(31)
+    hidden = _bf16(rng, (T, H))
+    att = _bf16(rng, (T, Hq * d))
+    wts = {"ln1": O.to_bf16((1 + 0.1 * rng.standard_normal(H)).astype(np.float32)),
+           "wqkv": _bf16(rng, ((Hq + 2 * Hkv) * d, H), 1 / math.sqrt(H)),
+           "wo": _bf16(rng, (H, Hq * d), 1 / math.sqrt(Hq * d)),
+           "ln2": O.to_bf16((1 + 0.1 * rng.standard_normal(H)).astype(np.float32)),
+           "wgu": _bf16(rng, (2 * F, H), 1 / math.sqrt(H)),
+           "wd": _bf16(rng, (H, F), 1 / math.sqrt(F))}
+    plan = sx.Plan(desc_of(w), w.requests, w.n_dst_blocks, w.n_src_blocks)
+    rows = torch.zeros(T, dtype=torch.int32, device="cuda")
+    rows[:len(R)] = torch.from_numpy(R.astype(np.int32)).cuda()
+    n_rows = torch.tensor([len(R)], dtype=torch.int32, device="cuda")
+    m = len(R)
+    z = lambda *s: torch.zeros(s, dtype=torch.bfloat16, device="cuda")
+    wd = {k: dev(v, w) for k, v in wts.items()}
+    hid, atd = dev(hidden, w), dev(att, w)
+    x1, q, k, v, h1, x2, gu, a = z(T, H), z(T, Hq, d), z(T, Hkv, d), z(T, Hkv, d), z(T, H), z(T, H), z(T, 2 * F), z(T, F)
+    sx.rmsnorm_rows(plan, rows, n_rows, m, hid, wd["ln1"], eps, x1, x_by_token=True)
+    sx.gemm_rows_split(plan, rows, n_rows, m, x1, wd["wqkv"], [q, k, v], y_by_token=True)
+    qk_pre = (host(q), host(k))
+    sx.rope_rows(plan, rows, n_rows, m, q, k)
+    sx.gemm_rows(plan, rows, n_rows, m, atd, wd["wo"], h1, residual=hid, y_by_token=True)
+    sx.rmsnorm_rows(plan, rows, n_rows, m, h1, wd["ln2"], eps, x2, x_by_token=True)
+    sx.gemm_rows(plan, rows, n_rows, m, x2, wd["wgu"], gu)
+    sx.silu_mul_rows(plan, n_rows, m, gu, a)
+    h1_before = host(h1)
+    sx.gemm_rows(plan, rows, n_rows, m, a, wd["wd"], hid, residual=h1, y_by_token=True)
+    torch.cuda.synchronize()
+
+    pick = np.unique(np.concatenate([[0, 1, m - 2, m - 1], rng.choice(m, 60, replace=False)]))
+    tok = R[pick]          # token rows of the sampled slots
+    g = {n: host(t) for n, t in (("x1", x1), ("q", q), ("k", k), ("x2", x2), ("gu", gu), ("a", a), ("h2", hid))}
+
+    def gemm_ok(name, xin, wt, got, res=None):
+        ref = O.linear(xin, wt, res)
+        mag = np.abs(xin).astype(np.float64) @ np.abs(wt).astype(np.float64).T
+        bound = BF16_ULP * np.abs(ref) + 1e-5 * mag + 1e-6
+        worst = float((np.abs(got - ref) / bound).max())
+        log(f"  {name}: worst error / bound {worst:.3f}")
+        assert worst <= 1.0, name
+
+    # RMSNorm of the hidden states (token rows in, slot rows out)
+    ref = O.rmsnorm(hidden[tok], wts["ln1"], eps)
+    assert np.all(np.abs(g["x1"][pick] - ref) <= 2 * BF16_ULP * np.abs(ref) + 1e-6)
+    # stacked Q/K/V (slot rows in, token rows out), before RoPE
+    n_q = Hq * d
+    gemm_ok("q|k|v", g["x1"][pick], wts["wqkv"],
+            np.concatenate([qk_pre[0][tok].reshape(len(tok), -1), qk_pre[1][tok].reshape(len(tok), -1),
+                            host(v)[tok].reshape(len(tok), -1)], axis=1))
+    # RoPE at the tokens' positions in the new sequence, bit for bit
+    _, pos, _ = O.token_layout(T, req.segments)
+    for got, pre in ((g["q"], qk_pre[0]), (g["k"], qk_pre[1])):
+        want = O.store(O.rope_at_positions(pre[tok], pos[tok], w.rope_base, w.rope_style), "bf16")
+        assert np.array_equal(got[tok], want)
+    # output projection + residual, RMSNorm, gate|up, SwiGLU, down projection + residual
+    gemm_ok("o + residual", att[pick], wts["wo"], h1_before[tok], res=hidden[tok])
+    ref = O.rmsnorm(h1_before[tok], wts["ln2"], eps)
+    assert np.all(np.abs(g["x2"][pick] - ref) <= 2 * BF16_ULP * np.abs(ref) + 1e-6)
+    gemm_ok("gate|up", g["x2"][pick], wts["wgu"], g["gu"][pick])
+    ref = O.silu_mul(g["gu"][pick])
+    assert np.all(np.abs(g["a"][pick] - ref) <= 2 * BF16_ULP * np.abs(ref) + 1e-6)
+    gemm_ok("down + residual", g["a"][pick], wts["wd"], g["h2"][tok], res=h1_before[tok])
+    # rows outside R keep their hidden state
+    others = np.setdiff1d(np.arange(T), R)[:: max(1, (T - m) // 512)]
+    assert np.array_equal(g["h2"][others], hidden[others])
+    plan.close()
