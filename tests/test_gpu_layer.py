@@ -422,3 +422,50 @@ def test_layer_body_full_size_sampled_rows():
     others = np.setdiff1d(np.arange(T), R)[:: max(1, (T - m) // 512)]
     assert np.array_equal(g["h2"][others], hidden[others])
     plan.close()
+
+
+def test_layer_ops_with_an_empty_request():
+    """A request whose row list is empty (n_rows = 0) between two that have rows: nothing of it is
+    read or written, the others are computed as usual (GEMM, split GEMM, RMSNorm, RoPE, SwiGLU)."""
+    w = _ragged_workload(seed=17)
+    rng = np.random.default_rng(18)
+    per, rows, n_rows, m = _rows(w, rng, 0.5)
+    per[1] = per[1][:0]
+    n_rows[1] = 0
+    tot, K, N, F = w.total_tokens, 256, 512, 256
+    x = _bf16(rng, (tot, K))
+    wt = _bf16(rng, (N, K), 1 / math.sqrt(K))
+    gamma = O.to_bf16((1 + 0.2 * rng.standard_normal(K)).astype(np.float32))
+    gu = _bf16(rng, (tot, 2 * F), 2.0)
+    q = _bf16(rng, (tot, 8, 128))
+    k = _bf16(rng, (tot, 2, 128))
+    plan = sx.Plan(desc_of(w), w.requests, w.n_dst_blocks, w.n_src_blocks)
+    full = lambda n: torch.full((tot, n), CANARY, dtype=torch.bfloat16, device="cuda")
+    y, y1, y2, xn, a = full(N), full(256), full(256), full(K), full(F)
+    qd, kd = dev(q, w), dev(k, w)
+    sx.gemm_rows(plan, rows, n_rows, m, dev(x, w), dev(wt, w), y, x_by_token=True, y_by_token=True)
+    sx.gemm_rows_split(plan, rows, n_rows, m, dev(x, w), dev(wt, w), [y1, y2], x_by_token=True, y_by_token=True)
+    sx.rmsnorm_rows(plan, rows, n_rows, m, dev(x, w), dev(gamma, w), 1e-5, xn, x_by_token=True, y_by_token=True)
+    sx.silu_mul_rows(plan, n_rows, m, dev(gu, w), a)
+    sx.rope_rows(plan, rows, n_rows, m, qd, kd)
+    torch.cuda.synchronize()
+    off = w.token_offsets
+    for r in range(3):
+        ti = off[r] + per[r]
+        si = off[r] + np.arange(len(per[r]))
+        span = np.arange(off[r], off[r + 1])
+        if r == 1:   # the empty request: its rows keep the canary / their input values
+            for t in (y, y1, y2, xn, a):
+                assert np.all(host(t)[span] == CANARY)
+            assert np.array_equal(host(qd)[span], q[span]) and np.array_equal(host(kd)[span], k[span])
+            continue
+        ref = O.linear(x[ti], wt)
+        mag = np.abs(x[ti]).astype(np.float64) @ np.abs(wt).astype(np.float64).T
+        bound = BF16_ULP * np.abs(ref) + 1e-5 * mag + 1e-6
+        assert np.all(np.abs(host(y)[ti] - ref) <= bound)
+        assert np.all(np.abs(np.concatenate([host(y1)[ti], host(y2)[ti]], axis=1) - ref) <= bound)
+        ref = O.rmsnorm(x[ti], gamma, 1e-5)
+        assert np.all(np.abs(host(xn)[ti] - ref) <= 2 * BF16_ULP * np.abs(ref) + 1e-6)
+        ref = O.silu_mul(gu[si])
+        assert np.all(np.abs(host(a)[si] - ref) <= 2 * BF16_ULP * np.abs(ref) + 1e-6)
+    plan.close()
