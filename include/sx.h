@@ -84,8 +84,14 @@ typedef struct sx_layer_desc {
   int32_t rope_style;     /* SX_ROPE_NEOX or SX_ROPE_GPTJ */
   double rope_base;       /* > 0 */
   float softmax_scale;    /* 0 -> 1/sqrt(head_dim) */
-  int32_t reserved;       /* must be 0 */
+  int32_t flags;          /* 0, or SX_TOPK_ALL_POSITIONS */
 } sx_layer_desc;
+
+/* sx_layer_desc.flags.  SX_TOPK_ALL_POSITIONS: the top-k of Eq. topk ranges over every position of
+ * the request (the equation as printed) instead of the reused positions only; the budget becomes
+ * k = min(T, floor(ratio * T + 1/2)).  I_nr, the overflow and the tail-fallback rows are unchanged
+ * and still always in R, so a selected uncached position spends budget without adding a row. */
+#define SX_TOPK_ALL_POSITIONS 1
 
 /* One contiguous segment of a request (Section 3.1 segment-level cache; Algorithm 1 input:
  * original positions p_m and current positions p'_m). */
@@ -115,7 +121,7 @@ typedef struct sx_plan_info {
   int64_t total_tokens;     /* sum T */
   int32_t n_requests;
   int32_t max_tokens;       /* max T */
-  int64_t n_reused;         /* sum |I_reuse| (top-k candidates) */
+  int64_t n_reused;         /* sum of top-k candidates: |I_reuse| (T with SX_TOPK_ALL_POSITIONS) */
   int64_t n_nonreused;      /* sum |I_nr| */
   int64_t n_probes;         /* sum |I_nr U S_tail| (Sparse-Q rows that score) */
   int64_t n_base;           /* sum |I_nr U S_ov U S_tail| (rows of R whatever the scores) */
@@ -233,7 +239,8 @@ sx_status sx_sparseq_score(const sx_plan* plan, const void* q, const void* k_cac
                            float* scores, void* stream);
 
 /* Eq. topk, Section 3.3 and Algorithm 1 steps 14-17, per request: S_key = the k_r reused
- * positions with the largest score (k_r as in sx_plan_budget; ties go to the lower index),
+ * positions (every position with SX_TOPK_ALL_POSITIONS) with the largest score (k_r as in
+ * sx_plan_budget; ties go to the lower index),
  * R = sorted(I_nr U S_key U S_ov U S_tail) written in the row-list layout.  Selection compares
  * the float32 scores exactly.  ratio outside [0, 1] -> SX_EINVAL. */
 sx_status sx_topk_select(const sx_plan* plan, const float* scores, double ratio, int32_t* rows,

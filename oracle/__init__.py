@@ -252,13 +252,16 @@ def topk_keys(scores: np.ndarray, candidates: np.ndarray, k: int) -> np.ndarray:
     return np.array(sorted(cand[:k]), dtype=np.int64)
 
 
-def recompute_set(n_tokens: int, segments, scores: np.ndarray, ratio: float, block: int) -> dict:
+def recompute_set(n_tokens: int, segments, scores: np.ndarray, ratio: float, block: int,
+                  candidates: str = "reused") -> dict:
     """Algorithm 1 step 17: R = I_nr U S_key U S_ov U S_tail, sorted.  Candidates of the top-k
-    are the reused positions, with k = budget(|I_reuse|, ratio)."""
+    are the reused positions, with k = budget(|I_reuse|, ratio); candidates="all" takes Eq. topk
+    as printed, over every position (k = budget(T, ratio))."""
     i_nr = nonreuse_positions(n_tokens, segments)
     i_reuse = reuse_positions(n_tokens, segments)
-    k = budget(len(i_reuse), ratio)
-    s_key = topk_keys(scores, i_reuse, k)
+    cand = i_reuse if candidates == "reused" else np.arange(n_tokens, dtype=np.int64)
+    k = budget(len(cand), ratio)
+    s_key = topk_keys(scores, cand, k)
     s_ov = overflow_positions(n_tokens, segments, block)
     s_tail = tail_fallback(n_tokens, segments)
     R = np.union1d(np.union1d(i_nr, s_key), np.union1d(s_ov, s_tail)).astype(np.int64)

@@ -25,8 +25,8 @@ from typing import Optional, Sequence
 __all__ = [
     "LIB_PATH", "SxError", "lib", "LayerDesc", "Plan", "rope_realign", "kv_scatter", "realign_scatter",
     "realign_scatter_layers", "rows_mask", "realign_scatter_masked", "sparseq_score",
-    "topk_select", "sparse_attn", "full_attn", "gemm_rows", "rmsnorm_rows", "rope_rows", "silu_mul_rows",
-    "F32", "BF16", "ROPE_NEOX", "ROPE_GPTJ", "EXPORTED",
+    "topk_select", "sparse_attn", "full_attn", "gemm_rows", "gemm_rows_split", "rmsnorm_rows", "rope_rows",
+    "silu_mul_rows", "F32", "BF16", "ROPE_NEOX", "ROPE_GPTJ", "TOPK_ALL_POSITIONS", "EXPORTED",
 ]
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libsx.so")
@@ -44,6 +44,9 @@ EXPORTED = (
 )
 
 
+TOPK_ALL_POSITIONS = 1   # sx_layer_desc.flags: Eq. topk over every position
+
+
 class SxError(RuntimeError):
     def __init__(self, status: int, msg: str):
         super().__init__(f"libsx status {status}: {msg}")
@@ -54,7 +57,7 @@ class LayerDesc(ctypes.Structure):
     _fields_ = [
         ("n_q_heads", ctypes.c_int32), ("n_kv_heads", ctypes.c_int32), ("head_dim", ctypes.c_int32),
         ("block_size", ctypes.c_int32), ("dtype", ctypes.c_int32), ("rope_style", ctypes.c_int32),
-        ("rope_base", ctypes.c_double), ("softmax_scale", ctypes.c_float), ("reserved", ctypes.c_int32),
+        ("rope_base", ctypes.c_double), ("softmax_scale", ctypes.c_float), ("flags", ctypes.c_int32),
     ]
 
 
@@ -146,13 +149,14 @@ def _stream(stream) -> Optional[int]:
 
 
 def make_desc(n_q_heads, n_kv_heads, head_dim, dtype, rope_base, rope_style=ROPE_NEOX, block_size=16,
-              softmax_scale=0.0) -> LayerDesc:
+              softmax_scale=0.0, topk_all_positions=False) -> LayerDesc:
+    """A layer descriptor; topk_all_positions sets SX_TOPK_ALL_POSITIONS (Eq. topk over every position)."""
     if isinstance(dtype, str):
         dtype = {"f32": F32, "bf16": BF16}[dtype]
     if isinstance(rope_style, str):
         rope_style = {"neox": ROPE_NEOX, "gptj": ROPE_GPTJ}[rope_style]
     return LayerDesc(n_q_heads, n_kv_heads, head_dim, block_size, dtype, rope_style, float(rope_base),
-                     float(softmax_scale), 0)
+                     float(softmax_scale), TOPK_ALL_POSITIONS if topk_all_positions else 0)
 
 
 class Plan:

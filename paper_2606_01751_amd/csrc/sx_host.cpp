@@ -62,7 +62,7 @@ sx_status validate_desc(const sx_layer_desc* d) {
   if (!(d->rope_base > 0.0) || !std::isfinite(d->rope_base)) return fail(SX_EINVAL, "rope_base must be > 0");
   if (!(d->softmax_scale >= 0.0f) || !std::isfinite(d->softmax_scale))
     return fail(SX_EINVAL, "softmax_scale must be finite and >= 0");
-  if (d->reserved != 0) return fail(SX_EINVAL, "reserved field must be 0");
+  if (d->flags & ~SX_TOPK_ALL_POSITIONS) return fail(SX_EINVAL, "unknown flags 0x%x", (unsigned)d->flags);
   return SX_OK;
 }
 
@@ -261,6 +261,10 @@ sx_status sx_plan_create(const sx_layer_desc* desc, const sx_request* requests, 
       cnt_reuse += cand;
       if (!cand || t >= tail_lo) probe[off + cnt_probe++] = t;
       if (base[t]) { fl[t] |= sx::kFlagBase; ++cnt_base; }
+    }
+    if (p->desc.flags & SX_TOPK_ALL_POSITIONS) {   // Eq. topk over every position
+      for (int t = 0; t < T; ++t) fl[t] |= sx::kFlagCandidate;
+      cnt_reuse = T;
     }
     h.n_reuse = cnt_reuse;
     h.n_probe = cnt_probe;

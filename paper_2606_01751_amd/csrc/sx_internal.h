@@ -20,7 +20,7 @@ struct ReqDev {
   int32_t T;        // tokens of the request
   int32_t tok_off;  // first token in the concatenation of all requests
   int32_t bt_off;   // first entry of its block table in the concatenated tables
-  int32_t n_reuse;  // |I_reuse|: top-k candidates
+  int32_t n_reuse;  // top-k candidates: |I_reuse|, or T with SX_TOPK_ALL_POSITIONS
   int32_t n_probe;  // |I_nr U S_tail|: Sparse-Q rows
   int32_t n_nr;     // |I_nr|
   int32_t n_base;   // |I_nr U S_ov U S_tail|

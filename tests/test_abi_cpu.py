@@ -69,6 +69,9 @@ def test_plan_rejects_bad_descriptors():
     assert _status(_desc(dtype=7), r)[0] == sx.SX_EUNSUPPORTED
     assert _status(_desc(rope_base=-1.0), r)[0] == sx.SX_EINVAL
     assert _status(_desc(rope_style=5), r)[0] == sx.SX_EINVAL
+    d = _desc()
+    d.flags = 2                                   # no such flag
+    assert _status(d, r)[0] == sx.SX_EINVAL
 
 
 def test_plan_rejects_bad_segment_tables():

@@ -294,6 +294,33 @@ def test_topk_ties_and_zeros_exact():
         assert max(len(x) for x in gR) <= g.plan.budget(ratio)[1]
 
 
+def test_topk_all_positions_flag_exact():
+    """SX_TOPK_ALL_POSITIONS: the selection over every position, against the oracle's reading of
+    Eq. topk as printed, on the same scores (many ties)."""
+    log("[topk all positions]")
+    w = CASES[4][1]
+    rng = np.random.default_rng(6)
+    s = rng.integers(0, 4, size=w.total_tokens).astype(np.float32) * np.float32(0.25)
+    desc = sx.make_desc(w.n_q_heads, w.n_kv_heads, w.head_dim, w.dtype, w.rope_base, w.rope_style,
+                        topk_all_positions=True)
+    plan = sx.Plan(desc, w.requests, w.n_dst_blocks, w.n_src_blocks)
+    assert plan.info()["n_reused"] == w.total_tokens
+    scores = torch.from_numpy(s).cuda()
+    rows = torch.zeros(w.total_tokens, dtype=torch.int32, device="cuda")
+    n_rows = torch.zeros(len(w.requests), dtype=torch.int32, device="cuda")
+    offs = w.token_offsets
+    for ratio in (0.0, 0.07, 0.33, 0.999, 1.0):
+        sx.topk_select(plan, scores, ratio, rows, n_rows)
+        torch.cuda.synchronize()
+        gR = rows_per_request(w, rows, n_rows)
+        for r, req in enumerate(w.requests):
+            want = O.recompute_set(req.n_tokens, req.segments, s[offs[r]:offs[r + 1]].astype(np.float64), ratio,
+                                   w.block_size, candidates="all")["R"]
+            np.testing.assert_array_equal(gR[r], want)
+        assert max(len(x) for x in gR) <= plan.budget(ratio)[1]
+    plan.close()
+
+
 def test_ratio_one_equals_full_attention():
     log("[ratio 1]")
     for name, w in (CASES[0], CASES[3]):

@@ -301,6 +301,34 @@ def _seg(specs):
     return w.requests[0]
 
 
+@pytest.mark.parametrize("seed", range(3))
+def test_recompute_set_over_all_positions(seed):
+    """Eq. topk as printed (candidates = every position): S_key holds the k = floor(r T + 1/2)
+    positions that a rank count over all T positions puts first; the other parts of R are those of
+    the default reading, and with every position a candidate R can only grow with the ratio."""
+    rng = np.random.default_rng(40 + seed)
+    r = _seg([(48, True, 0, None), (16, False, 0, None), (64, True, 5, None), (32, False, 0, None)])
+    T = 160
+    scores = rng.integers(0, 8, size=T).astype(np.float64)
+    prev = None
+    for ratio in (0.0, 0.1, 0.25, 0.5, 1.0):
+        got = O.recompute_set(T, r.segments, scores, ratio, 16, candidates="all")
+        base = O.recompute_set(T, r.segments, scores, ratio, 16)
+        k = int(np.floor(ratio * T + 0.5))
+        assert got["k"] == k and len(got["S_key"]) == k
+        rank = np.array([sum(1 for j2 in range(T) if scores[j2] > scores[j] or (scores[j2] == scores[j] and j2 < j))
+                         for j in range(T)])
+        np.testing.assert_array_equal(got["S_key"], np.flatnonzero(rank < k))
+        for part in ("I_nr", "S_ov", "S_tail"):
+            np.testing.assert_array_equal(got[part], base[part])
+        np.testing.assert_array_equal(got["R"], np.union1d(base["I_nr"], np.union1d(got["S_key"], np.union1d(
+            base["S_ov"], base["S_tail"]))))
+        if prev is not None:
+            assert set(prev) <= set(got["R"])
+        prev = got["R"]
+    assert len(prev) == T
+
+
 def test_overflow_edge_layouts():
     # uncached run at the start: only a right-hand block
     r = _seg([(20, False, 0, None), (40, True, 0, None)])
