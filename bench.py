@@ -46,6 +46,7 @@ def parse():
     ap.add_argument("--ratio", type=float, default=None)
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-peaks", action="store_true", help="skip the copy / GEMM measurement of achievable peaks")
     ap.add_argument("--layers", type=int, default=None, help="override the number of layers (profiling)")
     ap.add_argument("--score-passes", type=int, choices=(1, 2), default=1,
                     help="Sparse-Q scoring in hybrid stacks: 1 = denominators from the boundary layer's full "
@@ -164,7 +165,9 @@ class Timers:
         out = {}
         for k, lst in self.ev.items():
             ms = [s.elapsed_time(e) for s, e in lst]
-            out[k] = {"launches": len(ms), "avg_ms": float(np.mean(ms)), "total_ms": float(np.sum(ms))}
+            p10, p50, p90 = np.percentile(ms, [10, 50, 90])
+            out[k] = {"launches": len(ms), "avg_ms": float(np.mean(ms)), "total_ms": float(np.sum(ms)),
+                      "p10_ms": float(p10), "median_ms": float(p50), "p90_ms": float(p90)}
         return out
 
 
@@ -419,6 +422,8 @@ def main():
         kind, amount = work[name]
         sec = k["avg_ms"] / 1e3
         e = {"launches_per_step": k["launches"] // args.steps, "avg_us": round(k["avg_ms"] * 1e3, 2),
+             "median_us": round(k["median_ms"] * 1e3, 2), "p10_us": round(k["p10_ms"] * 1e3, 2),
+             "p90_us": round(k["p90_ms"] * 1e3, 2),
              "share_of_step": round(k["total_ms"] / args.steps / ms_per_step, 4)}
         if kind == "mfma":
             e["tflops"] = round(amount / sec / 1e12, 2)
@@ -445,6 +450,19 @@ def main():
                 "algorithmic_per_launch": amount}
 
     value = T * L / (ms_per_step / 1e3)
+    # per layer kind: a sparse layer's calls (one-pass re-alignment + KV write, sparse attention), a
+    # full layer's (KV write of every row, full attention), and the once-per-step selection
+    layer_rates = None
+    us = {n: kern[n]["avg_ms"] * 1e3 for n in kern}
+    if not args.layer_body and "sx_sparse_attn" in us and "sx_full_attn" in us:
+        kv_us = us.get("sx_realign_scatter_masked", us.get("sx_realign_scatter", 0.0))
+        sp = kv_us + us["sx_sparse_attn"]
+        fu = us.get("sx_kv_scatter", 0.0) + us["sx_full_attn"]
+        layer_rates = {"sparse_layer_us": round(sp, 1), "sparse_layer_tokens_per_s": round(T / (sp / 1e6), 1),
+                       "full_layer_us": round(fu, 1), "full_layer_tokens_per_s": round(T / (fu / 1e6), 1),
+                       "selection_us": round(sum(us.get(n, 0.0) for n in ("sx_sparseq_score", "sx_topk_select",
+                                                                           "sx_rows_mask")), 1)}
+    peaks = None if args.no_peaks else measured_peaks(torch)
     cpu = None
     if not args.no_cpu_baseline and not args.layer_body:
         cpu = cpu_baseline(w, layers, R, nfull, L, ratio, torch)
@@ -458,9 +476,42 @@ def main():
                    "kv_write": args.kv_write, "layer_body": bool(args.layer_body),
                    **({"hidden": H, "ffn": F} if args.layer_body else {})},
         "kernels": kernels, "roofline": roof, "cpu_baseline": cpu,
+        "layer_rates": layer_rates, "measured_peaks": peaks,
     }
     print(json.dumps(res), flush=True)
     plan.close()
+
+
+def measured_peaks(torch):
+    """Achievable rates on this GPU next to the datasheet peaks: a device copy of 2 GiB (far beyond
+    the 256 MB Infinity Cache; read + write bytes) and a bf16 8192^3 matrix product (torch.matmul,
+    i.e. hipBLASLt).  Outside the timed steps."""
+    src = torch.empty(1 << 30, dtype=torch.bfloat16, device="cuda").fill_(1.0)
+    dst = torch.empty_like(src)
+    a = torch.randn((8192, 8192), dtype=torch.float32, device="cuda").to(torch.bfloat16)
+    b = torch.randn((8192, 8192), dtype=torch.float32, device="cuda").to(torch.bfloat16)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    dst.copy_(src)
+    torch.cuda.synchronize()
+    e0.record()
+    for _ in range(5):
+        dst.copy_(src)
+    e1.record()
+    torch.cuda.synchronize()
+    copy_gbs = 5 * 2 * src.numel() * 2 / (e0.elapsed_time(e1) / 1e3) / 1e9
+    c = a @ b
+    torch.cuda.synchronize()
+    e0.record()
+    for _ in range(10):
+        c = a @ b
+    e1.record()
+    torch.cuda.synchronize()
+    gemm_tf = 10 * 2 * 8192 ** 3 / (e0.elapsed_time(e1) / 1e3) / 1e12
+    del src, dst, a, b, c
+    torch.cuda.empty_cache()
+    return {"hbm_copy_gbps": round(copy_gbs, 1), "hbm_copy_frac_of_peak": round(copy_gbs / PEAK_HBM_GBS, 4),
+            "bf16_gemm_tflops": round(gemm_tf, 1), "bf16_gemm_frac_of_peak": round(gemm_tf / PEAK_BF16_TFLOPS, 4),
+            "copy": "device copy of 2 GiB (read + write bytes)", "gemm": "torch.matmul 8192^3 bf16 (hipBLASLt)"}
 
 
 def cpu_baseline(w, layers, R, nfull, L, ratio, torch):
@@ -520,7 +571,16 @@ def cpu_baseline(w, layers, R, nfull, L, ratio, torch):
     else:
         t_step = t["realign"] + 2 * t["scatter_R"] + t["score"] + t["topk"] + t["sparse_attn"]
     value = w.total_tokens * L / t_step
+    model = None
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                model = line.split(":", 1)[1].strip()
+                break
+    except OSError:
+        pass
     return {"value": round(value, 2), "unit": "tokens/s", "cores": int(threads), "kind": "oracle",
+            "cpu_model": model, "host_cpus": os.cpu_count(),
             "sample": (f"one layer of request 0: full re-alignment, KV writes and top-k; attention of {len(samp)} "
                        f"rows of R, {len(ps)} Sparse-Q probe rows and {ns} full-attention rows, scaled to the "
                        f"whole {L}-layer step by the oracle's cost per row"),
