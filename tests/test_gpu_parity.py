@@ -238,6 +238,36 @@ def test_full_attention_matches_oracle(name, w):
 @pytest.mark.parametrize("name,w", CASES, ids=IDS)
 @pytest.mark.parametrize("ratio", [0.15, 0.5])
 def test_sparse_layer_matches_oracle(name, w, ratio):
+    check_sparse_layer(name, w, ratio)
+
+
+def _random_case(seed):
+    """A seeded random layer: request count and lengths, segment layout, head shape (GQA group
+    1-8, one or more KV heads), head dim, storage type, RoPE pair layout and recompute ratio."""
+    rng = np.random.default_rng(1000 + seed)
+    Hq, Hkv = [(8, 2), (4, 4), (14, 2), (16, 2), (6, 1), (32, 8), (8, 1), (12, 4)][seed % 8]
+    d = int(rng.choice([64, 128]))
+    dtype = "f32" if seed % 4 == 3 else "bf16"
+    style = str(rng.choice(["neox", "gptj"]))
+    n_req = int(rng.integers(1, 4))
+    specs = [W.random_request_specs(rng, int(rng.integers(40, 700)), max_seg=int(rng.integers(20, 200)),
+                                    max_pos=int(rng.integers(1000, 60000)))
+             for _ in range(n_req)]
+    w = W.custom_workload(specs, n_q_heads=Hq, n_kv_heads=Hkv, head_dim=d, dtype=dtype,
+                          rope_base=float(rng.choice([1e4, 5e5, 1e6])), rope_style=style, seed=seed,
+                          plant_per_segment=int(rng.integers(0, 4)), name=f"random-{seed}")
+    return w, float(rng.uniform(0.05, 0.6))
+
+
+@pytest.mark.parametrize("seed", range(8))
+def test_random_layouts_match_oracle(seed):
+    """The whole selecting layer on seeded random layouts and shapes, to the same bar."""
+    w, ratio = _random_case(seed)
+    check_sparse_layer(f"random-{seed} ({w.n_q_heads}/{w.n_kv_heads}/{w.head_dim} {w.dtype} {w.rope_style}, "
+                       f"{len(w.requests)} requests)", w, ratio)
+
+
+def check_sparse_layer(name, w, ratio):
     log(f"[layer] {name} ratio {ratio}")
     t = W.layer_tensors(w, 0)
     g = GpuLayer(w, t)
