@@ -96,9 +96,15 @@ def _check(st: int) -> None:
 
 
 def _ints(xs):
-    """(pointer, count) of an int32 copy of xs; the pointer keeps the copy alive."""
-    a = np.ascontiguousarray(np.asarray(xs, dtype=np.int64).astype(np.int32) if not isinstance(xs, np.ndarray)
-                             or xs.dtype != np.int32 else xs)
+    """(pointer, count) of an int32 copy of xs (token ids and block ids are int32 in the ABI; values
+    outside that range raise); the pointer keeps the copy alive."""
+    if isinstance(xs, np.ndarray) and xs.dtype == np.int32:
+        a = np.ascontiguousarray(xs)
+    else:
+        wide = np.asarray(xs, dtype=np.int64)
+        if wide.size and (wide.min() < -2**31 or wide.max() >= 2**31):
+            raise ValueError("value outside the int32 range")
+        a = np.ascontiguousarray(wide.astype(np.int32))
     if a.size == 0:
         a = np.zeros(1, np.int32)
         n = 0

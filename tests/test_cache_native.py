@@ -155,6 +155,8 @@ def test_errors_leave_the_state_unchanged():
         c.frozen_delete([0, 0])                   # listed twice
     c.release(s.req_id)
     assert c.stats()["idle_frozen"] == 2
+    with pytest.raises(ValueError):
+        c.schedule([2**31])                        # token ids are int32
     with pytest.raises(N.SxError):
         N.BlockCache(0, 4)
     with pytest.raises(N.SxError):
