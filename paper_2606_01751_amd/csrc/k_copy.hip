@@ -3,6 +3,8 @@
 //
 // Every thread moves 16-byte vectors; consecutive threads cover consecutive 16-byte pieces of one
 // (block, head) row of the pool, so each wavefront touches whole 128-256 byte runs.
+#include <type_traits>
+
 #include "sx_device.h"
 #include "sx_internal.h"
 
@@ -178,31 +180,32 @@ struct LayerTable {
 // Re-alignment and KV write in one pass (Algorithm 1 steps 6 and 19-20 for sparse layers whose row
 // set R is known): every token's cache slot is written once -- the fresh K/V row if the token is
 // in R, else the re-aligned cached row if the token is reused; other tokens are not touched.
-// blockIdx.y selects the layer.  Work unit as in realign_kernel: VEC RoPE pairs of one head plus
-// 32 bytes of V; with d = 128 and 8 KV heads a wavefront is exactly one token, so the branch is
-// uniform.
+// blockIdx.y selects the layer.  Thread work unit: VEC RoPE pairs (two 16-byte K vectors) plus
+// the same 32 bytes of V, for HPT heads of one token; the unit's cos/sin values are loaded once
+// for its heads.  Threads are ordered unit fastest, then token, then head group, so for each head
+// a wavefront covers 64 / UPH consecutive tokens: consecutive slots of a (block, head) run of
+// the pool, i.e. contiguous runs of the source and destination caches.
 // Membership of a token in R: MASK = a caller's byte mask (nonzero = in R), else the plan's
-// generation marks (mark == gen).
-template <int D, bool BF16, bool NEOX, bool MASK>
+// generation marks (mark == gen).  The token's record (destination slot, source slot, cos/sin row)
+// and its membership are independent loads, so every row transfer waits for one load level.
+template <int D, bool BF16, bool NEOX, bool MASK, int HPT>
 __global__ __launch_bounds__(256) void realign_scatter_kernel(
-    const int32_t* __restrict__ tok_slot, const int32_t* __restrict__ tok_ra, const RealignRow* __restrict__ ra,
-    const float2* __restrict__ cs, const uint32_t* __restrict__ mark, const uint8_t* __restrict__ sel, uint32_t gen,
-    int64_t total, const LayerTable tab, int Hkv) {
+    const RealignRow* __restrict__ tok_row, const float2* __restrict__ cs, const uint32_t* __restrict__ mark,
+    const uint8_t* __restrict__ sel, uint32_t gen, int64_t total, const LayerTable tab, int Hkv) {
   constexpr int ESZ = BF16 ? 2 : 4;
   constexpr int VEC = 16 / ESZ;
   constexpr int UPH = D / (2 * VEC);
   const sx_layer_kv& lay = tab.l[blockIdx.y];
   char* kc = (char*)lay.k_cache;
   char* vc = (char*)lay.v_cache;
-  // 32-bit indexing: the host guarantees total * units < 2^31
-  const uint32_t units = (uint32_t)(Hkv * UPH);
+  // 32-bit indexing: the host guarantees total * UPH * (Hkv / HPT) < 2^31
   const uint32_t g = blockIdx.x * blockDim.x + threadIdx.x;
-  const uint32_t tok32 = g / units;
-  if (tok32 >= (uint32_t)total) return;
+  const uint32_t rest = g / UPH;
+  const int ui = (int)(g - rest * UPH);
+  const uint32_t tok32 = rest % (uint32_t)total;
+  const int h0 = (int)(rest / (uint32_t)total) * HPT;
+  if (h0 >= Hkv) return;
   const int64_t tok = tok32;
-  const int u = (int)(g - tok32 * units);
-  const int head = u / UPH;
-  const int ui = u - head * UPH;
   int64_t e0, e1;
   if constexpr (NEOX) {
     e0 = (int64_t)ui * VEC;
@@ -212,48 +215,61 @@ __global__ __launch_bounds__(256) void realign_scatter_kernel(
     e1 = e0 + VEC;
   }
   const int64_t v0 = (int64_t)ui * 2 * VEC;
-  const int64_t dof = pool_off(tok_slot[tok], head, Hkv, D) * ESZ;
-  if (MASK ? sel[tok] != 0 : mark[tok] == gen) {
-    // fresh row of a token in R (bit-exact copy)
-    const char* kn = (const char*)lay.k_new + (tok * Hkv + head) * D * ESZ;
-    const char* vn = (const char*)lay.v_new + (tok * Hkv + head) * D * ESZ;
-    *(uint4*)(kc + dof + e0 * ESZ) = *(const uint4*)(kn + e0 * ESZ);
-    *(uint4*)(kc + dof + e1 * ESZ) = *(const uint4*)(kn + e1 * ESZ);
-    *(uint4*)(vc + dof + v0 * ESZ) = *(const uint4*)(vn + v0 * ESZ);
-    *(uint4*)(vc + dof + (v0 + VEC) * ESZ) = *(const uint4*)(vn + (v0 + VEC) * ESZ);
+  const RealignRow rr = tok_row[tok];
+  const bool in_r = MASK ? sel[tok] != 0 : mark[tok] == gen;
+  if (in_r) {
+    // fresh rows of a token in R (bit-exact copies)
+#pragma unroll
+    for (int hh = 0; hh < HPT; ++hh) {
+      const int head = h0 + hh;
+      const int64_t dof = pool_off(rr.dst_slot, head, Hkv, D) * ESZ;
+      const char* kn = (const char*)lay.k_new + (tok * Hkv + head) * D * ESZ;
+      const char* vn = (const char*)lay.v_new + (tok * Hkv + head) * D * ESZ;
+      const uint4 ka = *(const uint4*)(kn + e0 * ESZ);
+      const uint4 kb = *(const uint4*)(kn + e1 * ESZ);
+      const uint4 va = *(const uint4*)(vn + v0 * ESZ);
+      const uint4 vb = *(const uint4*)(vn + (v0 + VEC) * ESZ);
+      *(uint4*)(kc + dof + e0 * ESZ) = ka;
+      *(uint4*)(kc + dof + e1 * ESZ) = kb;
+      *(uint4*)(vc + dof + v0 * ESZ) = va;
+      *(uint4*)(vc + dof + (v0 + VEC) * ESZ) = vb;
+    }
     return;
   }
-  const int32_t ri = tok_ra[tok];
-  if (ri < 0) return;   // uncached and not listed: left as it is
-  const RealignRow rr = ra[ri];
+  if (rr.src_slot < 0) return;   // uncached and not listed: left as it is
   const char* src_k = (const char*)lay.src_k;
   const char* src_v = (const char*)lay.src_v;
-  const int64_t so = pool_off(rr.src_slot, head, Hkv, D) * ESZ;
-  const uint4 ka = *(const uint4*)(src_k + so + e0 * ESZ);
-  const uint4 kb = *(const uint4*)(src_k + so + e1 * ESZ);
-  const uint4 va = *(const uint4*)(src_v + so + v0 * ESZ);
-  const uint4 vb = *(const uint4*)(src_v + so + (v0 + VEC) * ESZ);
   const float2* csr = cs + (int64_t)rr.cs_row * (D / 2) + (int64_t)ui * VEC;
   float2 c[VEC];
 #pragma unroll
   for (int e = 0; e < VEC; ++e) c[e] = csr[e];
-  float fa[VEC], fb[VEC], ya[VEC], yb[VEC];
-  unpack<BF16>(ka, fa);
-  unpack<BF16>(kb, fb);
-  if constexpr (NEOX) {
 #pragma unroll
-    for (int e = 0; e < VEC; ++e) rot(fa[e], fb[e], c[e].x, c[e].y, ya[e], yb[e]);
-  } else {
+  for (int hh = 0; hh < HPT; ++hh) {
+    const int head = h0 + hh;
+    const int64_t so = pool_off(rr.src_slot, head, Hkv, D) * ESZ;
+    const int64_t dof = pool_off(rr.dst_slot, head, Hkv, D) * ESZ;
+    const uint4 ka = *(const uint4*)(src_k + so + e0 * ESZ);
+    const uint4 kb = *(const uint4*)(src_k + so + e1 * ESZ);
+    const uint4 va = *(const uint4*)(src_v + so + v0 * ESZ);
+    const uint4 vb = *(const uint4*)(src_v + so + (v0 + VEC) * ESZ);
+    float fa[VEC], fb[VEC], ya[VEC], yb[VEC];
+    unpack<BF16>(ka, fa);
+    unpack<BF16>(kb, fb);
+    if constexpr (NEOX) {
 #pragma unroll
-    for (int e = 0; e < VEC / 2; ++e) {
-      rot(fa[2 * e], fa[2 * e + 1], c[e].x, c[e].y, ya[2 * e], ya[2 * e + 1]);
-      rot(fb[2 * e], fb[2 * e + 1], c[VEC / 2 + e].x, c[VEC / 2 + e].y, yb[2 * e], yb[2 * e + 1]);
+      for (int e = 0; e < VEC; ++e) rot(fa[e], fb[e], c[e].x, c[e].y, ya[e], yb[e]);
+    } else {
+#pragma unroll
+      for (int e = 0; e < VEC / 2; ++e) {
+        rot(fa[2 * e], fa[2 * e + 1], c[e].x, c[e].y, ya[2 * e], ya[2 * e + 1]);
+        rot(fb[2 * e], fb[2 * e + 1], c[VEC / 2 + e].x, c[VEC / 2 + e].y, yb[2 * e], yb[2 * e + 1]);
+      }
     }
+    *(uint4*)(kc + dof + e0 * ESZ) = pack<BF16>(ya);
+    *(uint4*)(kc + dof + e1 * ESZ) = pack<BF16>(yb);
+    *(uint4*)(vc + dof + v0 * ESZ) = va;
+    *(uint4*)(vc + dof + (v0 + VEC) * ESZ) = vb;
   }
-  *(uint4*)(kc + dof + e0 * ESZ) = pack<BF16>(ya);
-  *(uint4*)(kc + dof + e1 * ESZ) = pack<BF16>(yb);
-  *(uint4*)(vc + dof + v0 * ESZ) = va;
-  *(uint4*)(vc + dof + (v0 + VEC) * ESZ) = vb;
 }
 
 // scores[i] = sum over KV heads h (in order) of colsum[h][i], rounded once to float32.
@@ -305,23 +321,35 @@ hipError_t launch_scatter(const sx_plan* p, const void* k_new, const void* v_new
   return hipGetLastError();
 }
 
+// heads per thread of realign_scatter_kernel (measured at d = 128, 8 KV heads: 1, 2, 4, 8 heads
+// per thread ran 49.2, 48.4, 48.2, 48.5 us against 49.5 us for one head of one token)
+constexpr int kRsHeads = 4;
+
 template <int D, bool BF16, bool NEOX>
 hipError_t realign_scatter_dispatch(const sx_plan* p, int32_t n_layers, const sx_layer_kv* layers, uint32_t gen,
                                    const uint8_t* sel, hipStream_t s) {
   constexpr int VEC = BF16 ? 8 : 4;
-  const int units = p->desc.n_kv_heads * (D / (2 * VEC));
-  const int64_t threads = p->total * units;
+  // heads per thread: the largest of kRsHeads, 2, 1 that divides the KV head count
+  constexpr int HPT = kRsHeads;
+  const int hkv = p->desc.n_kv_heads;
+  const int hpt = hkv % HPT == 0 ? HPT : (hkv % 2 == 0 ? 2 : 1);
+  const int64_t threads = p->total * (D / (2 * VEC)) * (hkv / hpt);
   for (int32_t l0 = 0; l0 < n_layers; l0 += kLayersPerLaunch) {
     const int nl = n_layers - l0 < kLayersPerLaunch ? n_layers - l0 : kLayersPerLaunch;
     LayerTable tab{};
     for (int i = 0; i < nl; ++i) tab.l[i] = layers[l0 + i];
     const dim3 grid((unsigned)((threads + 255) / 256), (unsigned)nl);
-    if (sel)
-      hipLaunchKernelGGL((realign_scatter_kernel<D, BF16, NEOX, true>), grid, dim3(256), 0, s, p->d_tok_slot,
-                         p->d_tok_ra, p->d_ra, p->d_cs, p->d_rmark, sel, gen, p->total, tab, p->desc.n_kv_heads);
-    else
-      hipLaunchKernelGGL((realign_scatter_kernel<D, BF16, NEOX, false>), grid, dim3(256), 0, s, p->d_tok_slot,
-                         p->d_tok_ra, p->d_ra, p->d_cs, p->d_rmark, sel, gen, p->total, tab, p->desc.n_kv_heads);
+    auto go = [&](auto mask, auto hpt_c) {
+      hipLaunchKernelGGL((realign_scatter_kernel<D, BF16, NEOX, decltype(mask)::value, decltype(hpt_c)::value>), grid,
+                         dim3(256), 0, s, p->d_tok_row, p->d_cs, p->d_rmark, sel, gen, p->total, tab, hkv);
+    };
+    auto by_hpt = [&](auto mask) {
+      if (hpt == HPT) go(mask, std::integral_constant<int, HPT>{});
+      else if (hpt == 2) go(mask, std::integral_constant<int, 2>{});
+      else go(mask, std::integral_constant<int, 1>{});
+    };
+    if (sel) by_hpt(std::true_type{});
+    else by_hpt(std::false_type{});
     const hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
   }

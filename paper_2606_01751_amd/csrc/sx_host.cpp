@@ -97,7 +97,7 @@ sx_status dev_upload(sx_plan* p, T** ptr, const std::vector<T>& host) {
 void free_plan(sx_plan* p) {
   if (!p) return;
   void* bufs[] = {p->d_req, p->d_bt, p->d_ra, p->d_cs, p->d_probe, p->d_nr, p->d_n_nr, p->d_n_probe,
-                  p->d_flags, p->d_tok_slot, p->d_tok_ra, p->d_rmark, p->d_lse, p->d_colsum,
+                  p->d_flags, p->d_tok_row, p->d_rmark, p->d_lse, p->d_colsum,
                   p->d_qp, p->d_lse2p, p->d_tok_pos, p->d_theta};
   for (void* b : bufs)
     if (b) (void)hipFree(b);
@@ -199,7 +199,8 @@ sx_status sx_plan_create(const sx_layer_desc* desc, const sx_request* requests, 
   std::vector<int32_t> probe((size_t)total + sx::kProbePad, 0), nr((size_t)total, 0);
   std::vector<int32_t> n_nr(n_requests), n_probe(n_requests);
   std::vector<uint8_t> flags((size_t)total, 0);
-  std::vector<int32_t> tok_slot((size_t)total, 0), tok_ra((size_t)total, -1), tok_pos((size_t)total, 0);
+  std::vector<sx::RealignRow> tok_row((size_t)total, sx::RealignRow{-1, 0, 0, 0});
+  std::vector<int32_t> tok_pos((size_t)total, 0);
   std::vector<double> theta(d / 2);
   for (int i = 0; i < d / 2; ++i) theta[i] = std::pow(desc->rope_base, -2.0 * i / d);
   int64_t off = 0;
@@ -213,7 +214,7 @@ sx_status sx_plan_create(const sx_layer_desc* desc, const sx_request* requests, 
     h.bt_off = (int32_t)bt_all.size();
     const int nblk = (T + b - 1) / b;
     bt_all.insert(bt_all.end(), q.block_table, q.block_table + nblk);
-    for (int t = 0; t < T; ++t) tok_slot[off + t] = q.block_table[t / b] * b + (t % b);
+    for (int t = 0; t < T; ++t) tok_row[off + t].dst_slot = q.block_table[t / b] * b + (t % b);
     uint8_t* fl = flags.data() + off;
     const sx_segment* last = nullptr;
     for (int m = 0; m < q.n_segments; ++m) {
@@ -234,7 +235,7 @@ sx_status sx_plan_create(const sx_layer_desc* desc, const sx_request* requests, 
         row.dst_slot = q.block_table[tok / b] * b + (tok % b);
         row.cs_row = cs_rows;
         row.pad = 0;
-        tok_ra[off + tok] = (int32_t)ra.size();
+        tok_row[off + tok] = row;
         ra.push_back(row);
       }
       ++cs_rows;
@@ -295,8 +296,7 @@ sx_status sx_plan_create(const sx_layer_desc* desc, const sx_request* requests, 
   if (st == SX_OK) st = dev_upload(p, &p->d_n_nr, n_nr);
   if (st == SX_OK) st = dev_upload(p, &p->d_n_probe, n_probe);
   if (st == SX_OK) st = dev_upload(p, &p->d_flags, flags);
-  if (st == SX_OK) st = dev_upload(p, &p->d_tok_slot, tok_slot);
-  if (st == SX_OK) st = dev_upload(p, &p->d_tok_ra, tok_ra);
+  if (st == SX_OK) st = dev_upload(p, &p->d_tok_row, tok_row);
   if (st == SX_OK) st = dev_upload(p, &p->d_tok_pos, tok_pos);
   if (st == SX_OK) st = dev_upload(p, &p->d_theta, theta);
   if (st == SX_OK) st = dev_upload(p, &p->d_rmark, std::vector<uint32_t>((size_t)total, 0u));

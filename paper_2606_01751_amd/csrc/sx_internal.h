@@ -67,8 +67,9 @@ struct sx_plan {
   int32_t* d_n_nr = nullptr;      // [n_req]
   int32_t* d_n_probe = nullptr;   // [n_req]
   uint8_t* d_flags = nullptr;     // [sum T]
-  int32_t* d_tok_slot = nullptr;  // [sum T] destination slot (block * b + slot) of every token
-  int32_t* d_tok_ra = nullptr;    // [sum T] index of the token's re-alignment row, -1 if uncached
+  // [sum T] every token's slots in one record: dst_slot (block * b + slot), and for a reused token
+  // its source slot and cos/sin row (src_slot = -1 for an uncached token)
+  sx::RealignRow* d_tok_row = nullptr;
   uint32_t* d_rmark = nullptr;    // [sum T] row-set generation marks (sx_realign_scatter)
   mutable uint32_t rgen = 0;      // last generation used
   float* d_lse = nullptr;         // scratch [sum T][Hq]
