@@ -71,24 +71,27 @@ def parse():
     return ap.parse_args()
 
 
-# kernel symbol -> (entry point, source file holding it)
-# (attention template arguments: head dim, paged, P.V product)
+# kernel symbol -> (entry point, source file holding it, whether each dispatch is one call of the
+# entry point; the others run inside a call beside such a kernel)
+# (attention template arguments: head dim, paged, P.V product, folded exponent; a full layer that
+# writes the log-sum-exp runs the unfolded variant)
 KERNELS = {
-    "attn_mfma_kernel<128, true, true>": ("sx_sparse_attn", "k_attn.hip"),
-    "attn_mfma_kernel<128, false, true>": ("sx_full_attn", "k_attn.hip"),
+    "attn_mfma_kernel<128, true, true, true>": ("sx_sparse_attn", "k_attn.hip", True),
+    "attn_mfma_kernel<128, false, true, true>": ("sx_full_attn", "k_attn.hip", True),
+    "attn_mfma_kernel<128, false, true, false>": ("sx_full_attn", "k_attn.hip", True),
     # two-pass scoring only (layers without a preceding full layer)
-    "attn_mfma_kernel<128, true, false>": ("sx_sparseq_score", "k_attn.hip"),
-    "colsum_mfma_kernel<128>": ("sx_sparseq_score", "k_attn.hip"),   # query heads per KV head > 64 only
-    "colsum2_kernel<128>": ("sx_sparseq_score", "k_attn.hip"),
-    "probe_gather_kernel<128>": ("sx_sparseq_score", "k_attn.hip"),
-    "head_reduce_kernel": ("sx_sparseq_score", "k_copy.hip"),
-    "realign_kernel": ("sx_rope_realign", "k_copy.hip"),
-    "scatter_kernel": ("sx_kv_scatter", "k_copy.hip"),
-    "realign_scatter_kernel": ("sx_realign_scatter_masked", "k_copy.hip"),   # (also the row-list variants)
-    "mark_rows_kernel": ("sx_realign_scatter", "k_copy.hip"),   # (also sx_realign_scatter_layers)
-    "fill_u8_kernel": ("sx_rows_mask", "k_copy.hip"),
-    "mask_rows_kernel": ("sx_rows_mask", "k_copy.hip"),
-    "topk_kernel": ("sx_topk_select", "k_topk.hip"),
+    "attn_mfma_kernel<128, true, false, false>": ("sx_sparseq_score", "k_attn.hip", False),
+    "colsum_mfma_kernel<128>": ("sx_sparseq_score", "k_attn.hip", True),   # query heads per KV head > 64 only
+    "colsum2_kernel<128>": ("sx_sparseq_score", "k_attn.hip", True),
+    "probe_gather_kernel<128>": ("sx_sparseq_score", "k_attn.hip", False),
+    "head_reduce_kernel": ("sx_sparseq_score", "k_copy.hip", False),
+    "realign_kernel": ("sx_rope_realign", "k_copy.hip", True),
+    "scatter_kernel": ("sx_kv_scatter", "k_copy.hip", True),
+    "realign_scatter_kernel": ("sx_realign_scatter_masked", "k_copy.hip", True),   # (also the row-list variants)
+    "mark_rows_kernel": ("sx_realign_scatter", "k_copy.hip", False),   # (also sx_realign_scatter_layers)
+    "fill_u8_kernel": ("sx_rows_mask", "k_copy.hip", True),
+    "mask_rows_kernel": ("sx_rows_mask", "k_copy.hip", False),
+    "topk_kernel": ("sx_topk_select", "k_topk.hip", True),
 }
 
 
@@ -130,16 +133,21 @@ def load_traffic(workload):
     if not os.path.exists(path):
         return {}
     d = json.load(open(path))
-    out, stale = {}, set()
+    total, calls, stale = {}, {}, set()
     for sym, e in d.get("kernels", {}).items():
         if sym not in KERNELS:
             continue
-        entry = KERNELS[sym][0]
-        if e.get("source_sha256") != source_hash(KERNELS[sym][1]):
+        entry, src, is_call = KERNELS[sym]
+        if e.get("source_sha256") != source_hash(src):
             stale.add(entry)       # the kernel changed since its counters were taken
             continue
-        out[entry] = out.get(entry, 0.0) + e["bytes_per_dispatch"]
-    return {k: v for k, v in out.items() if k not in stale}
+        n = e.get("dispatches", 1)
+        total[entry] = total.get(entry, 0.0) + e["bytes_per_dispatch"] * n
+        if is_call:
+            calls[entry] = calls.get(entry, 0) + n
+    # bytes per call of the entry point: the dispatch-weighted mean over its variants, plus the
+    # kernels that run inside each call
+    return {k: v / calls[k] for k, v in total.items() if k not in stale and calls.get(k)}
 
 
 class Timers:
@@ -190,6 +198,7 @@ def main():
             f = float(np.mean(fetch.get(sym, [0.0])))
             wr = float(np.mean(write.get(sym, [0.0])))
             rec["kernels"][sym] = {"entry_point": KERNELS[sym][0], "source_sha256": source_hash(KERNELS[sym][1]),
+                                   "dispatches": max(len(fetch.get(sym, [])), len(write.get(sym, []))),
                                    "fetch_kib": f, "write_kib": wr,
                                    "bytes_per_dispatch": (f * kf + wr * kw) * 1024.0}
         out = os.path.join(ROOT, "profiles", f"traffic_{w.name}.json")
