@@ -73,14 +73,12 @@ def parse():
 
 # kernel symbol -> (entry point, source file holding it, whether each dispatch is one call of the
 # entry point; the others run inside a call beside such a kernel)
-# (attention template arguments: head dim, paged, P.V product, folded exponent; a full layer that
-# writes the log-sum-exp runs the unfolded variant)
+# (attention template arguments: head dim, paged, P.V product)
 KERNELS = {
-    "attn_mfma_kernel<128, true, true, true>": ("sx_sparse_attn", "k_attn.hip", True),
-    "attn_mfma_kernel<128, false, true, true>": ("sx_full_attn", "k_attn.hip", True),
-    "attn_mfma_kernel<128, false, true, false>": ("sx_full_attn", "k_attn.hip", True),
+    "attn_mfma_kernel<128, true, true>": ("sx_sparse_attn", "k_attn.hip", True),
+    "attn_mfma_kernel<128, false, true>": ("sx_full_attn", "k_attn.hip", True),
     # two-pass scoring only (layers without a preceding full layer)
-    "attn_mfma_kernel<128, true, false, false>": ("sx_sparseq_score", "k_attn.hip", False),
+    "attn_mfma_kernel<128, true, false>": ("sx_sparseq_score", "k_attn.hip", False),
     "colsum_mfma_kernel<128>": ("sx_sparseq_score", "k_attn.hip", True),   # query heads per KV head > 64 only
     "colsum2_kernel<128>": ("sx_sparseq_score", "k_attn.hip", True),
     "probe_gather_kernel<128>": ("sx_sparseq_score", "k_attn.hip", False),

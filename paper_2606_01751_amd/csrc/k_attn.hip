@@ -22,9 +22,6 @@
 //     heads the round-robin dispatch keeps all tiles of one head on one XCD (one L2).
 //   * Softmax in the log2 domain; the running max is raised only when a probability would reach
 //     2^64, so the O^T rescale is rare and there is no max reduction on the common path.
-//   * Without a log-sum-exp output (FOLD), Q is pre-scaled by scale*log2(e) in bf16 and the
-//     S^T product starts from -m (the accumulator's initial value), so the MFMAs produce the
-//     exponent itself: per score the vector ALU runs the exponential, the bf16 pack and the sum.
 #include <type_traits>
 
 #include "sx_device.h"
@@ -83,9 +80,8 @@ __device__ __forceinline__ void sched_pipelined() {
   SX_SG(kSgMfma, PRE);
 }
 
-template <int D, bool PAGED, bool PV, bool FOLD>
+template <int D, bool PAGED, bool PV>
 __global__ __launch_bounds__(512, 1) void attn_mfma_kernel(AttnK a) {
-  static_assert(!FOLD || PV, "the folded exponent serves the P.V kernels (no log-sum-exp output)");
   constexpr int NW = 8;                       // waves: two groups of 4
   constexpr int ROWB = D * 2;                 // bytes of one key row
   constexpr int NCH = ROWB / 16;              // 16-byte chunks per row
@@ -152,15 +148,6 @@ __global__ __launch_bounds__(512, 1) void attn_mfma_kernel(AttnK a) {
 #pragma unroll
     for (int s = 0; s < D / 16; ++s) {
       uint4 v = valid ? *(const uint4*)(qp + 16 * s) : make_uint4(0, 0, 0, 0);
-      if constexpr (FOLD) {
-        // c2 q rounded to bf16 (round to nearest even); logits then carry a relative error of
-        // at most 2^-9 per product term
-        uint32_t wv[4] = {v.x, v.y, v.z, v.w};
-#pragma unroll
-        for (int t = 0; t < 4; ++t)
-          wv[t] = pack_bf16x2(bf16_lo(wv[t]) * c2, bf16_hi(wv[t]) * c2);
-        v = make_uint4(wv[0], wv[1], wv[2], wv[3]);
-      }
       qb[s] = __builtin_bit_cast(bf16x8_t, v);
     }
   }
@@ -189,12 +176,6 @@ __global__ __launch_bounds__(512, 1) void attn_mfma_kernel(AttnK a) {
   // running max (log2 domain); columns without a row start at 0 so their (unused) sums stay finite
   float m_run = valid ? -INFINITY : 0.f;
   float l_run = 0.f;
-  // FOLD: S^T accumulates from -m_ref (m_ref = m_run once that is finite, 0 before), held as a
-  // 16-register MFMA C operand
-  float m_ref = 0.f;
-  f32x16_t cneg;
-#pragma unroll
-  for (int e = 0; e < 16; ++e) cneg[e] = 0.f;
 
   // ---- global -> LDS tile transfers (16 bytes per lane, all 8 waves share each tile).
   // Transfer q (1 KB) of a tile holds rows RPK*q .. RPK*q + RPK - 1, all inside one 16-key block;
@@ -304,12 +285,10 @@ __global__ __launch_bounds__(512, 1) void attn_mfma_kernel(AttnK a) {
   for (int s = 0; s < D / 16; ++s) k_off[s] = l32 * ROWB + (((2 * s + hg) ^ (l32 & (NCH - 1))) << 4);
   auto s_body = [&](uint32_t Kb) {
     asm volatile("" : "+s"(Kb));   // opaque: one add per k-slice, no strength-reduced variants
-    if constexpr (!FOLD) {
 #pragma unroll
-      for (int mt = 0; mt < 2; ++mt)
+    for (int mt = 0; mt < 2; ++mt)
 #pragma unroll
-        for (int e = 0; e < 16; ++e) sacc[mt][e] = 0.f;
-    }
+      for (int e = 0; e < 16; ++e) sacc[mt][e] = 0.f;
 #pragma unroll
     for (int s = 0; s < D / 16; ++s) {
       uint32_t kbase = Kb + (uint32_t)k_off[s];
@@ -317,7 +296,7 @@ __global__ __launch_bounds__(512, 1) void attn_mfma_kernel(AttnK a) {
 #pragma unroll
       for (int mt = 0; mt < 2; ++mt) {
         const bf16x8_t ka = *(const __attribute__((address_space(3))) bf16x8_t*)(uintptr_t)(kbase + (uint32_t)(mt * 32 * ROWB));
-        sacc[mt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka, qb[s], (FOLD && s == 0) ? cneg : sacc[mt], 0, 0, 0);
+        sacc[mt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka, qb[s], sacc[mt], 0, 0, 0);
       }
     }
   };
@@ -388,42 +367,12 @@ __global__ __launch_bounds__(512, 1) void attn_mfma_kernel(AttnK a) {
         emit(kk, x);
       }
     };
-    if constexpr (FOLD) {
-      // sacc = c2 s - m_ref: p = 2^sacc against the reference; the first tile of a column (m_run
-      // still -inf) and any overflow take the rescale path, which raises m_run and m_ref together
-      psum = 0.f;
-#pragma unroll
-      for (int kk = 0; kk < 4; ++kk) {
-        float x[8];
-#pragma unroll
-        for (int t = 0; t < 8; ++t) x[t] = __builtin_amdgcn_exp2f(sacc[kk >> 1][(kk & 1) * 8 + t]);
-        emit(kk, x);
-      }
-      if (__ballot(!(psum < 0x1p64f) || m_run == -INFINITY)) {
-        const float m_new = fmaxf(m_run, tile_max() + m_ref);
-        rescale(m_new == -INFINITY ? 1.f : __builtin_amdgcn_exp2f(m_run - m_new));
-        m_run = m_new;
-        const float shift = m_new == -INFINITY ? 0.f : m_ref - m_new;
-        psum = 0.f;
-#pragma unroll
-        for (int kk = 0; kk < 4; ++kk) {
-          float x[8];
-#pragma unroll
-          for (int t = 0; t < 8; ++t) x[t] = __builtin_amdgcn_exp2f(sacc[kk >> 1][(kk & 1) * 8 + t] + shift);
-          emit(kk, x);
-        }
-        if (m_new != -INFINITY) m_ref = m_new;
-#pragma unroll
-        for (int e = 0; e < 16; ++e) cneg[e] = -m_ref;
-      }
-    } else {
-      expo(-m_run);
-      if (__ballot(!(psum < 0x1p64f))) {
-        const float m_new = fmaxf(m_run, tile_max() * c2);          // c2 > 0
-        rescale(m_new == -INFINITY ? 1.f : __builtin_amdgcn_exp2f(m_run - m_new));
-        m_run = m_new;
-        expo(m_new == -INFINITY ? 0.f : -m_new);
-      }
+    expo(-m_run);
+    if (__ballot(!(psum < 0x1p64f))) {
+      const float m_new = fmaxf(m_run, tile_max() * c2);          // c2 > 0
+      rescale(m_new == -INFINITY ? 1.f : __builtin_amdgcn_exp2f(m_run - m_new));
+      m_run = m_new;
+      expo(m_new == -INFINITY ? 0.f : -m_new);
     }
     l_run += psum;
   };
@@ -1054,14 +1003,7 @@ hipError_t launch_mfma(const AttnLaunch& L, hipStream_t s) {
   a.n_req = L.n_req;
   const int64_t ntiles = (L.grid_rows + a.rpw - 1) / a.rpw;
   const dim3 grid((unsigned)(ntiles * L.Hkv * L.n_req));
-  if constexpr (PV) {
-    if (a.lse == nullptr)   // no log-sum-exp output: the folded exponent (pre-scaled Q)
-      hipLaunchKernelGGL((attn_mfma_kernel<D, PAGED, true, true>), grid, dim3(512), 0, s, a);
-    else
-      hipLaunchKernelGGL((attn_mfma_kernel<D, PAGED, true, false>), grid, dim3(512), 0, s, a);
-  } else {
-    hipLaunchKernelGGL((attn_mfma_kernel<D, PAGED, false, false>), grid, dim3(512), 0, s, a);
-  }
+  hipLaunchKernelGGL((attn_mfma_kernel<D, PAGED, PV>), grid, dim3(512), 0, s, a);
   return hipGetLastError();
 }
 
