@@ -253,6 +253,34 @@ def test_full_attention_matches_oracle(name, w, with_lse):
     check_full_attention(name, w, with_lse)
 
 
+def _tiny(dtype, d, Hq, Hkv, seed):
+    """Requests shorter than one key tile, down to a single token: uncached, cached (the tail
+    fallback), split around block and tile sizes (16, 17, 63, 65 tokens), one batch."""
+    specs = [[(1, False, 0, None)],
+             [(1, True, 5, None)],
+             [(7, True, 100, None)],
+             [(16, False, 0, None)],
+             [(10, True, 3, None), (7, False, 0, None)],
+             [(40, True, 0, 20), (23, False, 0, None)],
+             [(65, False, 0, None)],
+             [(64, True, 1000, None), (1, False, 0, None), (65, True, 7, None)]]
+    return W.custom_workload(specs, n_q_heads=Hq, n_kv_heads=Hkv, head_dim=d, dtype=dtype, rope_base=1e4,
+                             seed=seed, plant_per_segment=1, name=f"tiny-{dtype}-{d}")
+
+
+TINY = [("tiny-bf16-d128-g4", _tiny("bf16", 128, 8, 2, 11)), ("tiny-f32-d64-g3", _tiny("f32", 64, 6, 2, 12))]
+
+
+@pytest.mark.parametrize("name,w", TINY, ids=[c[0] for c in TINY])
+def test_tiny_requests_match_oracle(name, w):
+    """A batch of requests of 1 to 130 tokens: full attention (with and without the log-sum-exp)
+    and the whole selecting layer at two ratios, to the same bar as the other layouts."""
+    check_full_attention(name, w, True)
+    check_full_attention(name, w, False)
+    check_sparse_layer(name, w, 0.15)
+    check_sparse_layer(name, w, 0.5)
+
+
 PEAKY = [c for c in CASES if c[0] in ("ragged-bf16-gptj-d128-g7", "edges-bf16")]
 
 
