@@ -1,0 +1,64 @@
+"""Host logic of bench.py (no GPU): the per-call HBM traffic it reports beside the roofline, from
+recorded per-dispatch counter values."""
+import json
+import os
+import sys
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+sys.path.insert(0, ROOT)
+import bench  # noqa: E402
+
+
+def _setup(tmp_path, monkeypatch, kernels, sources=("k_attn.hip", "k_copy.hip")):
+    csrc = tmp_path / "paper_2606_01751_amd" / "csrc"
+    csrc.mkdir(parents=True)
+    for f in sources:
+        (csrc / f).write_text(f"// {f}\n")
+    (tmp_path / "profiles").mkdir()
+    monkeypatch.setattr(bench, "ROOT", str(tmp_path))
+    rec = {"workload": "w", "kernels": {}}
+    for sym, (n, nbytes, src_changed) in kernels.items():
+        src = bench.KERNELS[sym][1]
+        h = "stale" if src_changed else bench.source_hash(src)
+        rec["kernels"][sym] = {"entry_point": bench.KERNELS[sym][0], "source_sha256": h, "dispatches": n,
+                               "fetch_kib": 0.0, "write_kib": 0.0, "bytes_per_dispatch": nbytes}
+    (tmp_path / "profiles" / "traffic_w.json").write_text(json.dumps(rec))
+
+
+def test_kernels_inside_a_call_add_up(tmp_path, monkeypatch):
+    # the scoring call runs the probe gather, the column sums and the head sum: bytes per call are
+    # the sum of the three
+    _setup(tmp_path, monkeypatch, {"colsum2_kernel<128>": (3, 100.0, False),
+                                   "probe_gather_kernel<128>": (3, 20.0, False),
+                                   "head_reduce_kernel": (3, 5.0, False)})
+    assert bench.load_traffic("w") == pytest.approx({"sx_sparseq_score": 125.0})
+
+
+def test_variants_of_one_entry_point_are_weighted_by_dispatches(tmp_path, monkeypatch):
+    # two column-sum variants serve sx_sparseq_score (by GQA group size): one call with 400 bytes and
+    # three with 100 bytes average 175 bytes per call
+    _setup(tmp_path, monkeypatch, {"colsum_mfma_kernel<128>": (1, 400.0, False),
+                                   "colsum2_kernel<128>": (3, 100.0, False)})
+    assert bench.load_traffic("w") == pytest.approx({"sx_sparseq_score": 175.0})
+
+
+def test_entry_without_counted_calls_or_with_stale_source_is_dropped(tmp_path, monkeypatch):
+    # the row-mark kernel alone is not a call of sx_realign_scatter; a kernel whose source changed
+    # since its counters were taken makes its whole entry point unreported
+    _setup(tmp_path, monkeypatch, {"mark_rows_kernel": (2, 7.0, False),
+                                   "scatter_kernel": (4, 50.0, True),
+                                   "attn_mfma_kernel<128, true, true>": (28, 300.0, False)})
+    assert bench.load_traffic("w") == pytest.approx({"sx_sparse_attn": 300.0})
+
+
+def test_missing_file_reports_nothing(tmp_path, monkeypatch):
+    monkeypatch.setattr(bench, "ROOT", str(tmp_path))
+    assert bench.load_traffic("w") == {}
+
+
+def test_every_kernel_symbol_names_a_source_that_exists():
+    for sym, (entry, src, is_call) in bench.KERNELS.items():
+        assert entry.startswith("sx_"), sym
+        assert os.path.exists(os.path.join(ROOT, "paper_2606_01751_amd", "csrc", src)), sym
