@@ -134,3 +134,17 @@ def test_workload_plans_validate_on_host():
         with pytest.raises(sx.SxError) as e:
             sx.Plan(desc, w.requests, w.n_dst_blocks, w.n_src_blocks)
         assert e.value.status in (sx.SX_ENOMEM, sx.SX_EHIP), str(e.value)
+
+
+def test_missing_library_fails_loudly(monkeypatch, tmp_path):
+    # no fallback: without the built library every entry point raises instead of computing
+    monkeypatch.setattr(sx, "LIB_PATH", str(tmp_path / "libsx.so"))
+    monkeypatch.setattr(sx, "_lib", None)
+    with pytest.raises(RuntimeError, match="is missing"):
+        sx.lib()
+    with pytest.raises(RuntimeError, match="is missing"):
+        sx.Plan(_desc(), [_good()], 8, 8)
+    import paper_2606_01751_amd.cache as C
+    monkeypatch.setattr(C, "_ready", False)
+    with pytest.raises(RuntimeError, match="is missing"):
+        C.sha256(b"abc")
