@@ -62,3 +62,13 @@ def test_every_kernel_symbol_names_a_source_that_exists():
     for sym, (entry, src, is_call) in bench.KERNELS.items():
         assert entry.startswith("sx_"), sym
         assert os.path.exists(os.path.join(ROOT, "paper_2606_01751_amd", "csrc", src)), sym
+
+
+def test_more_than_one_gpu_is_refused_with_a_message():
+    # the step runs on one GPU; asking for more exits with status 2 and says so, before any GPU use
+    import subprocess
+    r = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--gpus", "2"], capture_output=True,
+                       text=True, timeout=120)
+    assert r.returncode == 2
+    assert "one GPU" in r.stderr
+    assert r.stdout == ""
