@@ -47,6 +47,12 @@ struct AttnK {
   int Hq, Hkv, G, rpw, n_req;
   float scale_log2;
   int lse_base2;
+  // log-sum-exp pass (paged, no P.V): each row tile's keys in nsplit pieces of whole 16-tile
+  // windows; with nsplit > 1 every piece writes its (max, sum) to lse_part[piece][probe row][Hq]
+  // (probe rows of all requests concatenated) and lse_merge_kernel forms the log-sum-exp
+  int nsplit;
+  float2* lse_part;
+  int64_t n_part_rows;
 };
 
 typedef short shortx4_t __attribute__((ext_vector_type(4)));
@@ -107,14 +113,19 @@ __global__ __launch_bounds__(512, 1) void attn_mfma_kernel(AttnK a) {
   const int kvh = (int)(blockIdx.x % (unsigned)a.Hkv);
   const int rest = (int)(blockIdx.x / (unsigned)a.Hkv);
   const int r = rest % a.n_req;
-  const int rank = rest / a.n_req;
+  // pieces of one row tile are adjacent in the grid (heaviest row tiles first)
+  const int qi = rest / a.n_req;
+  const int nsplit = (PAGED && !PV) ? a.nsplit : 1;
+  const int rank = qi / nsplit;
+  const int piece = qi - rank * nsplit;
 
-  int T, tok_off, bt_off = 0, nrows;
+  int T, tok_off, bt_off = 0, nrows, p_off = 0;
   if constexpr (PAGED) {
     const ReqDev rq = a.reqs[r];
     T = rq.T;
     tok_off = rq.tok_off;
     bt_off = rq.bt_off;
+    p_off = rq.p_off;
     nrows = a.n_rows[r];
   } else {
     tok_off = a.cu[r];
@@ -137,9 +148,21 @@ __global__ __launch_bounds__(512, 1) void attn_mfma_kernel(AttnK a) {
   const int wg_max = PAGED ? a.rows[tok_off + last] : last;
   const int wave_max = wave_max_i(pos);
   const int wave_min = wave_min_i(valid ? pos : 0x7fffffff);
-  const int nkt = wg_max / KT + 1;
   const int qh = kvh * a.G + hh;
   const float c2 = a.scale_log2;
+  // key tiles [kt0, kt0 + nkt) of this workgroup: all of them, or one piece of whole 16-tile windows
+  const int nkt_all = wg_max / KT + 1;
+  int kt0 = 0, nkt = nkt_all;
+  if (nsplit > 1) {
+    const int tpp = ((nkt_all + nsplit - 1) / nsplit + 15) & ~15;
+    kt0 = piece * tpp;
+    nkt = min(tpp, nkt_all - kt0);
+    if (nkt <= 0) {   // no keys in this piece: an empty partial (uniform over the workgroup)
+      if (valid && hg == 0)
+        a.lse_part[((int64_t)piece * a.n_part_rows + p_off + ridx) * a.Hq + qh] = make_float2(-INFINITY, 0.f);
+      return;
+    }
+  }
 
   // Q^T as the B operand: lane owns column l32, d-slots 16s + 8hg .. +7.
   bf16x8_t qb[D / 16];
@@ -157,12 +180,12 @@ __global__ __launch_bounds__(512, 1) void attn_mfma_kernel(AttnK a) {
   // access in the loop.  Windows c and c + 1 are held; window c + 2 is loaded 16 tiles before its
   // first use.
   const int nblk = (T + 15) >> 4;
-  int win_c = 0;
+  int win_c = kt0 >> 4;   // window c: blocks of key tiles 16 c .. 16 c + 15 (kt0 is a multiple of 16)
   int32_t win0 = 0, win1 = 0;
   auto load_win = [&](int c) -> int32_t { return a.bt[bt_off + min(64 * c + lane, nblk - 1)]; };
   if constexpr (PAGED) {
-    win0 = load_win(0);
-    win1 = load_win(1);
+    win0 = load_win(win_c);
+    win1 = load_win(win_c + 1);
   }
   // Q must be complete before any tile transfer is issued: the compiler does not see those
   // transfers, so a later wait of its own for Q would also wait for them.
@@ -441,25 +464,27 @@ __global__ __launch_bounds__(512, 1) void attn_mfma_kernel(AttnK a) {
   auto ncur = [&](int j) {   // transfers (and window loads) this wave issues in iteration j
     return (j + 2 < nkt ? IPW : 0) + (PV && j + 1 < nkt ? IPW : 0) + ((PAGED && ((j + 2) & 15) == 0) ? 1 : 0);
   };
-  issue(a.k, k_last, 0, ktile(0), false);
-  if (nkt > 1) issue(a.k, k_last, 1, ktile(1), false);
-  if constexpr (PV) issue(a.v, v_last, 0, vtile(0), true);
+  // (iteration j works on key tile kt0 + j; the LDS buffers rotate with j)
+  issue(a.k, k_last, kt0, ktile(0), false);
+  if (nkt > 1) issue(a.k, k_last, kt0 + 1, ktile(1), false);
+  if constexpr (PV) issue(a.v, v_last, kt0, vtile(0), true);
   wait_vm((nkt > 1 ? IPW : 0) + (PV ? IPW : 0));   // K(0) has landed
   __syncthreads();
   auto matrix_phase = [&](int j) {
     // the wave in its matrix phase issues first: its MFMAs are not held back by the other
     // wave's softmax on the same SIMD
     __builtin_amdgcn_s_setprio(2);
-    if (j >= 1 && (j - 1) * KT <= wave_max) pv_tile(vtile_lds(j - 1));
-    if (j < nkt && j * KT <= wave_max) s_tile(ktile_lds(j));
+    if (j >= 1 && (kt0 + j - 1) * KT <= wave_max) pv_tile(vtile_lds(j - 1));
+    if (j < nkt && (kt0 + j) * KT <= wave_max) s_tile(ktile_lds(j));
     __builtin_amdgcn_s_setprio(0);
   };
   auto transfer_phase = [&](int j) {   // this wave's share of K(j+2) and V(j+1)
-    if (j + 2 < nkt) issue(a.k, k_last, j + 2, ktile(j + 2), false);
+    if (j + 2 < nkt) issue(a.k, k_last, kt0 + j + 2, ktile(j + 2), false);
     if constexpr (PV) {
-      if (j + 1 < nkt) issue(a.v, v_last, j + 1, vtile(j + 1), true);
+      if (j + 1 < nkt) issue(a.v, v_last, kt0 + j + 1, vtile(j + 1), true);
     }
     if constexpr (PAGED) {
+      // (kt0 is a multiple of 16: local and absolute tile indices agree mod 16)
       if (((j + 2) & 15) == 0) {   // tiles j + 2 and j + 3 lie in windows win_c + 1, win_c + 2
         win0 = win1;
         win1 = load_win(win_c + 2);
@@ -468,7 +493,7 @@ __global__ __launch_bounds__(512, 1) void attn_mfma_kernel(AttnK a) {
     }
   };
   auto vector_phase = [&](int j) {   // softmax of tile j
-    if (j >= 0 && j < nkt && j * KT <= wave_max) softmax_tile(j * KT);
+    if (j >= 0 && j < nkt && (kt0 + j) * KT <= wave_max) softmax_tile((kt0 + j) * KT);
   };
   if (grp == 0) {
     for (int j = 0; j <= nkt; ++j) {
@@ -507,10 +532,41 @@ __global__ __launch_bounds__(512, 1) void attn_mfma_kernel(AttnK a) {
         }
     }
   }
-  if (a.lse && valid && hg == 0) {
+  if (nsplit > 1) {
+    if (valid && hg == 0)
+      a.lse_part[((int64_t)piece * a.n_part_rows + p_off + ridx) * a.Hq + qh] = make_float2(m_run, l_tot);
+  } else if (a.lse && valid && hg == 0) {
     const float lse2 = m_run + __log2f(l_tot);
     a.lse[(int64_t)(tok_off + ridx) * a.Hq + qh] = a.lse_base2 ? lse2 : lse2 * 0.69314718055994531f;
   }
+}
+
+// Log-sum-exp of the pieces of the split log-sum-exp pass, for one (probe row, query head) per
+// thread: lse2 = m + log2(sum_i l_i 2^(m_i - m)) over the pieces that saw a key (l_i > 0), with m
+// their largest running max, combined in piece order.  blockIdx.y = request.
+__global__ __launch_bounds__(256) void lse_merge_kernel(const ReqDev* __restrict__ reqs,
+                                                        const float2* __restrict__ part, int nsplit,
+                                                        int64_t n_part_rows, int Hq, float* __restrict__ lse,
+                                                        int lse_base2) {
+  const ReqDev rq = reqs[blockIdx.y];
+  const int64_t g = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const int64_t i = g / Hq;
+  if (i >= rq.n_probe) return;
+  const int h = (int)(g - i * Hq);
+  const float2* pp = part + ((int64_t)rq.p_off + i) * Hq + h;
+  const int64_t step = n_part_rows * Hq;
+  float m = -INFINITY;
+  for (int s = 0; s < nsplit; ++s) {
+    const float2 v = pp[s * step];
+    if (v.y > 0.f) m = fmaxf(m, v.x);
+  }
+  float l = 0.f;
+  for (int s = 0; s < nsplit; ++s) {
+    const float2 v = pp[s * step];
+    if (v.y > 0.f) l += v.y * __builtin_amdgcn_exp2f(v.x - m);
+  }
+  const float lse2 = m + __log2f(l);
+  lse[(int64_t)(rq.tok_off + i) * Hq + h] = lse_base2 ? lse2 : lse2 * 0.69314718055994531f;
 }
 
 // Sparse-Q column sums, key-stationary: a workgroup owns 256 keys of one KV head (8 waves x 32; a
@@ -1002,8 +1058,22 @@ hipError_t launch_mfma(const AttnLaunch& L, hipStream_t s) {
   a.lse_base2 = L.lse_base2;
   a.n_req = L.n_req;
   const int64_t ntiles = (L.grid_rows + a.rpw - 1) / a.rpw;
-  const dim3 grid((unsigned)(ntiles * L.Hkv * L.n_req));
+  // the log-sum-exp pass of the Sparse-Q probe rows has few row tiles: split each row tile's keys
+  // into up to kLseSplit pieces until the grid has about 1024 workgroups
+  int ns = 1;
+  if (PAGED && !PV && L.lse_part) {
+    while (ns < kLseSplit && ntiles * L.Hkv * L.n_req * ns < 1024) ns *= 2;
+  }
+  a.nsplit = ns;
+  a.lse_part = L.lse_part;
+  a.n_part_rows = L.n_part_rows;
+  const dim3 grid((unsigned)(ntiles * ns * L.Hkv * L.n_req));
   hipLaunchKernelGGL((attn_mfma_kernel<D, PAGED, PV>), grid, dim3(512), 0, s, a);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess || ns == 1) return e;
+  const dim3 mg((unsigned)((L.grid_rows * (int64_t)L.Hq + 255) / 256), (unsigned)L.n_req);
+  hipLaunchKernelGGL(lse_merge_kernel, mg, dim3(256), 0, s, L.reqs, L.lse_part, ns, L.n_part_rows, L.Hq, L.lse,
+                     L.lse_base2);
   return hipGetLastError();
 }
 

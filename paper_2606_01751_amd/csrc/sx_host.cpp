@@ -98,7 +98,7 @@ void free_plan(sx_plan* p) {
   if (!p) return;
   void* bufs[] = {p->d_req, p->d_bt, p->d_ra, p->d_cs, p->d_probe, p->d_nr, p->d_n_nr, p->d_n_probe,
                   p->d_flags, p->d_tok_row, p->d_rmark, p->d_lse, p->d_colsum,
-                  p->d_qp, p->d_lse2p, p->d_tok_pos, p->d_theta};
+                  p->d_qp, p->d_lse2p, p->d_lsep, p->d_tok_pos, p->d_theta};
   for (void* b : bufs)
     if (b) (void)hipFree(b);
   delete p;
@@ -310,6 +310,10 @@ sx_status sx_plan_create(const sx_layer_desc* desc, const sx_request* requests, 
     st = dev_alloc(p, &qp, rows * desc->n_q_heads * d);
     p->d_qp = qp;
     if (st == SX_OK) st = dev_alloc(p, &p->d_lse2p, rows * desc->n_q_heads);
+    // (max, sum) partials of the split log-sum-exp pass: every entry of a probe row is written by
+    // its pieces before the merge reads it
+    if (st == SX_OK && p->n_probe > 0)
+      st = dev_alloc(p, &p->d_lsep, (size_t)sx::kLseSplit * p->n_probe * desc->n_q_heads);
     if (st == SX_OK) {
       hipError_t e = hipMemset(p->d_qp, 0, rows * desc->n_q_heads * d * sizeof(uint16_t));
       if (e == hipSuccess) e = hipMemset(p->d_lse2p, 0, rows * desc->n_q_heads * sizeof(float));
@@ -577,6 +581,8 @@ sx_status sx_sparseq_score(const sx_plan* p, const void* q, const void* k_cache,
   a.bt = p->d_bt;
   a.rows = p->d_probe;
   a.n_rows = p->d_n_probe;
+  a.lse_part = p->d_lsep;
+  a.n_part_rows = p->n_probe;
   sx_status st = SX_OK;
   if (p->max_probe > 0) {
     st = check_launch(sx::launch_attn_paged(a, s), "sx_sparseq_score pass 1 launch");

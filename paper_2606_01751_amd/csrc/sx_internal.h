@@ -78,6 +78,7 @@ struct sx_plan {
   double* d_theta = nullptr;      // [d/2] RoPE frequencies base^(-2i/d), float64
   void* d_qp = nullptr;           // scratch [n_probe][Hq][d]: query rows of the probe rows (bf16 plans)
   float* d_lse2p = nullptr;       // scratch [Hkv][n_probe][Hq / Hkv]: their base-2 log-sum-exp
+  float2* d_lsep = nullptr;       // scratch [kLseSplit][n_probe][Hq]: partials of the split pass (bf16 plans)
 };
 
 namespace sx {
@@ -141,7 +142,12 @@ struct AttnLaunch {
   const int32_t* n_rows;
   // dense mode
   const int32_t* cu;
+  // paged log-sum-exp pass: scratch for the (max, sum) partials of a split pass,
+  // [kLseSplit][n_part_rows][Hq] (n_part_rows = probe rows of all requests); NULL: no split
+  float2* lse_part;
+  int64_t n_part_rows;
 };
+constexpr int kLseSplit = 4;   // most key pieces per row tile of the log-sum-exp pass
 hipError_t launch_attn_paged(const AttnLaunch& a, hipStream_t s);   // rows over a paged cache
 hipError_t launch_attn_dense(const AttnLaunch& a, hipStream_t s);   // all rows, dense K/V
 // column sums of the Sparse-Q probabilities; lse: base-2 sums indexed by probe (lse_tok = 0, the
