@@ -79,6 +79,7 @@ KERNELS = {
     "attn_mfma_kernel<128, false, true>": ("sx_full_attn", "k_attn.hip", True),
     # two-pass scoring only (layers without a preceding full layer)
     "attn_mfma_kernel<128, true, false>": ("sx_sparseq_score", "k_attn.hip", False),
+    "lse_merge_kernel": ("sx_sparseq_score", "k_attn.hip", False),
     "colsum_mfma_kernel<128>": ("sx_sparseq_score", "k_attn.hip", True),   # query heads per KV head > 64 only
     "colsum2_kernel<128>": ("sx_sparseq_score", "k_attn.hip", True),
     "probe_gather_kernel<128>": ("sx_sparseq_score", "k_attn.hip", False),
