@@ -77,7 +77,7 @@ enum { SX_ROPE_NEOX = 0, SX_ROPE_GPTJ = 1 };
 
 typedef struct sx_layer_desc {
   int32_t n_q_heads;      /* Hq >= 1 */
-  int32_t n_kv_heads;     /* Hkv >= 1, Hq % Hkv == 0 */
+  int32_t n_kv_heads;     /* Hkv >= 1, Hq % Hkv == 0, Hq / Hkv <= 64 */
   int32_t head_dim;       /* d: 64 or 128 */
   int32_t block_size;     /* b: 16 */
   int32_t dtype;          /* SX_F32 or SX_BF16 */
@@ -159,14 +159,19 @@ sx_status sx_plan_nonreused_rows(const sx_plan* plan, const int32_t** rows, cons
  * x1' = x1*c - x2*s, x2' = x2*c + x1*s with c, s the float32 roundings of cos/sin(delta*theta_i)
  * (angle in float64), each product and sum rounded once in float32, then stored in the cache
  * type (bfloat16: round to nearest even).  Slots of non-cached tokens are not touched.
- * src pools and caches must not overlap. */
+ * Source slots and destination slots must not overlap.  One pool may serve as both the source
+ * pool and the cache (src_k == k_cache, the layout the segment cache manager produces) as long as
+ * the segments' source blocks and the request's destination blocks are distinct blocks. */
 sx_status sx_rope_realign(const sx_plan* plan, const void* src_k, const void* src_v, void* k_cache,
                           void* v_cache, void* stream);
 
 /* Algorithm 1 steps 19-20: copies k_new/v_new row t of request r into the cache slot of t for
  * every listed row (bit-exact).  rows == NULL writes every token of every request (n_rows and
- * max_rows are then ignored).  Otherwise rows/n_rows use the row-list layout and max_rows must
- * be >= every n_rows[r] (sx_plan_budget gives it); rows beyond max_rows are not written. */
+ * max_rows are then ignored).  Otherwise rows/n_rows use the row-list layout and max_rows should
+ * be >= every n_rows[r] (sx_plan_budget gives it): only the first min(n_rows[r], max_rows) rows of
+ * each request are written, so an undersized bound drops the last rows of a list.  Every other
+ * entry point that takes rows/n_rows/max_rows processes the same first min(n_rows[r], max_rows)
+ * rows. */
 sx_status sx_kv_scatter(const sx_plan* plan, const void* k_new, const void* v_new, const int32_t* rows,
                         const int32_t* n_rows, int32_t max_rows, void* k_cache, void* v_cache,
                         void* stream);
@@ -250,7 +255,8 @@ sx_status sx_topk_select(const sx_plan* plan, const float* scores, double ratio,
  *   out[off_r + n, h] = sum_{j <= i} softmax_j(scale * q[off_r + i, h] . K[j]) V[j]
  * with K/V read from the paged cache of request r.  bfloat16 runs on matrix cores with float32
  * accumulation and bfloat16 probabilities; float32 runs on vector ALUs.  max_rows as in
- * sx_kv_scatter. */
+ * sx_kv_scatter: the rows n >= min(n_rows[r], max_rows) are neither computed nor written, so the
+ * attention covers exactly the rows whose K/V sx_kv_scatter writes for the same list. */
 sx_status sx_sparse_attn(const sx_plan* plan, const void* q, const int32_t* rows, const int32_t* n_rows,
                          int32_t max_rows, const void* k_cache, const void* v_cache, void* out,
                          void* stream);
@@ -269,8 +275,9 @@ sx_status sx_full_attn(const sx_layer_desc* desc, const void* q, const void* k, 
  * layer.  bfloat16 plans only (SX_EUNSUPPORTED otherwise); float32 arithmetic inside, bfloat16
  * results rounded to nearest even.
  *
- * Rows: for request r, rows[off_r + n] for n < n_rows[r] (the row-list layout of sx_topk_select;
- * max_rows >= every n_rows[r], at most the longest request).  An operand row is addressed
+ * Rows: for request r, rows[off_r + n] for n < min(n_rows[r], max_rows) (the row-list layout of
+ * sx_topk_select; max_rows is at most the longest request and should be >= every n_rows[r], as for
+ * sx_kv_scatter).  An operand row is addressed
  *   by slot  (`*_by_token` = 0): row off_r + n of a [sum T][...] array -- compact per request,
  *            the layout of sx_sparse_attn's output;
  *   by token (`*_by_token` = 1): row off_r + rows[off_r + n] -- the request's token rows, the

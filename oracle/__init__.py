@@ -44,7 +44,7 @@ __all__ = [
     "rope_rotate", "to_bf16", "store", "realign_request", "scatter_rows", "gather_tokens",
     "tail_fallback", "overflow_positions", "probe_positions", "budget", "topk_keys",
     "recompute_set", "sparseq_scores", "attention_rows", "full_attention", "softmax_scale",
-    "sparse_layer", "full_layer", "rmsnorm", "linear", "rope_at_positions", "silu_mul", "layer_body",
+    "sparse_layer", "rmsnorm", "linear", "rope_at_positions", "silu_mul", "layer_body",
 ]
 
 
@@ -412,22 +412,6 @@ def sparse_layer(w, tensors: dict, ratio: float, *, scores_from=None, R_from=Non
     res["k_pool"] = kp
     res["v_pool"] = vp
     return res
-
-
-def full_layer(w, tensors: dict, rows_sample=None) -> dict:
-    """A layer before the hybrid threshold: fresh K/V of every token are written to the cache
-    and every row runs plain causal attention on fresh Q/K/V (Algorithm 1 steps 7-10)."""
-    scale = softmax_scale(w.head_dim)
-    kp, vp = _empty_pool(w), _empty_pool(w)
-    offs = w.token_offsets
-    out = []
-    for r, req in enumerate(w.requests):
-        o0, o1 = offs[r], offs[r + 1]
-        q, k, v = tensors["q"][o0:o1], tensors["k"][o0:o1], tensors["v"][o0:o1]
-        scatter_rows(req, w, np.arange(req.n_tokens), k, v, kp, vp)
-        rows = None if rows_sample is None else rows_sample[r]
-        out.append(full_attention(q, k, v, scale, rows))
-    return {"out": out, "k_pool": kp, "v_pool": vp}
 
 
 # ---------------------------------------------------------------------------------------------

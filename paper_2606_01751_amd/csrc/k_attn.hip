@@ -45,6 +45,7 @@ struct AttnK {
   const int32_t* n_rows;
   const int32_t* cu;
   int Hq, Hkv, G, rpw, n_req;
+  int grid_rows;   // paged: rows of a request beyond this bound are not processed
   float scale_log2;
   int lse_base2;
   // log-sum-exp pass (paged, no P.V): each row tile's keys in nsplit pieces of whole 16-tile
@@ -126,7 +127,8 @@ __global__ __launch_bounds__(512, 1) void attn_mfma_kernel(AttnK a) {
     tok_off = rq.tok_off;
     bt_off = rq.bt_off;
     p_off = rq.p_off;
-    nrows = a.n_rows[r];
+    // the first min(n_rows, max_rows) rows: the rows the KV write of the same row list covers
+    nrows = min(a.n_rows[r], a.grid_rows);
   } else {
     tok_off = a.cu[r];
     T = a.cu[r + 1] - tok_off;
@@ -569,183 +571,7 @@ __global__ __launch_bounds__(256) void lse_merge_kernel(const ReqDev* __restrict
   lse[(int64_t)(rq.tok_off + i) * Hq + h] = lse_base2 ? lse2 : lse2 * 0.69314718055994531f;
 }
 
-// Sparse-Q column sums, key-stationary: a workgroup owns 256 keys of one KV head (8 waves x 32; a
-// wave holds K^T of its keys as the MFMA A operand) and streams the probe columns (probe row,
-// query head of the group) 32 at a time: S^T = K Q^T, p = 2^(scale*log2e*s - lse2) masked
-// causally, summed per key.  The Q rows of a chunk are loaded once per workgroup and staged in
-// LDS (double-buffered; loads issued two chunks ahead).  Per-lane partial sums are float32 over
-// 8 chunks and float64 beyond; the cross-lane sum at the end has a fixed order, so the result is
-// deterministic.
-struct ColsumK {
-  const uint16_t* q;
-  const uint16_t* k;
-  const float* lse;
-  const ReqDev* reqs;
-  const int32_t* bt;
-  const int32_t* probe;
-  double* colsum;
-  int64_t total;
-  int Hq, Hkv, G, n_req;
-  float scale_log2;
-  int lse_tok;   // 0: base-2 sums indexed by probe; 1: natural-log sums indexed by token
-};
-
 constexpr int CS_KEYS = 256;   // keys per column-sum workgroup (8 waves x 32)
-
-template <int D>
-__global__ __launch_bounds__(512, 1) void colsum_mfma_kernel(ColsumK a) {
-  constexpr int ROWB = D * 2;                 // bytes of one Q row
-  constexpr int NCH = ROWB / 16;              // 16-byte chunks per row
-  constexpr int CPI = 64 / NCH;               // columns per 1 KB load of one wave
-  constexpr int NLD = 32 / CPI;               // waves that load a 32-column chunk
-  __shared__ __attribute__((aligned(1024))) char qs[2][32 * ROWB];
-  const int tid = threadIdx.x;
-  const int lane = tid & 63;
-  const int w = tid >> 6;
-  const int l32 = lane & 31;
-  const int hg = lane >> 5;
-  // 1-D grid: KV head fastest, then request, then key tile from the first keys (most probe rows)
-  const int kvh = (int)(blockIdx.x % (unsigned)a.Hkv);
-  const int rest = (int)(blockIdx.x / (unsigned)a.Hkv);
-  const ReqDev rq = a.reqs[rest % a.n_req];
-  const int T = rq.T;
-  const int j0 = (rest / a.n_req) * CS_KEYS;
-  if (j0 >= T) return;
-  const int jw = j0 + w * 32;
-  // K rows of the wave's 32 keys as the A operand
-  bf16x8_t ka[D / 16];
-  {
-    const int key = jw + l32;
-    const uint16_t* kp = nullptr;
-    if (key < T) {
-      const int32_t blk = a.bt[rq.bt_off + (key >> 4)];
-      kp = a.k + (((int64_t)blk * a.Hkv + kvh) * 16 + (key & 15)) * D + hg * 8;
-    }
-#pragma unroll
-    for (int s = 0; s < D / 16; ++s) {
-      uint4 v = kp ? *(const uint4*)(kp + 16 * s) : make_uint4(0, 0, 0, 0);
-      ka[s] = __builtin_bit_cast(bf16x8_t, v);
-    }
-  }
-  // first probe row that can see the workgroup's first key
-  const int32_t* probe = a.probe + rq.tok_off;
-  const int np = rq.n_probe;
-  int lo = 0, hi = np;
-  while (lo < hi) {
-    const int mid = (lo + hi) >> 1;
-    if (probe[mid] < j0) lo = mid + 1; else hi = mid;
-  }
-  const int ncols = np * a.G;
-  const int c_start = lo * a.G;
-  const int nch = (ncols - c_start + 31) / 32;
-  // loading lanes (waves < NLD): column c_start + 32 k + CPI w + lane / NCH, chunk lane % NCH;
-  // the chunk is stored at (column, chunk ^ (column mod NCH)) so the B-operand reads are
-  // conflict-free
-  const bool loader = w < NLD;
-  const int lcol = CPI * w + lane / NCH;
-  const int lpc = lane % NCH;
-  auto ld_pos = [&](int k) -> int {
-    const int c = c_start + 32 * k + lcol;
-    return (loader && c < ncols) ? probe[c / a.G] : -1;
-  };
-  auto ld_q = [&](int k, int pos) -> uint4 {
-    const int c = c_start + 32 * k + lcol;
-    if (!loader || c >= ncols) return make_uint4(0, 0, 0, 0);
-    const int h = c % a.G;
-    const int lc = lpc ^ (lcol & (NCH - 1));   // logical chunk stored at this lane's slot
-    return *(const uint4*)(a.q + ((int64_t)(rq.tok_off + pos) * a.Hq + kvh * a.G + h) * D + lc * 8);
-  };
-  auto st_q = [&](int k, uint4 v) {
-    if (loader) *(uint4*)(qs[k & 1] + lcol * ROWB + lpc * 16) = v;
-  };
-  // computing lanes: column c_start + 32 k + l32 (position, denominator)
-  auto cm_pos = [&](int k) -> int {
-    const int c = c_start + 32 * k + l32;
-    return c < ncols ? probe[c / a.G] : -1;
-  };
-  auto cm_lse = [&](int k, int pos) -> float {
-    const int c = c_start + 32 * k + l32;
-    if (c >= ncols) return INFINITY;
-    const int pidx = c / a.G;
-    const int qh = kvh * a.G + (c - pidx * a.G);
-    return a.lse_tok ? a.lse[(int64_t)(rq.tok_off + pos) * a.Hq + qh] * 1.4426950408889634f
-                     : a.lse[(int64_t)(rq.tok_off + pidx) * a.Hq + qh];
-  };
-
-  double acc64[16];
-  float acc32[16];
-#pragma unroll
-  for (int e = 0; e < 16; ++e) {
-    acc64[e] = 0.0;
-    acc32[e] = 0.f;
-  }
-  int pending = 0;
-  // prologue: chunk 0 in LDS, chunk 1 in registers, positions of chunk 2 on the way
-  int pl1 = ld_pos(1);
-  uint4 q0 = ld_q(0, ld_pos(0));
-  uint4 q1 = ld_q(1, pl1);
-  int pl2 = ld_pos(2);
-  int pc0 = cm_pos(0);
-  float lc0 = cm_lse(0, pc0);
-  int pc1 = cm_pos(1);
-  st_q(0, q0);
-  __syncthreads();
-  for (int k = 0; k < nch; ++k) {
-    // chunk k+1 into the other buffer (last read in iteration k-1); loads for chunk k+2
-    st_q(k + 1, q1);
-    q1 = ld_q(k + 2, pl2);
-    pl2 = ld_pos(k + 3);
-    const float lc1 = cm_lse(k + 1, pc1);
-    const int pc2 = cm_pos(k + 2);
-    // S^T of chunk k
-    const char* qb = qs[k & 1];
-    f32x16_t s = {};
-#pragma unroll
-    for (int st = 0; st < D / 16; ++st) {
-      const int c = 2 * st + hg;
-      const bf16x8_t b = *(const bf16x8_t*)(qb + l32 * ROWB + ((c ^ (l32 & (NCH - 1))) << 4));
-      s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka[st], b, s, 0, 0, 0);
-    }
-    // the chunk's first column (lane 0's) has the smallest row; no mask when it sees all 32 keys
-    const int first_pos = __builtin_amdgcn_readfirstlane(pc0);
-    const bool need_mask = first_pos < jw + 31;
-#pragma unroll
-    for (int e = 0; e < 16; ++e) {
-      float p = __builtin_amdgcn_exp2f(s[e] * a.scale_log2 - lc0);
-      if (need_mask) {
-        const int key = jw + (e >> 2) * 8 + hg * 4 + (e & 3);
-        p = key <= pc0 ? p : 0.f;
-      }
-      acc32[e] += p;
-    }
-    if (++pending == 8) {
-#pragma unroll
-      for (int e = 0; e < 16; ++e) {
-        acc64[e] += (double)acc32[e];
-        acc32[e] = 0.f;
-      }
-      pending = 0;
-    }
-    pc0 = pc1;
-    lc0 = lc1;
-    pc1 = pc2;
-    __syncthreads();
-  }
-#pragma unroll
-  for (int e = 0; e < 16; ++e) acc64[e] += (double)acc32[e];
-  // sum over the 32 columns (lanes with the same hg), fixed butterfly order
-#pragma unroll
-  for (int e = 0; e < 16; ++e)
-#pragma unroll
-    for (int o = 1; o < 32; o <<= 1) acc64[e] += __shfl_xor(acc64[e], o, 64);
-  if (l32 == 0) {
-#pragma unroll
-    for (int e = 0; e < 16; ++e) {
-      const int key = jw + (e >> 2) * 8 + hg * 4 + (e & 3);
-      if (key < T) a.colsum[(int64_t)kvh * a.total + rq.tok_off + key] = acc64[e];
-    }
-  }
-}
 
 // Gather of the Sparse-Q probe columns for colsum2_kernel: the query rows of every probe row
 // (all heads) and the base-2 log-sum-exp of every (probe row, query head), in probe order, so
@@ -778,9 +604,10 @@ __global__ __launch_bounds__(256) void probe_gather_kernel(const uint16_t* __res
   }
 }
 
-// Sparse-Q column sums from the gathered probe columns.  Same key-stationary work split as
-// colsum_mfma_kernel (a workgroup = 256 keys of one KV head, a wave's 32 keys held as the MFMA A
-// operand), but the probe columns stream in chunks of RC probe rows x G heads (at most 64
+// Sparse-Q column sums from the gathered probe columns, key-stationary: a workgroup owns 256 keys
+// of one KV head (8 waves x 32, a wave's 32 keys held as the MFMA A operand) and computes
+// S^T = K Q^T, p = 2^(scale*log2e*s - lse2) masked causally, summed per key.  The probe columns
+// (probe row x query head of the group) stream in chunks of RC probe rows x G heads (at most 64
 // columns, two 32-column MFMA groups) that move global -> LDS directly: the query rows (16 bytes
 // per lane, XOR-swizzled 16-byte chunks), the chunk's 64 log-sum-exps and its RC probe positions
 // (4 bytes per lane), triple-buffered and issued two chunks ahead.  No global load in the loop
@@ -1057,6 +884,7 @@ hipError_t launch_mfma(const AttnLaunch& L, hipStream_t s) {
   a.scale_log2 = L.scale * 1.4426950408889634f;
   a.lse_base2 = L.lse_base2;
   a.n_req = L.n_req;
+  a.grid_rows = L.grid_rows;
   const int64_t ntiles = (L.grid_rows + a.rpw - 1) / a.rpw;
   // the log-sum-exp pass of the Sparse-Q probe rows has few row tiles: split each row tile's keys
   // into up to kLseSplit pieces until the grid has about 1024 workgroups
@@ -1081,8 +909,8 @@ hipError_t launch_mfma(const AttnLaunch& L, hipStream_t s) {
 
 // float32 variants (vector ALU), defined in k_attn_f32.hip
 hipError_t launch_attn_f32(const AttnLaunch& a, bool paged, hipStream_t s);
-hipError_t launch_colsum_f32(const sx_plan* p, const void* q, const void* kc, const float* lse, int lse_tok,
-                             hipStream_t s);
+hipError_t launch_colsum_f32(const sx_plan* p, double* colsum, const void* q, const void* kc, const float* lse,
+                             int lse_tok, hipStream_t s);
 
 hipError_t launch_attn_paged(const AttnLaunch& a, hipStream_t s) {
   if (a.dtype == SX_F32) return launch_attn_f32(a, true, s);
@@ -1098,70 +926,47 @@ hipError_t launch_attn_dense(const AttnLaunch& a, hipStream_t s) {
   return launch_mfma<64, false, true>(a, s);
 }
 
-hipError_t launch_colsum(const sx_plan* p, const void* q, const void* kc, const float* lse, int lse_tok,
-                         hipStream_t s) {
-  if (p->desc.dtype == SX_F32) return launch_colsum_f32(p, q, kc, lse, lse_tok, s);
-  const int G = p->desc.n_q_heads / p->desc.n_kv_heads;
-  if (G <= 64 && p->d_qp) {
-    // gather the probe columns, then the column sums from them
-    const int D = p->desc.head_dim;
-    const int64_t threads = (int64_t)p->max_probe * p->desc.n_q_heads * (D * 2 / 16);
-    if (threads > 0) {
-      const dim3 gg((unsigned)((threads + 255) / 256), (unsigned)p->n_req);
-      if (D == 128)
-        hipLaunchKernelGGL(probe_gather_kernel<128>, gg, dim3(256), 0, s, (const uint16_t*)q, lse, lse_tok, p->d_req,
-                           p->d_probe, p->desc.n_q_heads, p->desc.n_kv_heads, p->n_probe, (uint16_t*)p->d_qp,
-                           p->d_lse2p);
-      else
-        hipLaunchKernelGGL(probe_gather_kernel<64>, gg, dim3(256), 0, s, (const uint16_t*)q, lse, lse_tok, p->d_req,
-                           p->d_probe, p->desc.n_q_heads, p->desc.n_kv_heads, p->n_probe, (uint16_t*)p->d_qp,
-                           p->d_lse2p);
-      const hipError_t e = hipGetLastError();
-      if (e != hipSuccess) return e;
-    }
-    Colsum2K c{};
-    c.k = (const uint16_t*)kc;
-    c.qp = (const uint16_t*)p->d_qp;
-    c.lse2p = p->d_lse2p;
-    c.reqs = p->d_req;
-    c.bt = p->d_bt;
-    c.probe = p->d_probe;
-    c.colsum = p->d_colsum;
-    c.total = p->total;
-    c.n_probe_total = p->n_probe;
-    c.Hq = p->desc.n_q_heads;
-    c.Hkv = p->desc.n_kv_heads;
-    c.G = G;
-    c.RC = 64 / G;
-    c.n_req = p->n_req;
-    c.scale_log2 = p->scale * 1.4426950408889634f;
-    const dim3 grid((unsigned)(((p->max_T + CS_KEYS - 1) / CS_KEYS) * c.Hkv * p->n_req));
+hipError_t launch_colsum(const sx_plan* p, const ScoreScratch& sc, const void* q, const void* kc, const float* lse,
+                         int lse_tok, hipStream_t s) {
+  if (p->desc.dtype == SX_F32) return launch_colsum_f32(p, sc.colsum, q, kc, lse, lse_tok, s);
+  const int G = p->desc.n_q_heads / p->desc.n_kv_heads;   // <= 64 (checked on the host)
+  // gather the probe columns, then the column sums from them
+  const int D = p->desc.head_dim;
+  const int64_t threads = (int64_t)p->max_probe * p->desc.n_q_heads * (D * 2 / 16);
+  if (threads > 0) {
+    const dim3 gg((unsigned)((threads + 255) / 256), (unsigned)p->n_req);
     if (D == 128)
-      hipLaunchKernelGGL(colsum2_kernel<128>, grid, dim3(512), 0, s, c);
+      hipLaunchKernelGGL(probe_gather_kernel<128>, gg, dim3(256), 0, s, (const uint16_t*)q, lse, lse_tok, p->d_req,
+                         p->d_probe, p->desc.n_q_heads, p->desc.n_kv_heads, p->n_probe, (uint16_t*)sc.qp,
+                         sc.lse2p);
     else
-      hipLaunchKernelGGL(colsum2_kernel<64>, grid, dim3(512), 0, s, c);
-    return hipGetLastError();
+      hipLaunchKernelGGL(probe_gather_kernel<64>, gg, dim3(256), 0, s, (const uint16_t*)q, lse, lse_tok, p->d_req,
+                         p->d_probe, p->desc.n_q_heads, p->desc.n_kv_heads, p->n_probe, (uint16_t*)sc.qp,
+                         sc.lse2p);
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
   }
-  ColsumK a{};
-  a.q = (const uint16_t*)q;
-  a.k = (const uint16_t*)kc;
-  a.lse = lse;
-  a.lse_tok = lse_tok;
-  a.reqs = p->d_req;
-  a.bt = p->d_bt;
-  a.probe = p->d_probe;
-  a.colsum = p->d_colsum;
-  a.total = p->total;
-  a.Hq = p->desc.n_q_heads;
-  a.Hkv = p->desc.n_kv_heads;
-  a.G = a.Hq / a.Hkv;
-  a.scale_log2 = p->scale * 1.4426950408889634f;
-  a.n_req = p->n_req;
-  const dim3 grid((unsigned)(((p->max_T + CS_KEYS - 1) / CS_KEYS) * a.Hkv * p->n_req));
-  if (p->desc.head_dim == 128)
-    hipLaunchKernelGGL(colsum_mfma_kernel<128>, grid, dim3(512), 0, s, a);
+  Colsum2K c{};
+  c.k = (const uint16_t*)kc;
+  c.qp = (const uint16_t*)sc.qp;
+  c.lse2p = sc.lse2p;
+  c.reqs = p->d_req;
+  c.bt = p->d_bt;
+  c.probe = p->d_probe;
+  c.colsum = sc.colsum;
+  c.total = p->total;
+  c.n_probe_total = p->n_probe;
+  c.Hq = p->desc.n_q_heads;
+  c.Hkv = p->desc.n_kv_heads;
+  c.G = G;
+  c.RC = 64 / G;
+  c.n_req = p->n_req;
+  c.scale_log2 = p->scale * 1.4426950408889634f;
+  const dim3 grid((unsigned)(((p->max_T + CS_KEYS - 1) / CS_KEYS) * c.Hkv * p->n_req));
+  if (D == 128)
+    hipLaunchKernelGGL(colsum2_kernel<128>, grid, dim3(512), 0, s, c);
   else
-    hipLaunchKernelGGL(colsum_mfma_kernel<64>, grid, dim3(512), 0, s, a);
+    hipLaunchKernelGGL(colsum2_kernel<64>, grid, dim3(512), 0, s, c);
   return hipGetLastError();
 }
 

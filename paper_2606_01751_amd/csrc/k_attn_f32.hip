@@ -207,8 +207,8 @@ hipError_t launch_attn_f32(const AttnLaunch& L, bool paged, hipStream_t s) {
   return hipGetLastError();
 }
 
-hipError_t launch_colsum_f32(const sx_plan* p, const void* q, const void* kc, const float* lse, int lse_tok,
-                             hipStream_t s) {
+hipError_t launch_colsum_f32(const sx_plan* p, double* colsum, const void* q, const void* kc, const float* lse,
+                             int lse_tok, hipStream_t s) {
   ColsumF a{};
   a.q = (const float*)q;
   a.k = (const float*)kc;
@@ -217,7 +217,7 @@ hipError_t launch_colsum_f32(const sx_plan* p, const void* q, const void* kc, co
   a.reqs = p->d_req;
   a.bt = p->d_bt;
   a.probe = p->d_probe;
-  a.colsum = p->d_colsum;
+  a.colsum = colsum;
   a.total = p->total;
   a.Hq = p->desc.n_q_heads;
   a.Hkv = p->desc.n_kv_heads;

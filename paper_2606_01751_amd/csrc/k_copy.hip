@@ -115,10 +115,11 @@ __global__ __launch_bounds__(256) void realign_kernel(const RealignRow* __restri
   *(uint4*)(vc + dof + (v0 + VEC) * ESZ) = vb;
 }
 
-// Copies 16-byte pieces of fresh K and V rows into their cache slots.
+// Copies 16-byte pieces of fresh K and V rows into their cache slots: the first
+// min(n_rows, max_rows) listed rows of each request (rows == NULL: every token).
 __global__ __launch_bounds__(256) void scatter_kernel(const ReqDev* __restrict__ reqs, const int32_t* __restrict__ bt,
                                                       const int32_t* __restrict__ rows,
-                                                      const int32_t* __restrict__ n_rows,
+                                                      const int32_t* __restrict__ n_rows, int max_rows,
                                                       const uint4* __restrict__ k_new, const uint4* __restrict__ v_new,
                                                       uint4* __restrict__ kc, uint4* __restrict__ vc, int Hkv,
                                                       int upr /*16-byte units per token row*/, int uph /*per head*/) {
@@ -126,7 +127,7 @@ __global__ __launch_bounds__(256) void scatter_kernel(const ReqDev* __restrict__
   const int64_t g = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   const int64_t idx = g / upr;
   const int n = rows ? n_rows[blockIdx.y] : rq.T;
-  if (idx >= n) return;
+  if (idx >= n || idx >= max_rows) return;
   const int u = (int)(g - idx * upr);
   const int t = rows ? rows[rq.tok_off + idx] : (int)idx;
   const int head = u / uph;
@@ -316,7 +317,7 @@ hipError_t launch_scatter(const sx_plan* p, const void* k_new, const void* v_new
   const int upr = p->desc.n_kv_heads * uph;
   const int64_t threads = (int64_t)max_rows * upr;
   const dim3 grid((unsigned)((threads + 255) / 256), (unsigned)p->n_req);
-  hipLaunchKernelGGL(scatter_kernel, grid, dim3(256), 0, s, p->d_req, p->d_bt, rows, n_rows, (const uint4*)k_new,
+  hipLaunchKernelGGL(scatter_kernel, grid, dim3(256), 0, s, p->d_req, p->d_bt, rows, n_rows, max_rows, (const uint4*)k_new,
                      (const uint4*)v_new, (uint4*)kc, (uint4*)vc, p->desc.n_kv_heads, upr, uph);
   return hipGetLastError();
 }
@@ -400,10 +401,30 @@ hipError_t launch_realign_scatter(const sx_plan* p, int32_t n_layers, const sx_l
 #undef SX_RS
 }
 
-hipError_t launch_head_reduce(const sx_plan* p, float* scores, hipStream_t s) {
+hipError_t launch_head_reduce(const sx_plan* p, const double* colsum, float* scores, hipStream_t s) {
   const dim3 grid((unsigned)((p->total + 255) / 256));
-  hipLaunchKernelGGL(head_reduce_kernel, grid, dim3(256), 0, s, p->d_colsum, p->total, p->desc.n_kv_heads, scores);
+  hipLaunchKernelGGL(head_reduce_kernel, grid, dim3(256), 0, s, colsum, p->total, p->desc.n_kv_heads, scores);
   return hipGetLastError();
+}
+
+hipError_t launch_probe_pad_clear(const sx_plan* p, const ScoreScratch& sc, hipStream_t s) {
+  const int64_t G = p->desc.n_q_heads / p->desc.n_kv_heads;
+  // queries: the kProbePad rows after the last probe row, all heads (bf16 zero = 0)
+  const int64_t qrow = (int64_t)p->desc.n_q_heads * p->desc.head_dim * 2;   // bytes per probe row
+  const int64_t qwords = kProbePad * qrow / 4;
+  hipLaunchKernelGGL(fill_u32_kernel, dim3((unsigned)((qwords + 255) / 256)), dim3(256), 0, s,
+                     (uint32_t*)((char*)sc.qp + p->n_probe * qrow), qwords, 0u);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  // log-sum-exps: the kProbePad rows after the last probe row of every KV head
+  for (int h = 0; h < p->desc.n_kv_heads; ++h) {
+    float* base = sc.lse2p + ((int64_t)h * (p->n_probe + kProbePad) + p->n_probe) * G;
+    hipLaunchKernelGGL(fill_u32_kernel, dim3((unsigned)((kProbePad * G + 255) / 256)), dim3(256), 0, s,
+                       (uint32_t*)base, (int64_t)kProbePad * G, 0u);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  return hipSuccess;
 }
 
 }  // namespace sx

@@ -56,7 +56,7 @@ struct GemmRowsK {
   const uint16_t* res;
   uint16_t* y[kGemmMaxParts];   // output part p: columns pn[p] .. pn[p + 1] - 1, row stride pn[p + 1] - pn[p]
   int pn[kGemmMaxParts + 1];
-  int n_parts, K, N, n_req, m_tiles, x_tok, y_tok;
+  int n_parts, K, N, n_req, m_tiles, max_rows, x_tok, y_tok;
 };
 
 // physical chunk of logical chunk c in tile row `row` (CH chunks per row): 16 consecutive rows
@@ -106,7 +106,7 @@ __global__ __launch_bounds__(NW * 64, 1) void gemm_rows_kernel(GemmRowsK a) {
   const int r = mt_all / a.m_tiles;
   const int m0 = (mt_all - r * a.m_tiles) * GBM;
   const ReqDev rq = a.reqs[r];
-  const int nr = a.n_rows[r];
+  const int nr = min(a.n_rows[r], a.max_rows);
   if (m0 >= nr) return;
   const int n0 = nt * GBN;
   const int K = a.K;
@@ -303,14 +303,14 @@ __global__ __launch_bounds__(NW * 64, 1) void gemm_rows_kernel(GemmRowsK a) {
 // RMSNorm of listed rows: one wave per row, float32 sum of squares in a fixed order.
 // ---------------------------------------------------------------------------------------------
 __global__ __launch_bounds__(256) void rmsnorm_rows_kernel(const ReqDev* __restrict__ reqs, const int32_t* __restrict__ rows,
-                                                           const int32_t* __restrict__ n_rows,
+                                                           const int32_t* __restrict__ n_rows, int max_rows,
                                                            const uint16_t* __restrict__ x, int x_tok,
                                                            const uint16_t* __restrict__ gamma, float eps, int H,
                                                            uint16_t* __restrict__ y, int y_tok) {
   const ReqDev rq = reqs[blockIdx.y];
   const int n = blockIdx.x * 4 + (threadIdx.x >> 6);
   const int lane = threadIdx.x & 63;
-  if (n >= n_rows[blockIdx.y]) return;
+  if (n >= n_rows[blockIdx.y] || n >= max_rows) return;
   const uint16_t* xr = x + row_index(rq, rows, n, x_tok) * H;
   uint16_t* yr = y + row_index(rq, rows, n, y_tok) * H;
   float ss = 0.f;
@@ -347,7 +347,7 @@ __global__ __launch_bounds__(256) void rmsnorm_rows_kernel(const ReqDev* __restr
 // ---------------------------------------------------------------------------------------------
 template <int D, bool NEOX>
 __global__ __launch_bounds__(256) void rope_rows_kernel(const ReqDev* __restrict__ reqs, const int32_t* __restrict__ rows,
-                                                        const int32_t* __restrict__ n_rows,
+                                                        const int32_t* __restrict__ n_rows, int max_rows,
                                                         const int32_t* __restrict__ tok_pos,
                                                         const double* __restrict__ theta, uint16_t* __restrict__ q,
                                                         uint16_t* __restrict__ k, int Hq, int Hkv) {
@@ -356,7 +356,7 @@ __global__ __launch_bounds__(256) void rope_rows_kernel(const ReqDev* __restrict
   const int g = blockIdx.x * blockDim.x + threadIdx.x;
   const int n = g / UPR;
   const int u = g - n * UPR;
-  if (n >= n_rows[blockIdx.y]) return;
+  if (n >= n_rows[blockIdx.y] || n >= max_rows) return;
   const int64_t t = row_index(rq, rows, n, true);
   const double pos = (double)tok_pos[t];
   float c[8], s[8];
@@ -407,7 +407,7 @@ __global__ __launch_bounds__(256) void rope_rows_kernel(const ReqDev* __restrict
 // silu(g) = g / (1 + e^-g) in float32.
 // ---------------------------------------------------------------------------------------------
 __global__ __launch_bounds__(256) void silu_mul_rows_kernel(const ReqDev* __restrict__ reqs,
-                                                            const int32_t* __restrict__ n_rows,
+                                                            const int32_t* __restrict__ n_rows, int max_rows,
                                                             const uint16_t* __restrict__ gu, int f,
                                                             uint16_t* __restrict__ y) {
   const ReqDev rq = reqs[blockIdx.y];
@@ -415,7 +415,7 @@ __global__ __launch_bounds__(256) void silu_mul_rows_kernel(const ReqDev* __rest
   const int upr = f / 8;
   const int64_t n = g / upr;
   const int c = (int)(g - n * upr) * 8;
-  if (n >= n_rows[blockIdx.y]) return;
+  if (n >= n_rows[blockIdx.y] || n >= max_rows) return;
   const int64_t row = (int64_t)rq.tok_off + n;
   const uint4 gv = *(const uint4*)(gu + row * 2 * f + c);
   const uint4 uv = *(const uint4*)(gu + row * 2 * f + f + c);
@@ -454,6 +454,7 @@ hipError_t launch_gemm_rows(const sx_plan* p, const RowsArg& r, const void* x, i
   a.N = n;
   a.n_req = p->n_req;
   a.m_tiles = (r.max_rows + GBM - 1) / GBM;
+  a.max_rows = r.max_rows;
   constexpr int BK = SX_GEMM_BK, NST = SX_GEMM_NST, GM = SX_GEMM_GM, NW = SX_GEMM_NW, MF = SX_GEMM_MF;
   a.x_tok = x_tok;
   a.y_tok = y_tok;
@@ -466,7 +467,7 @@ hipError_t launch_gemm_rows(const sx_plan* p, const RowsArg& r, const void* x, i
 hipError_t launch_rmsnorm_rows(const sx_plan* p, const RowsArg& r, const void* x, int x_tok, const void* gamma,
                                float eps, int h, void* y, int y_tok, hipStream_t s) {
   const dim3 grid((unsigned)((r.max_rows + 3) / 4), (unsigned)p->n_req);
-  hipLaunchKernelGGL(rmsnorm_rows_kernel, grid, dim3(256), 0, s, p->d_req, r.rows, r.n_rows, (const uint16_t*)x, x_tok,
+  hipLaunchKernelGGL(rmsnorm_rows_kernel, grid, dim3(256), 0, s, p->d_req, r.rows, r.n_rows, r.max_rows, (const uint16_t*)x, x_tok,
                      (const uint16_t*)gamma, eps, h, (uint16_t*)y, y_tok);
   return hipGetLastError();
 }
@@ -478,7 +479,7 @@ hipError_t launch_rope_rows(const sx_plan* p, const RowsArg& r, void* q, void* k
   const bool neox = p->desc.rope_style == SX_ROPE_NEOX;
   const int Hq = p->desc.n_q_heads, Hkv = p->desc.n_kv_heads;
 #define SX_ROPE(D_, N_)                                                                                               \
-  hipLaunchKernelGGL((rope_rows_kernel<D_, N_>), grid, dim3(256), 0, s, p->d_req, r.rows, r.n_rows, p->d_tok_pos,   \
+  hipLaunchKernelGGL((rope_rows_kernel<D_, N_>), grid, dim3(256), 0, s, p->d_req, r.rows, r.n_rows, r.max_rows, p->d_tok_pos,   \
                      p->d_theta, (uint16_t*)q, (uint16_t*)k, Hq, Hkv)
   if (D == 128) {
     if (neox) SX_ROPE(128, true); else SX_ROPE(128, false);
@@ -492,7 +493,7 @@ hipError_t launch_rope_rows(const sx_plan* p, const RowsArg& r, void* q, void* k
 hipError_t launch_silu_mul_rows(const sx_plan* p, const RowsArg& r, const void* gu, int f, void* y, hipStream_t s) {
   const int64_t threads = (int64_t)r.max_rows * (f / 8);
   const dim3 grid((unsigned)((threads + 255) / 256), (unsigned)p->n_req);
-  hipLaunchKernelGGL(silu_mul_rows_kernel, grid, dim3(256), 0, s, p->d_req, r.n_rows, (const uint16_t*)gu, f,
+  hipLaunchKernelGGL(silu_mul_rows_kernel, grid, dim3(256), 0, s, p->d_req, r.n_rows, r.max_rows, (const uint16_t*)gu, f,
                      (uint16_t*)y);
   return hipGetLastError();
 }

@@ -52,7 +52,8 @@ sx_status validate_desc(const sx_layer_desc* d) {
   if (d->n_q_heads < 1 || d->n_kv_heads < 1) return fail(SX_ESHAPE, "head counts must be >= 1");
   if (d->n_q_heads % d->n_kv_heads != 0)
     return fail(SX_ESHAPE, "n_q_heads (%d) must be a multiple of n_kv_heads (%d)", d->n_q_heads, d->n_kv_heads);
-  if (d->n_q_heads / d->n_kv_heads > 128) return fail(SX_EUNSUPPORTED, "more than 128 query heads per KV head");
+  // the scoring kernel streams at most 64 query columns (probe row x head of the group) per step
+  if (d->n_q_heads / d->n_kv_heads > 64) return fail(SX_EUNSUPPORTED, "more than 64 query heads per KV head");
   if (d->head_dim != 64 && d->head_dim != 128)
     return fail(SX_EUNSUPPORTED, "head_dim %d unsupported (64 or 128)", d->head_dim);
   if (d->block_size != sx::kBlock) return fail(SX_EUNSUPPORTED, "block_size %d unsupported (16)", d->block_size);
@@ -65,6 +66,9 @@ sx_status validate_desc(const sx_layer_desc* d) {
   if (d->flags & ~SX_TOPK_ALL_POSITIONS) return fail(SX_EINVAL, "unknown flags 0x%x", (unsigned)d->flags);
   return SX_OK;
 }
+
+// largest thread count of a one-dimensional launch (gridDim.x * blockDim.x < 2^32, with margin)
+constexpr int64_t kMaxThreads = ((int64_t)1 << 32) - ((int64_t)1 << 16);
 
 float effective_scale(const sx_layer_desc* d) {
   return d->softmax_scale > 0.0f ? d->softmax_scale : (float)(1.0 / std::sqrt((double)d->head_dim));
@@ -103,6 +107,9 @@ void free_plan(sx_plan* p) {
     if (b) (void)hipFree(b);
   delete p;
 }
+
+// The scoring scratch a plan owns (allocated and padded in sx_plan_create).
+sx::ScoreScratch plan_scratch(const sx_plan* p) { return sx::ScoreScratch{p->d_colsum, p->d_qp, p->d_lse2p}; }
 
 // k_r = min(n, floor(ratio * n + 1/2)), each float64 operation rounded on its own.
 int64_t budget_of(int64_t n, double ratio) {
@@ -177,6 +184,13 @@ sx_status sx_plan_create(const sx_layer_desc* desc, const sx_request* requests, 
     }
     total += q.n_tokens;
     if (total > INT32_MAX) return fail(SX_EUNSUPPORTED, "more than 2^31 tokens in one plan");
+  }
+  {
+    // the element-wise kernels give each thread one 16-byte piece of a token row (queries have the
+    // most pieces), in one-dimensional grids of fewer than 2^32 threads
+    const int64_t pieces = total * desc->n_q_heads * d * (desc->dtype == SX_BF16 ? 2 : 4) / 16;
+    if (pieces >= kMaxThreads)
+      return fail(SX_EUNSUPPORTED, "%lld tokens x %d query heads exceed one launch", (long long)total, desc->n_q_heads);
   }
 
   sx_plan* p = new (std::nothrow) sx_plan();
@@ -546,6 +560,7 @@ sx_status sx_silu_mul_rows(const sx_plan* p, const int32_t* n_rows, int32_t max_
   if (st != SX_OK) return st;
   if (!gate_up || !y) return fail(SX_EINVAL, "NULL tensor argument");
   if (f <= 0 || f % 8 != 0) return fail(SX_EUNSUPPORTED, "feed-forward size %d must be a positive multiple of 8", f);
+  if ((int64_t)max_rows * (f / 8) >= kMaxThreads) return fail(SX_EUNSUPPORTED, "%d rows x %d exceed one launch", max_rows, f);
   if (max_rows == 0) return SX_OK;
   const sx::RowsArg r{nullptr, n_rows, max_rows};
   return check_launch(sx::launch_silu_mul_rows(p, r, gate_up, f, y, (hipStream_t)stream), "sx_silu_mul_rows launch");
@@ -558,9 +573,10 @@ sx_status sx_sparseq_score(const sx_plan* p, const void* q, const void* k_cache,
   hipStream_t s = (hipStream_t)stream;
   if (lse_in) {
     // one pass: the denominators come from the caller (natural log, indexed by token)
-    sx_status st = check_launch(sx::launch_colsum(p, q, k_cache, lse_in, 1, s), "sx_sparseq_score column-sum launch");
+    sx_status st = check_launch(sx::launch_colsum(p, plan_scratch(p), q, k_cache, lse_in, 1, s),
+                                "sx_sparseq_score column-sum launch");
     if (st != SX_OK) return st;
-    return check_launch(sx::launch_head_reduce(p, scores, s), "sx_sparseq_score head-sum launch");
+    return check_launch(sx::launch_head_reduce(p, p->d_colsum, scores, s), "sx_sparseq_score head-sum launch");
   }
   // pass 1: log-sum-exp of every (probe row, query head)
   sx::AttnLaunch a{};
@@ -589,10 +605,10 @@ sx_status sx_sparseq_score(const sx_plan* p, const void* q, const void* k_cache,
     if (st != SX_OK) return st;
   }
   // pass 2: per-key column sums of the probabilities, per KV head
-  st = check_launch(sx::launch_colsum(p, q, k_cache, p->d_lse, 0, s), "sx_sparseq_score pass 2 launch");
+  st = check_launch(sx::launch_colsum(p, plan_scratch(p), q, k_cache, p->d_lse, 0, s), "sx_sparseq_score pass 2 launch");
   if (st != SX_OK) return st;
   // pass 3: fixed-order sum over KV heads
-  return check_launch(sx::launch_head_reduce(p, scores, s), "sx_sparseq_score pass 3 launch");
+  return check_launch(sx::launch_head_reduce(p, p->d_colsum, scores, s), "sx_sparseq_score pass 3 launch");
 }
 
 sx_status sx_topk_select(const sx_plan* p, const float* scores, double ratio, int32_t* rows, int32_t* n_rows,

@@ -88,7 +88,17 @@ hipError_t launch_realign(const sx_plan* p, const void* src_k, const void* src_v
                           hipStream_t s);
 hipError_t launch_scatter(const sx_plan* p, const void* k_new, const void* v_new, const int32_t* rows,
                           const int32_t* n_rows, int32_t max_rows, void* kc, void* vc, hipStream_t s);
-hipError_t launch_head_reduce(const sx_plan* p, float* scores, hipStream_t s);
+// Scratch of the Sparse-Q column sums: per-KV-head float64 sums [Hkv][sum T]; (bf16 plans) the
+// gathered probe columns, queries [n_probe + kProbePad][Hq][d] and base-2 log-sum-exps
+// [Hkv][n_probe + kProbePad][Hq / Hkv], whose kProbePad padding rows must hold finite values.
+struct ScoreScratch {
+  double* colsum;
+  void* qp;
+  float* lse2p;
+};
+hipError_t launch_head_reduce(const sx_plan* p, const double* colsum, float* scores, hipStream_t s);
+// zeroes the padding rows of the gathered probe columns in `sc`
+hipError_t launch_probe_pad_clear(const sx_plan* p, const ScoreScratch& sc, hipStream_t s);
 // fused re-alignment + KV write of n_layers layers (host array of per-layer pointers): marks the
 // rows with `gen` (after clearing every mark when clear_marks), then writes every token's slot of
 // every layer once
@@ -152,7 +162,7 @@ hipError_t launch_attn_paged(const AttnLaunch& a, hipStream_t s);   // rows over
 hipError_t launch_attn_dense(const AttnLaunch& a, hipStream_t s);   // all rows, dense K/V
 // column sums of the Sparse-Q probabilities; lse: base-2 sums indexed by probe (lse_tok = 0, the
 // plan's pass-1 scratch) or natural-log sums indexed by token (lse_tok = 1, a caller's input)
-hipError_t launch_colsum(const sx_plan* p, const void* q, const void* kc, const float* lse, int lse_tok,
-                         hipStream_t s);
+hipError_t launch_colsum(const sx_plan* p, const ScoreScratch& sc, const void* q, const void* kc, const float* lse,
+                         int lse_tok, hipStream_t s);
 
 }  // namespace sx

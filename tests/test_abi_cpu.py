@@ -64,6 +64,9 @@ def _good():
 def test_plan_rejects_bad_descriptors():
     r = [_good()]
     assert _status(_desc(n_q_heads=6, n_kv_heads=4), r)[0] == sx.SX_ESHAPE
+    # more than 64 query heads per KV head: the scoring streams at most 64 columns per chunk
+    assert _status(_desc(n_q_heads=65, n_kv_heads=1), r)[0] == sx.SX_EUNSUPPORTED
+    assert _status(_desc(n_q_heads=256, n_kv_heads=2), r)[0] == sx.SX_EUNSUPPORTED
     assert _status(_desc(head_dim=96), r)[0] == sx.SX_EUNSUPPORTED
     assert _status(_desc(block_size=32), r)[0] == sx.SX_EUNSUPPORTED
     assert _status(_desc(dtype=7), r)[0] == sx.SX_EUNSUPPORTED

@@ -517,3 +517,84 @@ def test_one_pass_scores_from_full_attention_lse(name, w):
         rel12 = (np.abs(s1[sl] - s2[sl])[big] / s_o[big]).max()
         assert rel12 < 2e-5, rel12
     log(f"  one-pass score rel err {worst:.3g}")
+
+
+UNDERSIZED = [c for c in CASES if c[0] in ("ragged-f32-neox-d64", "ragged-bf16-gptj-d128-g7")]
+
+
+@pytest.mark.parametrize("name,w", UNDERSIZED, ids=[c[0] for c in UNDERSIZED])
+def test_undersized_max_rows_covers_the_same_rows(name, w):
+    """Every entry point that takes a row list handles the first min(n_rows[r], max_rows) rows of each
+    request: with an undersized (odd) bound, the KV write, the one-pass re-alignment + KV write, the byte
+    mask, the sparse attention and the layer-body product all cover exactly those rows and leave the
+    rest of their outputs untouched."""
+    log(f"[max_rows] {name}")
+    t = W.layer_tensors(w, 0)
+    g = GpuLayer(w, t)
+    rng = np.random.default_rng(23)
+    sets = [np.sort(rng.choice(r.n_tokens, size=max(1, (r.n_tokens * 2) // 5), replace=False)) for r in w.requests]
+    lens = sorted(len(s) for s in sets)
+    m = (lens[0] + lens[-1]) // 2 | 1
+    assert lens[0] <= m < lens[-1]
+    kept = [s[:m] for s in sets]
+    g.set_rows(sets)
+    offs = w.token_offsets
+    scale = O.softmax_scale(w.head_dim)
+    # KV write into a zeroed cache (zero keys and values keep the attention below well conditioned;
+    # a written row that should not have been shows as fresh values where the oracle has zeros)
+    g.k_cache.zero_()
+    g.v_cache.zero_()
+    sx.kv_scatter(g.plan, g.t["k"], g.t["v"], g.k_cache, g.v_cache, rows=g.rows, n_rows=g.n_rows, max_rows=m)
+    torch.cuda.synchronize()
+    kp = np.zeros(g.k_cache.shape, np.float32)
+    vp = np.zeros(g.v_cache.shape, np.float32)
+    for r, req in enumerate(w.requests):
+        O.scatter_rows(req, w, kept[r], t["k"][offs[r]:offs[r + 1]], t["v"][offs[r]:offs[r + 1]], kp, vp)
+    assert np.array_equal(host(g.k_cache), kp) and np.array_equal(host(g.v_cache), vp)
+    # sparse attention over that cache: rows n < min(n_r, m) computed, the others keep the canary
+    g.out.fill_(CANARY)
+    sx.sparse_attn(g.plan, g.t["q"], g.rows, g.n_rows, m, g.k_cache, g.v_cache, g.out)
+    torch.cuda.synchronize()
+    got = host(g.out)
+    for r, req in enumerate(w.requests):
+        o0 = offs[r]
+        n = len(kept[r])
+        ref = O.attention_rows(t["q"][o0:offs[r + 1]], O.gather_tokens(req, w, kp), O.gather_tokens(req, w, vp),
+                               kept[r], scale)
+        assert np.abs(got[o0:o0 + n] - ref).max() <= _tol_attn(w)
+        assert np.all(got[o0 + n:offs[r + 1]] == CANARY)
+    # byte mask
+    mask = torch.full((w.total_tokens,), 0x55, dtype=torch.uint8, device="cuda")
+    sx.rows_mask(g.plan, g.rows, g.n_rows, m, mask)
+    want = np.zeros(w.total_tokens, np.uint8)
+    for r in range(len(w.requests)):
+        want[offs[r] + kept[r]] = 1
+    assert np.array_equal(mask.cpu().numpy(), want)
+    # one-pass re-alignment + KV write with the row list
+    g.k_cache.fill_(CANARY)
+    g.v_cache.fill_(CANARY)
+    sx.realign_scatter(g.plan, g.t["k_src"], g.t["v_src"], g.t["k"], g.t["v"], g.rows, g.n_rows, m, g.k_cache,
+                       g.v_cache)
+    torch.cuda.synchronize()
+    kp, vp = oracle_pool(w), oracle_pool(w)
+    for r, req in enumerate(w.requests):
+        O.realign_request(req, w, t["k_src"], t["v_src"], kp, vp)
+        O.scatter_rows(req, w, kept[r], t["k"][offs[r]:offs[r + 1]], t["v"][offs[r]:offs[r + 1]], kp, vp)
+    tol = 1e-2 if w.dtype == "bf16" else 1e-5
+    assert np.abs(host(g.k_cache) - kp).max() <= tol and np.array_equal(host(g.v_cache), vp)
+    if w.dtype != "bf16":
+        return
+    # layer-body product by slot: y rows n < min(n_r, m) written, the others keep the canary
+    k_in, n_out = 128, 256
+    x = torch.from_numpy(W.round_bf16(rng.standard_normal((w.total_tokens, k_in)).astype(np.float32))).to("cuda")
+    wt = torch.from_numpy(W.round_bf16(rng.standard_normal((n_out, k_in)).astype(np.float32) * 0.1)).to("cuda")
+    x, wt = x.to(torch.bfloat16), wt.to(torch.bfloat16)
+    y = torch.full((w.total_tokens, n_out), CANARY, dtype=torch.bfloat16, device="cuda")
+    sx.gemm_rows(g.plan, g.rows, g.n_rows, m, x, wt, y)
+    torch.cuda.synchronize()
+    yh, xh, wh = host(y), host(x).astype(np.float64), host(wt).astype(np.float64)
+    for r in range(len(w.requests)):
+        o0, n = offs[r], len(kept[r])
+        ref = xh[o0:o0 + n] @ wh.T
+        assert np.abs(yh[o0:o0 + n] - ref).max() <= 2 ** -7 * np.abs(ref).max() + 1e-2
+        assert np.all(yh[o0 + n:offs[r + 1]] == CANARY)

@@ -44,7 +44,7 @@ def _bad_pairs(head_dim, style):
 
 _orig = {name: getattr(O, name) for name in ("budget", "overflow_positions", "tail_fallback", "topk_keys",
                                               "realign_request", "softmax_scale", "rmsnorm", "silu_mul",
-                                              "rope_at_positions", "linear", "attention_rows")}
+                                              "rope_at_positions", "linear", "attention_rows", "sparse_layer")}
 
 
 def _bad_budget(n, ratio):
@@ -118,6 +118,21 @@ def _bad_attention_head_map(q, k, v, rows, scale, chunk=256):
     return _orig["attention_rows"](q, k2, v2, rows, scale, chunk)
 
 
+def _bad_sparse_layer_scores_first(w, tensors, ratio, **kw):
+    # the Sparse-Q scores are taken before the fresh keys of I_nr are written, so the uncached rows
+    # score against whatever their cache slots held (Algorithm 1 steps 11-12 out of order)
+    kp = O._empty_pool(w)
+    vp = O._empty_pool(w)
+    offs = w.token_offsets
+    scores = []
+    for r, req in enumerate(w.requests):
+        O.realign_request(req, w, tensors["k_src"], tensors["v_src"], kp, vp)
+        q = tensors["q"][offs[r]:offs[r + 1]]
+        scores.append(O.sparseq_scores(q, O.gather_tokens(req, w, kp), O.probe_positions(req.n_tokens, req.segments),
+                                       O.softmax_scale(w.head_dim)))
+    return _orig["sparse_layer"](w, tensors, ratio, scores_from=scores, **kw)
+
+
 CASES = [
     ("rope sign", "rope_rotate", _bad_rope_rotate_sign,
      [(P.test_rope_closed_form_d4, ()), (P.test_rope_relative_property, ("neox",))]),
@@ -143,6 +158,8 @@ CASES = [
      [(P.test_rope_at_positions_absolute_and_relative, ("neox",))]),
     ("missing residual", "linear", _bad_linear_no_residual,
      [(P.test_linear_matches_loops_and_identity, ())]),
+    ("scores before the I_nr write", "sparse_layer", _bad_sparse_layer_scores_first,
+     [(P.test_selecting_layer_scores_fresh_nonreused_and_realigned_cached_keys, ())]),
 ]
 
 

@@ -461,6 +461,43 @@ def test_zero_deviation_sparse_equals_full(ratio):
     np.testing.assert_allclose(res["out"][0], full, rtol=1e-10, atol=1e-12)
 
 
+def test_selecting_layer_scores_fresh_nonreused_and_realigned_cached_keys():
+    # Section 3.2 with Algorithm 1 steps 6 and 11-12: in the selecting layer the Sparse-Q rows score
+    # against the current context -- their own fresh keys on I_nr and the cached keys moved to their
+    # new positions on I_reuse.  The key matrix is built here on its own: each cached token's source
+    # row (read from the pool by block id) rotated by its segment's shift with complex-number RoPE,
+    # each uncached token's fresh key.  Probes are the uncached tokens plus the whole final cached
+    # segment (30 tokens, shorter than the 64-token fallback).  Scores: scipy's softmax per probe row
+    # and head over the visible keys, summed.
+    from scipy.special import softmax
+    specs = [(40, True, 300, None), (24, False, 0, None), (56, True, 5, None), (17, False, 0, None),
+             (30, True, 900, None)]
+    base = 1e4
+    w = W.custom_workload([specs], n_q_heads=4, n_kv_heads=2, head_dim=16, dtype="f32", rope_base=base, seed=8)
+    t = W.layer_tensors(w, 0)
+    req = w.requests[0]
+    T, b, G = req.n_tokens, w.block_size, 2
+    keys = np.empty((T, 2, 16))
+    probes = []
+    for s in req.segments:
+        for j in range(s.length):
+            tok = s.seq_start + j
+            if s.cached:
+                blk = req.src_block_ids[s.src_block_start + j // b]
+                keys[tok] = _rope_complex(t["k_src"][blk, :, j % b, :], s.new_pos - s.old_pos, base, "neox")
+            else:
+                keys[tok] = t["k"][tok]
+                probes.append(tok)
+    probes += list(range(T - 30, T))
+    scale = 1.0 / math.sqrt(16)
+    want = np.zeros(T)
+    for i in probes:
+        for h in range(4):
+            want[: i + 1] += softmax(keys[: i + 1, h // G, :] @ t["q"][i, h].astype(np.float64) * scale)
+    got = O.sparse_layer(w, t, 0.3, skip_attention=True)["scores"][0]
+    np.testing.assert_allclose(got, want, rtol=1e-5, atol=1e-12)
+
+
 def test_scatter_is_exact_and_local():
     specs = [(40, True, 0, None), (25, False, 0, None), (30, True, 9, None)]
     w = W.custom_workload([specs], n_q_heads=2, n_kv_heads=1, head_dim=8)

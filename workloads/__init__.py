@@ -490,6 +490,54 @@ def layer_tensors(w: Workload, layer: int = 0, seed: int = 0) -> dict:
     return out
 
 
+def request_tensors(w: Workload, layer: int, r: int, seed: int = 0) -> dict:
+    """Host tensors of request r of one layer, drawn from the request's own streams (keyed by
+    (config, layer, 1 + r, tensor id, seed)), so that one request of a large batch can be checked on
+    the CPU without drawing the whole batch there.
+
+    q [T_r][Hq][d], k/v [T_r][Hkv][d]: the request's fresh rows.  src_blocks: the sorted source-pool
+    block ids its cached segments read; k_src/v_src [len(src_blocks)][Hkv][b][d] their contents
+    (planted rows of the request scaled by plant_scale).  Same distributions as layer_tensors;
+    float32, bf16-exact for bf16 workloads.  A device batch drawn by layer_tensors_torch takes
+    these values by overwriting the request's rows and blocks."""
+    req = w.requests[r]
+    T = req.n_tokens
+    Hq, Hkv, d, b = w.n_q_heads, w.n_kv_heads, w.head_dim, w.block_size
+    cid = w.config_id
+
+    def draw(tid, shape):
+        return _rng(cid, layer, 1 + r, tid, seed).standard_normal(size=shape, dtype=np.float32)
+
+    blocks = np.unique(np.asarray(req.src_block_ids, dtype=np.int64))
+    out = {
+        "q": draw(_Q, (T, Hq, d)),
+        "k": draw(_K, (T, Hkv, d)),
+        "v": draw(_V, (T, Hkv, d)),
+        "k_src": draw(_KSRC, (len(blocks), Hkv, b, d)),
+        "v_src": draw(_VSRC, (len(blocks), Hkv, b, d)),
+    }
+    where = {int(x): i for i, x in enumerate(blocks)}
+    for t in np.asarray(req.planted, dtype=np.int64):
+        seg = next(s for s in req.segments if s.seq_start <= t < s.seq_start + s.length)
+        j = int(t) - seg.seq_start
+        out["k_src"][where[int(req.src_block_ids[seg.src_block_start + j // b])], :, j % b, :] *= np.float32(w.plant_scale)
+    if w.dtype == "bf16":
+        out = {k: round_bf16(v) for k, v in out.items()}
+    out["src_blocks"] = blocks
+    return out
+
+
+def request_pools(w: Workload, r: int, rt: dict) -> tuple:
+    """Full-size source pools [n_src_blocks][Hkv][b][d] (zeros) holding request r's source blocks
+    from request_tensors, for the oracle's re-alignment of that request."""
+    shape = (w.n_src_blocks, w.n_kv_heads, w.block_size, w.head_dim)
+    ks = np.zeros(shape, np.float32)
+    vs = np.zeros(shape, np.float32)
+    ks[rt["src_blocks"]] = rt["k_src"]
+    vs[rt["src_blocks"]] = rt["v_src"]
+    return ks, vs
+
+
 def layer_tensors_torch(w: Workload, layer: int = 0, seed: int = 0, device="cuda", which=None) -> dict:
     """Device tensors of one layer, drawn with torch's generator (for sizes too big to draw on
     the host).  Same distributions and planting as layer_tensors, different random stream.
