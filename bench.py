@@ -48,6 +48,9 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-peaks", action="store_true", help="skip the copy / GEMM measurement of achievable peaks")
     ap.add_argument("--layers", type=int, default=None, help="override the number of layers (profiling)")
+    ap.add_argument("--buffer-sets", type=int, default=None,
+                    help="distinct per-layer input/cache buffer sets, layer l uses set l mod N (default: one per "
+                         "layer; the 400k-token batch rotates 3 sets, since 32 resident layers would not fit)")
     ap.add_argument("--score-passes", type=int, choices=(1, 2), default=1,
                     help="Sparse-Q scoring in hybrid stacks: 1 = denominators from the boundary layer's full "
                          "attention (exact-logit variant), 2 = own log-sum-exp pass")
@@ -226,14 +229,19 @@ def main():
     log(f"workload {w.name}: T={T} layers={L} (full {nfull}) ratio={ratio} k={k_total} max_rows={max_rows}")
 
     t0 = time.time()
-    layers = []
+    # per-layer buffers; with --buffer-sets N the layers rotate N sets (each far beyond the 256 MB
+    # Infinity Cache, so no layer finds the previous one's data there)
+    nsets = args.buffer_sets if args.buffer_sets else (3 if w.total_tokens > 200000 else L)
+    nsets = max(1, min(nsets, L))
+    sets = []
     pool = (w.n_dst_blocks, Hkv, w.block_size, d)
-    for l in range(L):
-        need = ("q", "k", "v") + (("k_src", "v_src") if l >= nfull else ())
+    for l in range(nsets):
+        need = ("q", "k", "v") + (("k_src", "v_src") if (l >= nfull or nsets < L) else ())
         tl = W.layer_tensors_torch(w, l, args.seed, which=need)
         tl["kc"] = torch.zeros(pool, dtype=dt, device="cuda")
         tl["vc"] = torch.zeros(pool, dtype=dt, device="cuda")
-        layers.append(tl)
+        sets.append(tl)
+    layers = [sets[l % nsets] for l in range(L)]
     out = torch.empty((T, Hq, d), dtype=dt, device="cuda")
     lse = torch.empty((T, Hq), dtype=torch.float32, device="cuda")   # boundary layer's denominators
     rmask = torch.zeros(T, dtype=torch.uint8, device="cuda")           # R as a byte mask
@@ -244,7 +252,8 @@ def main():
     max_T = max(r.n_tokens for r in w.requests)
     nr_rows, nr_n, nr_max = plan.nonreused_rows()
     torch.cuda.synchronize()
-    log(f"inputs resident in HBM ({torch.cuda.memory_allocated() / 2**30:.1f} GiB) in {time.time() - t0:.1f}s")
+    log(f"inputs resident in HBM ({torch.cuda.memory_allocated() / 2**30:.1f} GiB, {nsets} buffer sets for {L} "
+        f"layers) in {time.time() - t0:.1f}s")
 
     H, F, eps = Hq * d, args.ffn, 1e-5
     body = None
@@ -481,7 +490,7 @@ def main():
         "config": {"workload": f"{w.name}: {w.description}", "tokens": T, "layers": L, "full_layers": nfull,
                    "ratio": ratio, "recompute_rows": n_R, "k": int(k_total), "q_heads": Hq, "kv_heads": Hkv,
                    "head_dim": d, "requests": len(w.requests), "score_passes": args.score_passes,
-                   "kv_write": args.kv_write, "layer_body": bool(args.layer_body),
+                   "kv_write": args.kv_write, "layer_body": bool(args.layer_body), "buffer_sets": nsets,
                    **({"hidden": H, "ffn": F} if args.layer_body else {})},
         "kernels": kernels, "roofline": roof, "cpu_baseline": cpu,
         "layer_rates": layer_rates, "measured_peaks": peaks,
@@ -522,12 +531,34 @@ def measured_peaks(torch):
             "copy": "device copy of 2 GiB (read + write bytes)", "gemm": "torch.matmul 8192^3 bf16 (hipBLASLt)"}
 
 
-def cpu_baseline(w, layers, R, nfull, L, ratio, torch):
+def cpu_model() -> str:
+    """The host CPU's model name as lscpu reports it (or /proc/cpuinfo)."""
+    import subprocess
+    try:
+        out = subprocess.run(["lscpu"], capture_output=True, text=True, timeout=10).stdout
+        for line in out.splitlines():
+            if line.strip().startswith("Model name:"):
+                return line.split(":", 1)[1].strip()
+    except (OSError, subprocess.SubprocessError):
+        pass
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def cpu_baseline(w, layers, R, nfull, L, ratio, torch, n_sample=512):
     """The CPU oracle timed on a bounded sample of one step, scaled to the metric.
 
-    Timed on the host: one layer's full re-alignment, KV writes and top-k selection; the
-    attention and scoring rows of the oracle on samples of rows, scaled by the oracle's own cost
-    model (the matrix form costs the same per row; the per-row full attention costs i + 1)."""
+    Timed on the host for one layer of request 0: the full re-alignment of every reused token, the
+    KV writes of R and of every row, the selection (Eq. topk, overflow, tail) over the full score
+    vector; and, each on n_sample seeded rows, the sparse attention of rows of R, the Sparse-Q scores
+    of probe rows and full attention of rows (the oracle's matrix form).  The sampled parts are
+    scaled by the oracle's cost per row (a row's cost is proportional to the keys it sees), the
+    request-0 parts by the requests' token counts."""
     import threadpoolctl
 
     import oracle as O
@@ -536,62 +567,68 @@ def cpu_baseline(w, layers, R, nfull, L, ratio, torch):
     b = w.block_size
     scale = O.softmax_scale(w.head_dim)
     req = w.requests[0]
-    lay = layers[min(nfull, L - 1)]
-    h = {k: lay[k].float().cpu().numpy() for k in ("q", "k", "v", "k_src", "v_src") if k in lay}
-    threads = max(x.get("num_threads", 1) for x in threadpoolctl.threadpool_info()) if threadpoolctl.threadpool_info() else 1
     T = req.n_tokens
+    lay = layers[min(nfull, L - 1)]
+    o1 = int(w.token_offsets[1])
+    h = {k: lay[k][:o1].float().cpu().numpy() for k in ("q", "k", "v") if k in lay}
+    h.update({k: lay[k].float().cpu().numpy() for k in ("k_src", "v_src") if k in lay})
+    info = threadpoolctl.threadpool_info()
+    threads = max((x.get("num_threads", 1) for x in info), default=1)
+    tot_tokens = float(sum(r.n_tokens for r in w.requests))
+    share = T / tot_tokens
     kp = np.zeros((w.n_dst_blocks, w.n_kv_heads, b, w.head_dim), np.float32)
     vp = np.zeros_like(kp)
     t = {}
     s0 = time.perf_counter()
-    for r in w.requests:
-        O.realign_request(r, w, h["k_src"], h["v_src"], kp, vp)
-    t["realign"] = time.perf_counter() - s0
+    O.realign_request(req, w, h["k_src"], h["v_src"], kp, vp)
+    t["realign"] = (time.perf_counter() - s0) / share
     s0 = time.perf_counter()
     O.scatter_rows(req, w, R[0], h["k"], h["v"], kp, vp)
-    t["scatter_R"] = (time.perf_counter() - s0) * len(w.requests)
+    t["scatter_R"] = (time.perf_counter() - s0) * sum(len(x) for x in R) / max(1, len(R[0]))
     s0 = time.perf_counter()
     O.scatter_rows(req, w, np.arange(T), h["k"], h["v"], kp, vp)
-    t["scatter_all"] = (time.perf_counter() - s0) * len(w.requests)
+    t["scatter_all"] = (time.perf_counter() - s0) / share
     kt, vt = O.gather_tokens(req, w, kp), O.gather_tokens(req, w, vp)
-    ns = 32
-    samp = np.sort(rng.choice(len(R[0]), size=min(ns, len(R[0])), replace=False))
+
+    def per_key_cost(rows_all, rows_s):
+        # the sampled rows' share of the keys every listed row sees
+        return float(np.sum(rows_s + 1)) / float(np.sum(rows_all + 1))
+
+    R_all = [np.asarray(x, dtype=np.int64) for x in R]
+    samp = np.sort(rng.choice(R_all[0], size=min(n_sample, len(R_all[0])), replace=False))
     s0 = time.perf_counter()
-    O.attention_rows(h["q"][:T], kt, vt, R[0][samp], scale)
-    t["sparse_attn"] = (time.perf_counter() - s0) * sum(len(x) for x in R) / len(samp)
-    probes = np.flatnonzero(~req.cached_mask())
-    ps = np.sort(rng.choice(probes, size=min(ns, len(probes)), replace=False))
+    O.attention_rows(h["q"], kt, vt, samp, scale)
+    pairs_R = sum(float(np.sum(x + 1)) for x in R_all)
+    t["sparse_attn"] = (time.perf_counter() - s0) * pairs_R / float(np.sum(samp + 1))
+    probes_all = [O.probe_positions(r.n_tokens, r.segments) for r in w.requests]
+    ps = np.sort(rng.choice(probes_all[0], size=min(n_sample, len(probes_all[0])), replace=False))
     s0 = time.perf_counter()
-    sc = O.sparseq_scores(h["q"][:T], kt, ps, scale)
-    t["score"] = (time.perf_counter() - s0) * sum(int((~r.cached_mask()).sum()) for r in w.requests) / len(ps)
+    sc = O.sparseq_scores(h["q"], kt, ps, scale)
+    # the matrix form evaluates every probe row against all T keys of its request
+    t["score"] = (time.perf_counter() - s0) * sum(len(p) * r.n_tokens for p, r in zip(probes_all, w.requests)) / (
+        len(ps) * T)
+    full_sc = np.zeros(T)
+    full_sc[:] = sc
     s0 = time.perf_counter()
-    O.recompute_set(T, req.segments, sc, ratio, b)
-    t["topk"] = (time.perf_counter() - s0) * len(w.requests)
-    full_rows = np.sort(rng.choice(T, size=ns, replace=False))
+    O.recompute_set(T, req.segments, full_sc, ratio, b)
+    t["topk"] = (time.perf_counter() - s0) / share
+    full_rows = np.sort(rng.choice(T, size=min(n_sample, T), replace=False))
     s0 = time.perf_counter()
-    O.full_attention(h["q"][:T], h["k"][:T], h["v"][:T], scale, rows=full_rows)
-    frac = float(np.sum(full_rows + 1)) / (T * (T + 1) / 2)
-    t["full_attn"] = (time.perf_counter() - s0) / frac * sum(
-        r.n_tokens * (r.n_tokens + 1) / 2 for r in w.requests) / (T * (T + 1) / 2)
+    O.attention_rows(h["q"], h["k"], h["v"], full_rows, scale)
+    pairs_full = sum(r.n_tokens * (r.n_tokens + 1) / 2 for r in w.requests)
+    t["full_attn"] = (time.perf_counter() - s0) * pairs_full / float(np.sum(full_rows + 1))
     if nfull > 0:
         t_step = nfull * (t["scatter_all"] + t["full_attn"]) + t["score"] + t["topk"] + (L - nfull) * (
             t["realign"] + t["scatter_R"] + t["sparse_attn"])
     else:
         t_step = t["realign"] + 2 * t["scatter_R"] + t["score"] + t["topk"] + t["sparse_attn"]
     value = w.total_tokens * L / t_step
-    model = None
-    try:
-        for line in open("/proc/cpuinfo"):
-            if line.startswith("model name"):
-                model = line.split(":", 1)[1].strip()
-                break
-    except OSError:
-        pass
     return {"value": round(value, 2), "unit": "tokens/s", "cores": int(threads), "kind": "oracle",
-            "cpu_model": model, "host_cpus": os.cpu_count(),
-            "sample": (f"one layer of request 0: full re-alignment, KV writes and top-k; attention of {len(samp)} "
-                       f"rows of R, {len(ps)} Sparse-Q probe rows and {ns} full-attention rows, scaled to the "
-                       f"whole {L}-layer step by the oracle's cost per row"),
+            "cpu_model": cpu_model(), "host_cpus": os.cpu_count(),
+            "sample": (f"one layer of request 0: full re-alignment, KV writes of R and of every row, selection over "
+                       f"the full score vector; attention of {len(samp)} rows of R, Sparse-Q scores of {len(ps)} "
+                       f"probe rows and full attention of {len(full_rows)} rows; sampled parts scaled by the keys "
+                       f"each row sees, request-0 parts by token counts, to the whole {L}-layer step"),
             "seconds_estimated_per_step": round(t_step, 2),
             "step_seconds": {k: round(v, 4) for k, v in t.items()}}
 

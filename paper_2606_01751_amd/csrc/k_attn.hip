@@ -30,6 +30,9 @@
 namespace sx {
 namespace {
 
+#ifndef SX_ATTN_NBUF
+#define SX_ATTN_NBUF 3     // K/V tile buffers of the attention kernel (3 or 4; 4 measured no faster)
+#endif
 constexpr int KT = 64;     // keys per tile
 constexpr int COLS = 256;  // query columns per workgroup (8 waves x 32)
 
@@ -96,10 +99,12 @@ __global__ __launch_bounds__(512, 1) void attn_mfma_kernel(AttnK a) {
   constexpr int RPK = 1024 / ROWB;            // rows per 1 KB transfer instruction
   constexpr int IPW = TILEB / 1024 / NW;      // transfer instructions per wave per matrix
   static_assert(IPW * RPK == 8, "a wave moves 8 consecutive rows of every tile");
-  // LDS: three buffers each of K and V tiles (tile t in buffer t mod 3), rows row-major; chunk c of
-  // row r of K sits at chunk c ^ (r mod NCH) (conflict-free 16-byte row reads), of V at
-  // c ^ v_swz(r) (conflict-free transposed 8-byte reads).
-  constexpr int NBUF = 3;
+  // LDS: NBUF buffers each of K and V tiles (tile t in buffer t mod NBUF), rows row-major; chunk c
+  // of row r of K sits at chunk c ^ (r mod NCH) (conflict-free 16-byte row reads), of V at
+  // c ^ v_swz(r) (conflict-free transposed 8-byte reads).  A tile is issued NBUF - 1 (K) or
+  // NBUF - 2 (V) iterations before it is read.
+  constexpr int NBUF = SX_ATTN_NBUF;
+  static_assert(NBUF == 3 || NBUF == 4, "three or four tile buffers");
   __shared__ __attribute__((aligned(1024))) char smem[(PV ? 2 : 1) * NBUF * TILEB];
   char* const kbuf = smem;
   char* const vbuf = smem + (PV ? NBUF * TILEB : 0);
@@ -243,7 +248,14 @@ __global__ __launch_bounds__(512, 1) void attn_mfma_kernel(AttnK a) {
   };
   auto dma16_sb = [&](const uint16_t* sbase, uint32_t voffset, const char* dst) {
     const uint32_t m0 = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) const char*)dst;
-    asm volatile("s_mov_b32 m0, %2\n\tglobal_load_lds_dwordx4 %0, %1" ::"v"(voffset), "s"(sbase), "s"(m0)
+    // the base is wave-uniform; readfirstlane makes that visible where the compiler cannot prove it
+    // (the instruction takes its base from an SGPR pair)
+    // (the builtin returns a signed int: each half goes through uint32_t so that nothing is sign-extended)
+    const uint64_t sb = (uint64_t)(uintptr_t)sbase;
+    const uint32_t lo = (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)sb);
+    const uint32_t hi = (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)(sb >> 32));
+    const uint64_t sbu = ((uint64_t)hi << 32) | (uint64_t)lo;
+    asm volatile("s_mov_b32 m0, %2\n\tglobal_load_lds_dwordx4 %0, %1" ::"v"(voffset), "s"(sbu), "s"(m0)
                  : "m0", "memory");
   };
   // per-lane byte offsets of the transfers inside a (block, head) run; tiles start at multiples
@@ -281,6 +293,7 @@ __global__ __launch_bounds__(512, 1) void attn_mfma_kernel(AttnK a) {
   };
   auto ktile = [&](int t) { return kbuf + (t % NBUF) * TILEB; };
   auto vtile = [&](int t) { return vbuf + (t % NBUF) * TILEB; };
+  constexpr int KD = NBUF - 1, VD = NBUF - 2;   // issue distances of K and V tiles (iterations)
   // the same buffers as LDS byte addresses (wave-uniform: the operand reads add a lane offset)
   const uint32_t kbuf_lds = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) char*)kbuf;
   const uint32_t vbuf_lds = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) char*)vbuf;
@@ -294,10 +307,15 @@ __global__ __launch_bounds__(512, 1) void attn_mfma_kernel(AttnK a) {
       case 2: SX_WAIT_VMCNT(2); break;
       case 3: SX_WAIT_VMCNT(3); break;
       case 4: SX_WAIT_VMCNT(4); break;
-      default: SX_WAIT_VMCNT(5); break;
+      case 5: SX_WAIT_VMCNT(5); break;
+      case 6: SX_WAIT_VMCNT(6); break;
+      case 7: SX_WAIT_VMCNT(7); break;
+      case 8: SX_WAIT_VMCNT(8); break;
+      case 9: SX_WAIT_VMCNT(9); break;
+      default: SX_WAIT_VMCNT(10); break;
     }
   };
-  static_assert(2 * IPW + 1 <= 5, "transfer count per iteration exceeds the wait table");
+  static_assert((NBUF - 2) * (2 * IPW + 1) <= 10, "transfers in flight exceed the wait table");
 
   // ---- tile computations ----
   // S^T = K Q^T for the 64 keys of a tile (two 32-key M tiles)
@@ -459,18 +477,32 @@ __global__ __launch_bounds__(512, 1) void attn_mfma_kernel(AttnK a) {
   // tile j] in the first slot and the softmax of tile j in the second; group Y runs the softmax of
   // tile j-1 in the first slot and M(j) in the second.  So in every slot one wave of each SIMD
   // issues MFMAs while the other runs the softmax on the vector ALU.
-  // Tiles are triple-buffered: at the start of its softmax slot of iteration j each wave issues its
-  // share of the transfers of K(j+2) and V(j+1) (an issue that waits for the address unit then
-  // delays vector work, not MFMAs); they land during iteration j+1 (waited for at its end) and are
-  // read in iteration j+2, and their buffers were last read in iteration j-1. ----
+  // Tiles rotate through NBUF buffers: at the start of its softmax slot of iteration j each wave
+  // issues its share of the transfers of K(j+KD) and V(j+VD) (an issue that waits for the address
+  // unit then delays vector work, not MFMAs); they have NBUF - 2 iterations to land (waited for at
+  // the end of iteration j + NBUF - 3) before they are read, and their buffers were last read in
+  // iteration j-1. ----
   auto ncur = [&](int j) {   // transfers (and window loads) this wave issues in iteration j
-    return (j + 2 < nkt ? IPW : 0) + (PV && j + 1 < nkt ? IPW : 0) + ((PAGED && ((j + 2) & 15) == 0) ? 1 : 0);
+    return (j + KD >= 0 && j + KD < nkt ? IPW : 0) + (PV && j + VD >= 0 && j + VD < nkt ? IPW : 0) +
+           ((PAGED && j >= 0 && ((j + KD) & 15) == 0) ? 1 : 0);
   };
-  // (iteration j works on key tile kt0 + j; the LDS buffers rotate with j)
+  // transfers of iterations j - NBUF + 4 .. j may still be in flight at the end of iteration j
+  auto inflight = [&](int j) {
+    int n = ncur(j);
+    if constexpr (NBUF == 4) n += ncur(j - 1);
+    return n;
+  };
+  // (iteration j works on key tile kt0 + j; the LDS buffers rotate with j.)  Prologue: K(0), then
+  // the transfers that iterations -(NBUF-2) .. -1 would have issued.
   issue(a.k, k_last, kt0, ktile(0), false);
-  if (nkt > 1) issue(a.k, k_last, kt0 + 1, ktile(1), false);
-  if constexpr (PV) issue(a.v, v_last, kt0, vtile(0), true);
-  wait_vm((nkt > 1 ? IPW : 0) + (PV ? IPW : 0));   // K(0) has landed
+#pragma unroll
+  for (int jj = -(NBUF - 2); jj < 0; ++jj) {
+    if (jj + KD < nkt) issue(a.k, k_last, kt0 + jj + KD, ktile(jj + KD), false);
+    if constexpr (PV) {
+      if (jj + VD < nkt) issue(a.v, v_last, kt0 + jj + VD, vtile(jj + VD), true);
+    }
+  }
+  wait_vm(inflight(-1));   // K(0) has landed
   __syncthreads();
   auto matrix_phase = [&](int j) {
     // the wave in its matrix phase issues first: its MFMAs are not held back by the other
@@ -480,14 +512,15 @@ __global__ __launch_bounds__(512, 1) void attn_mfma_kernel(AttnK a) {
     if (j < nkt && (kt0 + j) * KT <= wave_max) s_tile(ktile_lds(j));
     __builtin_amdgcn_s_setprio(0);
   };
-  auto transfer_phase = [&](int j) {   // this wave's share of K(j+2) and V(j+1)
-    if (j + 2 < nkt) issue(a.k, k_last, kt0 + j + 2, ktile(j + 2), false);
+  auto transfer_phase = [&](int j) {   // this wave's share of K(j+KD) and V(j+VD)
+    if (j + KD < nkt) issue(a.k, k_last, kt0 + j + KD, ktile(j + KD), false);
     if constexpr (PV) {
-      if (j + 1 < nkt) issue(a.v, v_last, kt0 + j + 1, vtile(j + 1), true);
+      if (j + VD < nkt) issue(a.v, v_last, kt0 + j + VD, vtile(j + VD), true);
     }
     if constexpr (PAGED) {
-      // (kt0 is a multiple of 16: local and absolute tile indices agree mod 16)
-      if (((j + 2) & 15) == 0) {   // tiles j + 2 and j + 3 lie in windows win_c + 1, win_c + 2
+      // (kt0 is a multiple of 16: local and absolute tile indices agree mod 16.)  Tile j + KD opens
+      // window win_c + 1: the later iterations issue tiles of windows win_c + 1 and win_c + 2.
+      if (((j + KD) & 15) == 0) {
         win0 = win1;
         win1 = load_win(win_c + 2);
         ++win_c;
@@ -503,7 +536,7 @@ __global__ __launch_bounds__(512, 1) void attn_mfma_kernel(AttnK a) {
       __syncthreads();
       transfer_phase(j);
       vector_phase(j);
-      wait_vm(ncur(j));   // this wave's transfers of iteration j-1 have landed
+      wait_vm(inflight(j));   // this wave's transfers of iteration j - NBUF + 3 have landed
       __syncthreads();
     }
   } else {
@@ -512,7 +545,7 @@ __global__ __launch_bounds__(512, 1) void attn_mfma_kernel(AttnK a) {
       vector_phase(j - 1);
       __syncthreads();
       matrix_phase(j);
-      wait_vm(ncur(j));
+      wait_vm(inflight(j));
       __syncthreads();
     }
   }

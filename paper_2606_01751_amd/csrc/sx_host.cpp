@@ -102,7 +102,7 @@ void free_plan(sx_plan* p) {
   if (!p) return;
   void* bufs[] = {p->d_req, p->d_bt, p->d_ra, p->d_cs, p->d_probe, p->d_nr, p->d_n_nr, p->d_n_probe,
                   p->d_flags, p->d_tok_row, p->d_rmark, p->d_lse, p->d_colsum,
-                  p->d_qp, p->d_lse2p, p->d_lsep, p->d_tok_pos, p->d_theta};
+                  p->d_qp, p->d_lse2p, p->d_lsep, p->d_tok_pos, p->d_theta, p->d_topk};
   for (void* b : bufs)
     if (b) (void)hipFree(b);
   delete p;
@@ -316,6 +316,29 @@ sx_status sx_plan_create(const sx_layer_desc* desc, const sx_request* requests, 
   if (st == SX_OK) st = dev_upload(p, &p->d_rmark, std::vector<uint32_t>((size_t)total, 0u));
   if (st == SX_OK) st = dev_alloc(p, &p->d_lse, (size_t)total * desc->n_q_heads);
   if (st == SX_OK) st = dev_alloc(p, &p->d_colsum, (size_t)total * desc->n_kv_heads);
+  if (st == SX_OK) {
+    // selection scratch, zeroed once: every call leaves the histograms and counters at zero
+    const int64_t chunks = (p->max_T + sx::kTopkChunk - 1) / sx::kTopkChunk;
+    const size_t words = (size_t)n_requests * (sx::kTopkBins + 1 + 4 + 5 * chunks);
+    st = dev_alloc(p, &p->d_topk, words);
+    if (st == SX_OK) {
+      hipError_t e = hipMemset(p->d_topk, 0, words * sizeof(uint32_t));
+      if (e != hipSuccess) st = hip_fail(e, "hipMemset (selection scratch)");
+    }
+    if (st == SX_OK) {
+      uint32_t* w = p->d_topk;
+      p->topk.hist = w;
+      w += (size_t)n_requests * sx::kTopkBins;
+      p->topk.ctr = w;
+      w += n_requests;
+      p->topk.state = w;
+      w += (size_t)n_requests * 4;
+      p->topk.cnt = (int32_t*)w;
+      w += (size_t)n_requests * 3 * chunks;
+      p->topk.pre = (int32_t*)w;
+      p->topk.max_chunks = (int32_t)chunks;
+    }
+  }
   if (st == SX_OK && desc->dtype == SX_BF16) {
     // gathered probe columns, kProbePad zeroed rows past the last probe row (per KV head for the
     // log-sum-exps) so that a chunk read past the end stays in bounds and finite

@@ -35,6 +35,21 @@ struct RealignRow {
   int32_t pad;
 };
 
+// Selection scratch (plan-owned, zeroed when the plan is made; every pass leaves it clean): per
+// request a radix histogram [kTopkBins] and an arrival counter, the selection state (digits found,
+// digit mask, ties still needed) [4], and per chunk of kTopkChunk tokens the counts (sure rows,
+// ties, ties that are not sure rows) [3] and the output offset and tie rank [2].
+constexpr int kTopkChunk = 2048;
+constexpr int kTopkBins = 2048;
+struct TopkScratch {
+  uint32_t* hist;    // [n_req][kTopkBins]
+  uint32_t* ctr;     // [n_req]
+  uint32_t* state;   // [n_req][4]
+  int32_t* cnt;      // [n_req][max_chunks][3]
+  int32_t* pre;      // [n_req][max_chunks][2]
+  int32_t max_chunks;
+};
+
 // Token flags used by the selection kernel.
 enum : uint8_t { kFlagCandidate = 1, kFlagBase = 2 };
 
@@ -79,6 +94,8 @@ struct sx_plan {
   void* d_qp = nullptr;           // scratch [n_probe][Hq][d]: query rows of the probe rows (bf16 plans)
   float* d_lse2p = nullptr;       // scratch [Hkv][n_probe][Hq / Hkv]: their base-2 log-sum-exp
   float2* d_lsep = nullptr;       // scratch [kLseSplit][n_probe][Hq]: partials of the split pass (bf16 plans)
+  uint32_t* d_topk = nullptr;     // selection scratch, carved into `topk`
+  sx::TopkScratch topk{};
 };
 
 namespace sx {
