@@ -243,6 +243,19 @@ sx_status sx_realign_scatter_masked(const sx_plan* plan, const void* src_k, cons
 sx_status sx_sparseq_score(const sx_plan* plan, const void* q, const void* k_cache, const float* lse_in,
                            float* scores, void* stream);
 
+/* sx_sparseq_score in one-pass mode (lse_in required) that allocates nothing and uses no plan scratch:
+ * for callers that cannot allocate device memory or should not touch the plan's scratch -- code under
+ * HIP graph capture, tight serving loops, harnesses that forbid hipMalloc.  Same kernels, same fixed
+ * summation order, so the scores are bit-identical to sx_sparseq_score's.  Its scratch (the per-KV-head
+ * column sums and the gathered probe columns) lives in a 32 MiB array inside the library that each
+ * device holds from the first call on that device until the process ends; a plan needing more
+ * (8 Hkv sum T + 2 (n_probes + 64) Hq d + 4 (n_probes + 64) Hq bytes, each part rounded up to 256;
+ * bfloat16 plans, float32 plans only the first part) returns SX_EUNSUPPORTED.  Every call on a
+ * device shares that array: calls that overlap in time on one device (different streams, threads or
+ * processes without ordering) race and give wrong scores.  No host synchronisation. */
+sx_status sx_sparseq_score_static(const sx_plan* plan, const void* q, const void* k_cache, const float* lse_in,
+                                  float* scores, void* stream);
+
 /* Eq. topk, Section 3.3 and Algorithm 1 steps 14-17, per request: S_key = the k_r reused
  * positions (every position with SX_TOPK_ALL_POSITIONS) with the largest score (k_r as in
  * sx_plan_budget; ties go to the lower index),

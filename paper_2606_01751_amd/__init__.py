@@ -24,7 +24,7 @@ from typing import Optional, Sequence
 
 __all__ = [
     "LIB_PATH", "SxError", "lib", "LayerDesc", "Plan", "rope_realign", "kv_scatter", "realign_scatter",
-    "realign_scatter_layers", "rows_mask", "realign_scatter_masked", "sparseq_score",
+    "realign_scatter_layers", "rows_mask", "realign_scatter_masked", "sparseq_score", "sparseq_score_static",
     "topk_select", "sparse_attn", "full_attn", "gemm_rows", "gemm_rows_split", "rmsnorm_rows", "rope_rows",
     "silu_mul_rows", "F32", "BF16", "ROPE_NEOX", "ROPE_GPTJ", "TOPK_ALL_POSITIONS", "EXPORTED",
 ]
@@ -38,7 +38,7 @@ SX_OK, SX_EINVAL, SX_ESHAPE, SX_EUNSUPPORTED, SX_EHIP, SX_ENOMEM = 0, -1, -2, -3
 EXPORTED = (
     "sx_plan_create", "sx_plan_destroy", "sx_plan_get_info", "sx_plan_budget", "sx_plan_nonreused_rows",
     "sx_rope_realign", "sx_kv_scatter", "sx_realign_scatter", "sx_realign_scatter_layers", "sx_rows_mask",
-    "sx_realign_scatter_masked", "sx_sparseq_score", "sx_topk_select",
+    "sx_realign_scatter_masked", "sx_sparseq_score", "sx_sparseq_score_static", "sx_topk_select",
     "sx_sparse_attn", "sx_full_attn", "sx_gemm_rows", "sx_gemm_rows_split", "sx_rmsnorm_rows", "sx_rope_rows", "sx_silu_mul_rows",
     "sx_last_error", "sx_version",
 )
@@ -106,6 +106,7 @@ def lib() -> ctypes.CDLL:
         L.sx_rows_mask.argtypes = [VP, VP, VP, I32, VP, VP]
         L.sx_realign_scatter_masked.argtypes = [VP, VP, VP, VP, VP, VP, VP, VP, VP]
         L.sx_sparseq_score.argtypes = [VP, VP, VP, VP, VP, VP]
+        L.sx_sparseq_score_static.argtypes = [VP, VP, VP, VP, VP, VP]
         L.sx_topk_select.argtypes = [VP, VP, D, VP, VP, VP]
         L.sx_sparse_attn.argtypes = [VP, VP, VP, VP, I32, VP, VP, VP, VP]
         L.sx_full_attn.argtypes = [P(LayerDesc), VP, VP, VP, VP, I32, I32, VP, VP, VP]
@@ -261,6 +262,12 @@ def realign_scatter_masked(plan: Plan, src_k, src_v, k_new, v_new, mask, k_cache
 
 def sparseq_score(plan: Plan, q, k_cache, scores, lse_in=None, stream=None):
     _check(lib().sx_sparseq_score(plan.handle, _ptr(q), _ptr(k_cache), _ptr(lse_in), _ptr(scores), _stream(stream)))
+
+
+def sparseq_score_static(plan: Plan, q, k_cache, scores, lse_in, stream=None):
+    """sparseq_score in one-pass mode with the library's static scratch: allocates nothing."""
+    _check(lib().sx_sparseq_score_static(plan.handle, _ptr(q), _ptr(k_cache), _ptr(lse_in), _ptr(scores),
+                                         _stream(stream)))
 
 
 def topk_select(plan: Plan, scores, ratio: float, rows, n_rows, stream=None):

@@ -4,6 +4,7 @@
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
+#include <mutex>
 #include <new>
 
 #include "sx_internal.h"
@@ -632,6 +633,73 @@ sx_status sx_sparseq_score(const sx_plan* p, const void* q, const void* k_cache,
   if (st != SX_OK) return st;
   // pass 3: fixed-order sum over KV heads
   return check_launch(sx::launch_head_reduce(p, p->d_colsum, scores, s), "sx_sparseq_score pass 3 launch");
+}
+
+}  // extern "C"
+
+namespace {
+
+// Scratch of sx_sparseq_score_static: one array per device, in the library's code object, so the
+// entry point needs no allocation.  Host code never uses the array's name as an address: the
+// device address comes from hipGetSymbolAddress, once per device on its first call.
+constexpr size_t kStaticScratchBytes = (size_t)32 << 20;
+__device__ __align__(256) char scratch[kStaticScratchBytes];
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+sx_status static_scratch(void** out) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+  if (dev < 0 || dev >= kMaxDevices) return fail(SX_EUNSUPPORTED, "device %d beyond the static scratch table", dev);
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* ptr = nullptr;
+    e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || !ptr) return hip_fail(e, "hipGetSymbolAddress of the static scratch");
+    g_scratch_ptr[dev] = ptr;
+  }
+  *out = g_scratch_ptr[dev];
+  return SX_OK;
+}
+
+size_t align256(size_t n) { return (n + 255) & ~(size_t)255; }
+
+}  // namespace
+
+extern "C" {
+
+sx_status sx_sparseq_score_static(const sx_plan* p, const void* q, const void* k_cache, const float* lse_in,
+                                  float* scores, void* stream) {
+  if (!p) return fail(SX_EINVAL, "plan is NULL");
+  if (!q || !k_cache || !scores) return fail(SX_EINVAL, "NULL tensor argument");
+  if (!lse_in) return fail(SX_EINVAL, "sx_sparseq_score_static needs lse_in (one-pass scoring)");
+  const int64_t Hq = p->desc.n_q_heads, Hkv = p->desc.n_kv_heads, G = Hq / Hkv;
+  const bool bf16 = p->desc.dtype == SX_BF16;
+  const int64_t rows = p->n_probe + sx::kProbePad;
+  const size_t colsum_b = align256((size_t)(Hkv * p->total) * sizeof(double));
+  const size_t qp_b = bf16 ? align256((size_t)(rows * Hq * p->desc.head_dim) * sizeof(uint16_t)) : 0;
+  const size_t lse_b = bf16 ? align256((size_t)(Hkv * rows * G) * sizeof(float)) : 0;
+  const size_t need = colsum_b + qp_b + lse_b;
+  if (need > kStaticScratchBytes)
+    return fail(SX_EUNSUPPORTED, "the plan needs %zu bytes of scoring scratch; the static scratch holds %zu", need,
+                kStaticScratchBytes);
+  void* base = nullptr;
+  sx_status st = static_scratch(&base);
+  if (st != SX_OK) return st;
+  char* b = (char*)base;
+  const sx::ScoreScratch sc{(double*)b, bf16 ? (void*)(b + colsum_b) : nullptr,
+                            bf16 ? (float*)(b + colsum_b + qp_b) : nullptr};
+  hipStream_t s = (hipStream_t)stream;
+  if (bf16) {
+    // the gathered probe columns' padding rows must be finite: an earlier call may have left anything
+    st = check_launch(sx::launch_probe_pad_clear(p, sc, s), "sx_sparseq_score_static padding clear");
+    if (st != SX_OK) return st;
+  }
+  st = check_launch(sx::launch_colsum(p, sc, q, k_cache, lse_in, 1, s), "sx_sparseq_score_static column-sum launch");
+  if (st != SX_OK) return st;
+  return check_launch(sx::launch_head_reduce(p, sc.colsum, scores, s), "sx_sparseq_score_static head-sum launch");
 }
 
 sx_status sx_topk_select(const sx_plan* p, const float* scores, double ratio, int32_t* rows, int32_t* n_rows,
