@@ -17,9 +17,10 @@
 //   * Ping-pong: two groups of 4 waves (one of each per SIMD) alternate a matrix phase
 //     (MFMAs fed by pipelined LDS reads) and a softmax phase, so the matrix cores and the vector
 //     ALU of a SIMD work at the same time; tile transfers are issued from the softmax phase.
-//   * The 1-D grid is decoded KV head fastest, then request, then query-row tile from the latest
-//     rows (most keys) to the earliest: the heaviest tiles of every head start first, and with 8 KV
-//     heads the round-robin dispatch keeps all tiles of one head on one XCD (one L2).
+//   * The 1-D grid is decoded KV head fastest, then request-major: the row tiles of request 0 from
+//     the latest rows (most keys) to the earliest, then request 1, ...  With 8 KV heads the
+//     round-robin dispatch keeps all tiles of one head on one XCD (one L2), and the workgroups
+//     running there at one time mostly belong to one request, so they share its K/V tiles.
 //   * Softmax in the log2 domain; the running max is raised only when a probability would reach
 //     2^64, so the O^T rescale is rare and there is no max reduction on the common path.
 #include <type_traits>
@@ -117,11 +118,24 @@ __global__ __launch_bounds__(512, 1) void attn_mfma_kernel(AttnK a) {
   const int l32 = lane & 31;
   const int hg = lane >> 5;
   const int kvh = (int)(blockIdx.x % (unsigned)a.Hkv);
-  const int rest = (int)(blockIdx.x / (unsigned)a.Hkv);
-  const int r = rest % a.n_req;
-  // pieces of one row tile are adjacent in the grid (heaviest row tiles first)
-  const int qi = rest / a.n_req;
+  const int rpw = a.rpw;
   const int nsplit = (PAGED && !PV) ? a.nsplit : 1;
+  // rows of request rr that are processed: the first min(n_rows, max_rows) rows (the rows the KV
+  // write of the same row list covers), or every row of a dense request
+  auto rows_of = [&](int rr) -> int {
+    if constexpr (PAGED) return min(a.n_rows[rr], a.grid_rows);
+    else return a.cu[rr + 1] - a.cu[rr];
+  };
+  // Request-major grid: for each KV head, the row tiles of request 0 (latest rows, i.e. most keys,
+  // first), then those of request 1, ...  The workgroups running together on one XCD then mostly
+  // belong to one request and share its K/V tiles through that XCD's L2.  (Pieces of one row tile
+  // are adjacent.)
+  int r, qi;
+  locate_request((int)(blockIdx.x / (unsigned)a.Hkv), a.n_req,
+                 [&](int rr) { return (rows_of(rr) + rpw - 1) / rpw * nsplit; }, &r, &qi);
+  if (r < 0) return;
+  r = __builtin_amdgcn_readfirstlane(r);
+  qi = __builtin_amdgcn_readfirstlane(qi);
   const int rank = qi / nsplit;
   const int piece = qi - rank * nsplit;
 
@@ -132,16 +146,12 @@ __global__ __launch_bounds__(512, 1) void attn_mfma_kernel(AttnK a) {
     tok_off = rq.tok_off;
     bt_off = rq.bt_off;
     p_off = rq.p_off;
-    // the first min(n_rows, max_rows) rows: the rows the KV write of the same row list covers
-    nrows = min(a.n_rows[r], a.grid_rows);
   } else {
     tok_off = a.cu[r];
     T = a.cu[r + 1] - tok_off;
-    nrows = T;
   }
-  const int rpw = a.rpw;
+  nrows = rows_of(r);
   const int ntiles = (nrows + rpw - 1) / rpw;
-  if (rank >= ntiles) return;
   const int row_tile = ntiles - 1 - rank;
   const int row0 = row_tile * rpw;
   const int col = w * 32 + l32;
@@ -679,11 +689,18 @@ __global__ __launch_bounds__(512, 1) void colsum2_kernel(Colsum2K a) {
   const int l32 = lane & 31;
   const int hg = lane >> 5;
   const int kvh = (int)(blockIdx.x % (unsigned)a.Hkv);
-  const int rest = (int)(blockIdx.x / (unsigned)a.Hkv);
-  const ReqDev rq = a.reqs[rest % a.n_req];
+  // request-major grid (per KV head: the key tiles of request 0 from the first keys, which the most
+  // probe rows see, then request 1, ...), so the workgroups running together on one XCD mostly
+  // stream the same request's probe columns
+  int r, kt;
+  locate_request((int)(blockIdx.x / (unsigned)a.Hkv), a.n_req,
+                 [&](int rr) { return (a.reqs[rr].T + CS_KEYS - 1) / CS_KEYS; }, &r, &kt);
+  if (r < 0) return;
+  r = __builtin_amdgcn_readfirstlane(r);
+  kt = __builtin_amdgcn_readfirstlane(kt);
+  const ReqDev rq = a.reqs[r];
   const int T = rq.T;
-  const int j0 = (rest / a.n_req) * CS_KEYS;
-  if (j0 >= T) return;
+  const int j0 = kt * CS_KEYS;
   const int jw = j0 + w * 32;
   const int G = a.G;
   const int RC = a.RC;

@@ -29,6 +29,37 @@ __device__ __forceinline__ float wave_max(float v) {
   return v;
 }
 
+// Request-major position of a workgroup: position idx of the concatenation of every request's
+// items (cnt(r) items of request r, requests in order) -> request *r and item *q inside it; *r = -1
+// past the last item.  Every wave computes the same answer (no LDS, no barrier); cnt is called for
+// requests in runs of 64, one per lane.
+template <typename CountF>
+__device__ __forceinline__ void locate_request(int idx, int n_req, CountF cnt, int* r, int* q) {
+  const int lane = threadIdx.x & 63;
+  int base = 0;
+  for (int c0 = 0; c0 < n_req; c0 += 64) {
+    const int rr = c0 + lane;
+    const int c = rr < n_req ? cnt(rr) : 0;
+    int x = c;   // inclusive prefix over the lanes
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+      const int y = __shfl_up(x, o, 64);
+      if (lane >= o) x += y;
+    }
+    const int tot = __shfl(x, 63, 64);
+    if (idx < base + tot) {
+      const uint64_t m = __ballot(base + x > idx);
+      const int l = __ffsll((unsigned long long)m) - 1;
+      *r = c0 + l;
+      *q = idx - (base + __shfl(x, l, 64) - __shfl(c, l, 64));
+      return;
+    }
+    base += tot;
+  }
+  *r = -1;
+  *q = 0;
+}
+
 __device__ __forceinline__ int wave_max_i(int v) {
 #pragma unroll
   for (int o = 32; o >= 1; o >>= 1) v = max(v, __shfl_xor(v, o, 64));
