@@ -23,6 +23,11 @@
  * ---------------------------------------
  * Status: every function returns SX_OK (0) or a negative sx_status; it never aborts and never
  *   throws.  sx_last_error() gives a text for the last failure of the calling thread.
+ * Validation: arguments the host can see (descriptors, segment and block tables, sizes) are checked
+ *   on the host.  Index arrays in device memory (row lists, n_rows, cu_seqlens) are trusted by the
+ *   release library, libsx.so; the checked library, libsx_checked.so (same ABI, built alongside),
+ *   validates them on the device before any compute kernel reads them, synchronising the call's
+ *   stream, and returns SX_EDEVICE for an invalid one.
  * Memory: every tensor argument is device memory allocated and owned by the caller; the library
  *   never frees or keeps it.  The plan owns only its own metadata and scratch (device memory it
  *   allocates in sx_plan_create and frees in sx_plan_destroy).
@@ -66,6 +71,9 @@ enum {
   SX_ESHAPE = -2,        /* inconsistent sizes (heads, block ids out of range, ...) */
   SX_EUNSUPPORTED = -3,  /* valid but not implemented (head_dim, block_size, dtype) */
   SX_EHIP = -4,          /* a HIP runtime call failed */
+  SX_EDEVICE = -5,       /* checked library only: an index array in device memory is invalid (a row
+                            list out of range or not ascending, n_rows > T, bad cu_seqlens); nothing
+                            was computed */
   SX_ENOMEM = -6,        /* device allocation failed */
   SX_EFULL = -7          /* the block pool cannot hold the request (sx_cache_schedule) */
 };

@@ -26,14 +26,18 @@ __all__ = [
     "LIB_PATH", "SxError", "lib", "LayerDesc", "Plan", "rope_realign", "kv_scatter", "realign_scatter",
     "realign_scatter_layers", "rows_mask", "realign_scatter_masked", "sparseq_score", "sparseq_score_static",
     "topk_select", "sparse_attn", "full_attn", "gemm_rows", "gemm_rows_split", "rmsnorm_rows", "rope_rows",
-    "silu_mul_rows", "F32", "BF16", "ROPE_NEOX", "ROPE_GPTJ", "TOPK_ALL_POSITIONS", "EXPORTED",
+    "silu_mul_rows", "F32", "BF16", "ROPE_NEOX", "ROPE_GPTJ", "TOPK_ALL_POSITIONS", "EXPORTED", "use_checked",
+    "RELEASE_LIB_PATH", "CHECKED_LIB_PATH",
 ]
 
-LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libsx.so")
+RELEASE_LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libsx.so")
+# same ABI, index arrays in device memory validated on the device (SX_EDEVICE)
+CHECKED_LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libsx_checked.so")
+LIB_PATH = RELEASE_LIB_PATH
 
 F32, BF16 = 0, 1
 ROPE_NEOX, ROPE_GPTJ = 0, 1
-SX_OK, SX_EINVAL, SX_ESHAPE, SX_EUNSUPPORTED, SX_EHIP, SX_ENOMEM = 0, -1, -2, -3, -4, -6
+SX_OK, SX_EINVAL, SX_ESHAPE, SX_EUNSUPPORTED, SX_EHIP, SX_EDEVICE, SX_ENOMEM = 0, -1, -2, -3, -4, -5, -6
 
 EXPORTED = (
     "sx_plan_create", "sx_plan_destroy", "sx_plan_get_info", "sx_plan_budget", "sx_plan_nonreused_rows",
@@ -124,6 +128,14 @@ def lib() -> ctypes.CDLL:
                 getattr(L, name).restype = ctypes.c_int32
         _lib = L
     return _lib
+
+
+def use_checked(on: bool = True) -> None:
+    """Switch every binding to the checked library (libsx_checked.so) or back to the release one.
+    Plans belong to the library that made them: switch before creating them."""
+    global LIB_PATH, _lib
+    LIB_PATH = CHECKED_LIB_PATH if on else RELEASE_LIB_PATH
+    _lib = None
 
 
 def _check(status: int):

@@ -1,7 +1,10 @@
-"""Builds libsx.so (the C-ABI library declared in include/sx.h) for gfx950 with hipcc.
+"""Builds libsx.so (the C-ABI library declared in include/sx.h) for gfx950 with hipcc, and beside it
+libsx_checked.so: the same library with the device-side validation of index arrays
+(SX_DEVICE_CHECKS: row lists and cu_seqlens checked before any kernel reads them, SX_EDEVICE).
 
 Usage: python -m paper_2606_01751_amd.build [--debug]
-Objects go to _build/ at the repository root; the library lands next to this file.
+Objects go to _build/ at the repository root; the libraries land next to this file.  --debug builds
+both without optimisation.
 """
 from __future__ import annotations
 
@@ -18,6 +21,7 @@ CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 BUILD = os.path.join(ROOT, "_build")
 LIB = os.path.join(PKG, "libsx.so")
+LIB_CHECKED = os.path.join(PKG, "libsx_checked.so")
 
 
 def hipcc() -> str:
@@ -35,9 +39,9 @@ def common_flags(debug: bool = False):
     ]
 
 
-def _compile(src: str, debug: bool) -> str:
-    obj = os.path.join(BUILD, os.path.basename(src) + ".o")
-    cmd = [hipcc(), "-x", "hip", "-c", src, "-o", obj] + common_flags(debug)
+def _compile(src: str, debug: bool, checked: bool = False) -> str:
+    obj = os.path.join(BUILD, os.path.basename(src) + (".checked.o" if checked else ".o"))
+    cmd = [hipcc(), "-x", "hip", "-c", src, "-o", obj] + common_flags(debug) + (["-DSX_DEVICE_CHECKS=1"] if checked else [])
     res = subprocess.run(cmd, capture_output=True, text=True)
     if res.returncode != 0:
         raise RuntimeError(f"compile failed: {' '.join(cmd)}\n{res.stdout}\n{res.stderr}")
@@ -47,15 +51,22 @@ def _compile(src: str, debug: bool) -> str:
 def build(debug: bool = False, jobs: int = 8) -> str:
     os.makedirs(BUILD, exist_ok=True)
     sources = sorted(glob.glob(os.path.join(CSRC, "*.hip"))) + sorted(glob.glob(os.path.join(CSRC, "*.cpp")))
+    host = os.path.join(CSRC, "sx_host.cpp")   # the only source the device checks change
     with cf.ThreadPoolExecutor(max_workers=jobs) as ex:
         objs = list(ex.map(lambda s: _compile(s, debug), sources))
-    tmp = LIB + ".tmp"
+        host_checked = ex.submit(_compile, host, debug, True).result()
+    _link(objs, LIB)
+    _link([host_checked if o.endswith("sx_host.cpp.o") else o for o in objs], LIB_CHECKED)
+    return LIB
+
+
+def _link(objs, out: str) -> None:
+    tmp = out + ".tmp"
     cmd = [hipcc(), "-shared", "-fPIC", "--offload-arch=gfx950", "-o", tmp] + objs
     res = subprocess.run(cmd, capture_output=True, text=True)
     if res.returncode != 0:
         raise RuntimeError(f"link failed: {' '.join(cmd)}\n{res.stdout}\n{res.stderr}")
-    os.replace(tmp, LIB)
-    return LIB
+    os.replace(tmp, out)
 
 
 if __name__ == "__main__":

@@ -27,6 +27,39 @@ sx_status ok() { return SX_OK; }
 
 }  // namespace
 
+// Checked library: device index arrays are validated before the kernels that read them.
+#ifndef SX_DEVICE_CHECKS
+#define SX_DEVICE_CHECKS 0
+#endif
+namespace {
+
+const char* kCheckWhat[] = {"", "n_rows outside [0, T]", "row outside [0, T)", "rows not strictly ascending",
+                            "cu_seqlens[0] is not 0", "request length negative or above max_seqlen"};
+
+sx_status device_rows_ok(const sx_plan* p, const int32_t* rows, const int32_t* n_rows, int32_t max_rows,
+                         void* stream, const char* who) {
+  if (!SX_DEVICE_CHECKS || !n_rows) return SX_OK;
+  int v[4] = {0, 0, 0, 0};
+  const hipError_t e = sx::device_check_rows(p, rows, n_rows, max_rows, (hipStream_t)stream, v);
+  if (e != hipSuccess) return fail(SX_EHIP, "%s: device check: %s", who, hipGetErrorString(e));
+  if (v[0] != 0)
+    return fail(SX_EDEVICE, "%s: %s (request %d, entry %d, value %d)", who, kCheckWhat[v[0] < 6 ? v[0] : 0], v[1],
+                v[2], v[3]);
+  return SX_OK;
+}
+
+sx_status device_cu_ok(const int32_t* cu, int32_t n_req, int32_t max_seqlen, void* stream, const char* who) {
+  if (!SX_DEVICE_CHECKS) return SX_OK;
+  int v[4] = {0, 0, 0, 0};
+  const hipError_t e = sx::device_check_cu(cu, n_req, max_seqlen, (hipStream_t)stream, v);
+  if (e != hipSuccess) return fail(SX_EHIP, "%s: device check: %s", who, hipGetErrorString(e));
+  if (v[0] != 0)
+    return fail(SX_EDEVICE, "%s: %s (request %d, value %d)", who, kCheckWhat[v[0] < 6 ? v[0] : 0], v[1], v[3]);
+  return SX_OK;
+}
+
+}  // namespace
+
 namespace sx {
 sx_status report(sx_status st, const char* msg) {
   g_err = msg;
@@ -128,7 +161,7 @@ extern "C" {
 
 const char* sx_last_error(void) { return g_err.c_str(); }
 
-const char* sx_version(void) { return "libsx 0.1 (gfx950)"; }
+const char* sx_version(void) { return SX_DEVICE_CHECKS ? "libsx 0.2 (gfx950, device checks)" : "libsx 0.2 (gfx950)"; }
 
 sx_status sx_plan_create(const sx_layer_desc* desc, const sx_request* requests, int32_t n_requests,
                          int64_t n_dst_blocks, int64_t n_src_blocks, sx_plan** out) {
@@ -434,6 +467,8 @@ sx_status sx_kv_scatter(const sx_plan* p, const void* k_new, const void* v_new, 
     if (!n_rows) return fail(SX_EINVAL, "n_rows is NULL while rows is not");
     if (max_rows < 0) return fail(SX_EINVAL, "max_rows must be >= 0");
     if (max_rows == 0) return SX_OK;
+    sx_status st = device_rows_ok(p, rows, n_rows, max_rows, stream, "sx_kv_scatter");
+    if (st != SX_OK) return st;
   }
   return check_launch(sx::launch_scatter(p, k_new, v_new, rows, n_rows, rows ? max_rows : p->max_T, k_cache,
                                          v_cache, (hipStream_t)stream),
@@ -453,6 +488,10 @@ sx_status sx_realign_scatter_layers(const sx_plan* p, int32_t n_layers, const sx
     if (p->n_realign > 0 && (!x.src_k || !x.src_v)) return fail(SX_EINVAL, "layer %d: NULL source pool", l);
   }
   if (p->total == 0 || n_layers == 0) return SX_OK;
+  {
+    sx_status st = device_rows_ok(p, rows, n_rows, max_rows, stream, "sx_realign_scatter");
+    if (st != SX_OK) return st;
+  }
   const int64_t units = (int64_t)p->desc.n_kv_heads * p->desc.head_dim * (p->desc.dtype == SX_BF16 ? 2 : 4) / 32;
   if (p->total * units >= ((int64_t)1 << 31))
     return fail(SX_EUNSUPPORTED, "%lld tokens x %lld units exceed one launch", (long long)p->total, (long long)units);
@@ -473,6 +512,10 @@ sx_status sx_rows_mask(const sx_plan* p, const int32_t* rows, const int32_t* n_r
   if (!rows || !n_rows || !mask) return fail(SX_EINVAL, "NULL argument");
   if (max_rows < 0) return fail(SX_EINVAL, "max_rows must be >= 0");
   if (p->total == 0) return SX_OK;
+  {
+    sx_status st = device_rows_ok(p, rows, n_rows, max_rows, stream, "sx_rows_mask");
+    if (st != SX_OK) return st;
+  }
   return check_launch(sx::launch_rows_mask(p, rows, n_rows, max_rows, mask, (hipStream_t)stream),
                       "sx_rows_mask launch");
 }
@@ -502,13 +545,15 @@ sx_status sx_realign_scatter(const sx_plan* p, const void* src_k, const void* sr
 
 namespace {
 
-sx_status check_rows(const sx_plan* p, const int32_t* rows, const int32_t* n_rows, int32_t max_rows, bool need_rows) {
+sx_status check_rows(const sx_plan* p, const int32_t* rows, const int32_t* n_rows, int32_t max_rows, bool need_rows,
+                     void* stream, const char* who) {
   if (!p) return fail(SX_EINVAL, "plan is NULL");
   if (p->desc.dtype != SX_BF16) return fail(SX_EUNSUPPORTED, "the layer body runs on bfloat16 plans");
   if (!n_rows || (need_rows && !rows)) return fail(SX_EINVAL, "NULL row list");
   if (max_rows < 0) return fail(SX_EINVAL, "max_rows must be >= 0");
   if (max_rows > p->max_T) return fail(SX_ESHAPE, "max_rows %d exceeds the longest request (%d)", max_rows, p->max_T);
-  return SX_OK;
+  if (max_rows == 0) return SX_OK;
+  return device_rows_ok(p, rows, n_rows, max_rows, stream, who);
 }
 
 }  // namespace
@@ -516,7 +561,7 @@ sx_status check_rows(const sx_plan* p, const int32_t* rows, const int32_t* n_row
 sx_status sx_gemm_rows(const sx_plan* p, const int32_t* rows, const int32_t* n_rows, int32_t max_rows, const void* x,
                        int32_t x_by_token, const void* w, int32_t k, int32_t n, const void* residual, void* y,
                        int32_t y_by_token, void* stream) {
-  sx_status st = check_rows(p, rows, n_rows, max_rows, x_by_token || y_by_token);
+  sx_status st = check_rows(p, rows, n_rows, max_rows, x_by_token || y_by_token, stream, "sx_gemm_rows");
   if (st != SX_OK) return st;
   if (!x || !w || !y) return fail(SX_EINVAL, "NULL tensor argument");
   if (k <= 0 || n <= 0 || k % 64 != 0 || n % 256 != 0)
@@ -533,7 +578,7 @@ sx_status sx_gemm_rows(const sx_plan* p, const int32_t* rows, const int32_t* n_r
 sx_status sx_gemm_rows_split(const sx_plan* p, const int32_t* rows, const int32_t* n_rows, int32_t max_rows,
                              const void* x, int32_t x_by_token, const void* w, int32_t k, int32_t n_parts,
                              const int32_t* part_n, void* const* y_parts, int32_t y_by_token, void* stream) {
-  sx_status st = check_rows(p, rows, n_rows, max_rows, x_by_token || y_by_token);
+  sx_status st = check_rows(p, rows, n_rows, max_rows, x_by_token || y_by_token, stream, "sx_gemm_rows_split");
   if (st != SX_OK) return st;
   if (!x || !w || !part_n || !y_parts) return fail(SX_EINVAL, "NULL argument");
   if (n_parts < 1 || n_parts > 4) return fail(SX_EINVAL, "n_parts %d outside 1..4", n_parts);
@@ -556,7 +601,7 @@ sx_status sx_gemm_rows_split(const sx_plan* p, const int32_t* rows, const int32_
 sx_status sx_rmsnorm_rows(const sx_plan* p, const int32_t* rows, const int32_t* n_rows, int32_t max_rows,
                           const void* x, int32_t x_by_token, const void* gamma, float eps, int32_t h, void* y,
                           int32_t y_by_token, void* stream) {
-  sx_status st = check_rows(p, rows, n_rows, max_rows, x_by_token || y_by_token);
+  sx_status st = check_rows(p, rows, n_rows, max_rows, x_by_token || y_by_token, stream, "sx_rmsnorm_rows");
   if (st != SX_OK) return st;
   if (!x || !gamma || !y) return fail(SX_EINVAL, "NULL tensor argument");
   if (h <= 0 || h % 8 != 0) return fail(SX_EUNSUPPORTED, "hidden size %d must be a positive multiple of 8", h);
@@ -570,7 +615,7 @@ sx_status sx_rmsnorm_rows(const sx_plan* p, const int32_t* rows, const int32_t* 
 
 sx_status sx_rope_rows(const sx_plan* p, const int32_t* rows, const int32_t* n_rows, int32_t max_rows, void* q,
                        void* k, void* stream) {
-  sx_status st = check_rows(p, rows, n_rows, max_rows, true);
+  sx_status st = check_rows(p, rows, n_rows, max_rows, true, stream, "sx_rope_rows");
   if (st != SX_OK) return st;
   if (!q || !k) return fail(SX_EINVAL, "NULL tensor argument");
   if (max_rows == 0) return SX_OK;
@@ -580,7 +625,7 @@ sx_status sx_rope_rows(const sx_plan* p, const int32_t* rows, const int32_t* n_r
 
 sx_status sx_silu_mul_rows(const sx_plan* p, const int32_t* n_rows, int32_t max_rows, const void* gate_up, int32_t f,
                            void* y, void* stream) {
-  sx_status st = check_rows(p, nullptr, n_rows, max_rows, false);
+  sx_status st = check_rows(p, nullptr, n_rows, max_rows, false, stream, "sx_silu_mul_rows");
   if (st != SX_OK) return st;
   if (!gate_up || !y) return fail(SX_EINVAL, "NULL tensor argument");
   if (f <= 0 || f % 8 != 0) return fail(SX_EUNSUPPORTED, "feed-forward size %d must be a positive multiple of 8", f);
@@ -717,6 +762,10 @@ sx_status sx_sparse_attn(const sx_plan* p, const void* q, const int32_t* rows, c
   if (!q || !rows || !n_rows || !k_cache || !v_cache || !out) return fail(SX_EINVAL, "NULL argument");
   if (max_rows < 0) return fail(SX_EINVAL, "max_rows must be >= 0");
   if (max_rows == 0) return SX_OK;
+  {
+    sx_status st = device_rows_ok(p, rows, n_rows, max_rows, stream, "sx_sparse_attn");
+    if (st != SX_OK) return st;
+  }
   sx::AttnLaunch a{};
   a.Hq = p->desc.n_q_heads;
   a.Hkv = p->desc.n_kv_heads;
@@ -746,6 +795,8 @@ sx_status sx_full_attn(const sx_layer_desc* desc, const void* q, const void* k, 
   if (n_requests < 1) return fail(SX_EINVAL, "n_requests must be >= 1");
   if (max_seqlen < 0) return fail(SX_EINVAL, "max_seqlen must be >= 0");
   if (max_seqlen == 0) return SX_OK;
+  st = device_cu_ok(cu_seqlens, n_requests, max_seqlen, stream, "sx_full_attn");
+  if (st != SX_OK) return st;
   sx::AttnLaunch a{};
   a.Hq = desc->n_q_heads;
   a.Hkv = desc->n_kv_heads;

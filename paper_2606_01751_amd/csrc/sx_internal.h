@@ -132,6 +132,12 @@ hipError_t launch_topk(const sx_plan* p, const float* scores, double ratio, int3
 // Row-sparse layer body (defined in k_layer.hip).  Rows are the listed rows of every request in
 // the row-list layout; an operand row is addressed by slot (off_r + n) or by token
 // (off_r + rows[off_r + n]).
+// Device-side validation (checked library): launches the checks on `s`, synchronises it and fills
+// verdict = {code (0 = valid), request, index, value}.  Row lists: rows may be NULL (counts only).
+hipError_t device_check_rows(const sx_plan* p, const int32_t* rows, const int32_t* n_rows, int32_t max_rows,
+                             hipStream_t s, int verdict[4]);
+hipError_t device_check_cu(const int32_t* cu, int32_t n_req, int32_t max_seqlen, hipStream_t s, int verdict[4]);
+
 // Sets the thread-local error message read by sx_last_error and returns st (for host-only
 // translation units without the dispatcher's helpers).
 sx_status report(sx_status st, const char* msg);

@@ -151,3 +151,19 @@ def test_missing_library_fails_loudly(monkeypatch, tmp_path):
     monkeypatch.setattr(C, "_ready", False)
     with pytest.raises(RuntimeError, match="is missing"):
         C.sha256(b"abc")
+
+
+def test_checked_library_exports_the_same_abi():
+    # libsx_checked.so: same entry points, device-side validation of index arrays compiled in
+    rel = ctypes.CDLL(sx.RELEASE_LIB_PATH)
+    chk = ctypes.CDLL(sx.CHECKED_LIB_PATH)
+    for name in _header_functions():
+        assert hasattr(chk, name), name
+    chk.sx_version.restype = rel.sx_version.restype = ctypes.c_char_p
+    assert b"device checks" in chk.sx_version() and b"device checks" not in rel.sx_version()
+    sx.use_checked(True)
+    try:
+        # host validation is unchanged in the checked library
+        assert _status(_desc(head_dim=96), [_good()])[0] == sx.SX_EUNSUPPORTED
+    finally:
+        sx.use_checked(False)
