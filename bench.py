@@ -83,7 +83,6 @@ KERNELS = {
     # two-pass scoring only (layers without a preceding full layer)
     "attn_mfma_kernel<128, true, false>": ("sx_sparseq_score", "k_attn.hip", False),
     "lse_merge_kernel": ("sx_sparseq_score", "k_attn.hip", False),
-    "colsum_mfma_kernel<128>": ("sx_sparseq_score", "k_attn.hip", True),   # query heads per KV head > 64 only
     "colsum2_kernel<128>": ("sx_sparseq_score", "k_attn.hip", True),
     "probe_gather_kernel<128>": ("sx_sparseq_score", "k_attn.hip", False),
     "head_reduce_kernel": ("sx_sparseq_score", "k_copy.hip", False),
@@ -93,7 +92,9 @@ KERNELS = {
     "mark_rows_kernel": ("sx_realign_scatter", "k_copy.hip", False),   # (also sx_realign_scatter_layers)
     "fill_u8_kernel": ("sx_rows_mask", "k_copy.hip", True),
     "mask_rows_kernel": ("sx_rows_mask", "k_copy.hip", False),
-    "topk_kernel": ("sx_topk_select", "k_topk.hip", True),
+    "topk_hist_kernel": ("sx_topk_select", "k_topk.hip", False),   # three radix passes per call
+    "topk_count_kernel": ("sx_topk_select", "k_topk.hip", False),
+    "topk_write_kernel": ("sx_topk_select", "k_topk.hip", True),
 }
 
 

@@ -31,6 +31,9 @@
 namespace sx {
 namespace {
 
+#ifndef SX_CS_NBUF
+#define SX_CS_NBUF 3       // probe-chunk buffers of the column-sum kernel (3 to 5)
+#endif
 #ifndef SX_ATTN_NBUF
 #define SX_ATTN_NBUF 3     // K/V tile buffers of the attention kernel (3 or 4; 4 measured no faster)
 #endif
@@ -679,7 +682,8 @@ __global__ __launch_bounds__(512, 1) void colsum2_kernel(Colsum2K a) {
   constexpr int PPW = (NPC + NW - 1) / NW;    // per wave
   constexpr int QB = NC * ROWB;
   constexpr int CHB = QB + 512;               // + 64 log-sum-exps + 64 positions
-  constexpr int NBUF = 3;
+  constexpr int NBUF = SX_CS_NBUF;            // chunk buffers; chunk k + NBUF - 1 is issued with chunk k
+  static_assert(NBUF >= 3 && NBUF <= 5, "three to five chunk buffers");
   static_assert(NPC % NW == 0, "query transfers spread evenly over the waves");
   __shared__ __attribute__((aligned(1024))) char smem[NBUF * CHB];
   const int tid = threadIdx.x;
@@ -727,7 +731,7 @@ __global__ __launch_bounds__(512, 1) void colsum2_kernel(Colsum2K a) {
     if (probe[mid] < j0) lo = mid + 1; else hi = mid;
   }
   const int nchunk = (np - lo + RC - 1) / RC;
-  // ---- transfers of chunk k into buffer k mod 3 (this wave's share).  Rows past the request's
+  // ---- transfers of chunk k into buffer k mod NBUF (this wave's share).  Rows past the request's
   // probe rows read the zeroed padding (at most RC - 1 < kProbePad rows), so no clamping ----
   // query pieces: slot column qc = CPP * piece + lane / NCH, physical chunk lane % NCH holding
   // logical chunk (lane % NCH) ^ (qc mod NCH); slot columns past RC * G repeat column RC * G - 1
@@ -770,10 +774,23 @@ __global__ __launch_bounds__(512, 1) void colsum2_kernel(Colsum2K a) {
       case 1: SX_WAIT_VMCNT(1); break;
       case 2: SX_WAIT_VMCNT(2); break;
       case 3: SX_WAIT_VMCNT(3); break;
-      default: SX_WAIT_VMCNT(4); break;
+      case 4: SX_WAIT_VMCNT(4); break;
+      case 5: SX_WAIT_VMCNT(5); break;
+      case 6: SX_WAIT_VMCNT(6); break;
+      case 7: SX_WAIT_VMCNT(7); break;
+      case 8: SX_WAIT_VMCNT(8); break;
+      default: SX_WAIT_VMCNT(9); break;
     }
   };
-  static_assert(PPW + 1 <= 4, "transfer count per chunk exceeds the wait table");
+  static_assert((NBUF - 2) * (PPW + 1) <= 9, "transfers in flight exceed the wait table");
+  // this wave's transfers still allowed in flight once chunk k + 1 must have landed: those of
+  // chunks k + 2 .. k + NBUF - 1
+  auto inflight = [&](int k) {
+    int n = 0;
+#pragma unroll
+    for (int c = 2; c < NBUF; ++c) n += k + c < nchunk ? n_mine : 0;
+    return n;
+  };
   // chunks whose first probe row lies before the workgroup's last key may miss keys of a wave
   // (causal mask); the later ones see all 256 keys.  Probe rows ascend, so the masked chunks come
   // first: nmask of them.
@@ -798,9 +815,9 @@ __global__ __launch_bounds__(512, 1) void colsum2_kernel(Colsum2K a) {
   // K must be in registers before the first transfer wait (the compiler does not count the
   // transfers, so a later wait of its own for K would also wait for them)
   SX_WAIT_VMCNT(0);
-  issue(0);
-  issue(1);
-  wait_vm(1 < nchunk ? n_mine : 0);
+#pragma unroll
+  for (int c = 0; c < NBUF - 1; ++c) issue(c);
+  wait_vm(inflight(-1));   // chunk 0 has landed
   __syncthreads();
   const float c2 = a.scale_log2;
   // S^T of column group gi of the chunk in buffer b
@@ -860,17 +877,17 @@ __global__ __launch_bounds__(512, 1) void colsum2_kernel(Colsum2K a) {
     m1 = meta(smem, 0, 1);
     s0 = s_group(smem, 0);
   }
-  // one chunk; `phase` is k mod 3 when known at compile time (the buffer bases then fold into the
-  // LDS reads' immediate offsets), else -1
+  // one chunk; `phase` is k mod NBUF when known at compile time (the buffer bases then fold into
+  // the LDS reads' immediate offsets), else -1
   auto body = [&](int k, auto masked, auto phase) {
     constexpr int PH = decltype(phase)::value;
-    issue(k + 2);
+    issue(k + NBUF - 1);
     const char* b = smem + (PH >= 0 ? PH : k % NBUF) * CHB;
     s1 = s_group(b, 1);
     accumulate(s0, m0, masked);
     interleave(masked);
     const Meta m1k = m1;
-    wait_vm(k + 2 < nchunk ? n_mine : 0);   // this wave's transfers of chunk k + 1 have landed
+    wait_vm(inflight(k));   // this wave's transfers of chunk k + 1 have landed
     __syncthreads();
     const char* bn = smem + (PH >= 0 ? (PH + 1) % NBUF : (k + 1) % NBUF) * CHB;
     m0 = meta(bn, k + 1, 0);
@@ -890,6 +907,8 @@ __global__ __launch_bounds__(512, 1) void colsum2_kernel(Colsum2K a) {
   using p0 = std::integral_constant<int, 0>;
   using p1 = std::integral_constant<int, 1>;
   using p2 = std::integral_constant<int, 2>;
+  using p3 = std::integral_constant<int, 3>;
+  using p4 = std::integral_constant<int, 4>;
   int k = 0;
   for (; k < nmask; ++k) body(k, std::true_type{}, dyn{});
   for (; k < nchunk && k % NBUF != 0; ++k) body(k, std::false_type{}, dyn{});
@@ -897,6 +916,8 @@ __global__ __launch_bounds__(512, 1) void colsum2_kernel(Colsum2K a) {
     body(k, std::false_type{}, p0{});
     body(k + 1, std::false_type{}, p1{});
     body(k + 2, std::false_type{}, p2{});
+    if constexpr (NBUF > 3) body(k + 3, std::false_type{}, p3{});
+    if constexpr (NBUF > 4) body(k + 4, std::false_type{}, p4{});
   }
   for (; k < nchunk; ++k) body(k, std::false_type{}, dyn{});
 #pragma unroll

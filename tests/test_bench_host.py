@@ -36,12 +36,13 @@ def test_kernels_inside_a_call_add_up(tmp_path, monkeypatch):
     assert bench.load_traffic("w") == pytest.approx({"sx_sparseq_score": 125.0})
 
 
-def test_variants_of_one_entry_point_are_weighted_by_dispatches(tmp_path, monkeypatch):
-    # two column-sum variants serve sx_sparseq_score (by GQA group size): one call with 400 bytes and
-    # three with 100 bytes average 175 bytes per call
-    _setup(tmp_path, monkeypatch, {"colsum_mfma_kernel<128>": (1, 400.0, False),
-                                   "colsum2_kernel<128>": (3, 100.0, False)})
-    assert bench.load_traffic("w") == pytest.approx({"sx_sparseq_score": 175.0})
+def test_several_dispatches_of_one_kernel_per_call_add_up(tmp_path, monkeypatch):
+    # a selection call runs three radix passes, a count pass and a write pass: with per-dispatch
+    # means of 10, 20 and 30 bytes over 3 calls, a call moves 3 x 10 + 20 + 30 = 80 bytes
+    _setup(tmp_path, monkeypatch, {"topk_hist_kernel": (9, 10.0, False), "topk_count_kernel": (3, 20.0, False),
+                                   "topk_write_kernel": (3, 30.0, False)},
+           sources=("k_topk.hip",))
+    assert bench.load_traffic("w") == pytest.approx({"sx_topk_select": 80.0})
 
 
 def test_entry_without_counted_calls_or_with_stale_source_is_dropped(tmp_path, monkeypatch):
