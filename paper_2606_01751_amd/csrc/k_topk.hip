@@ -4,24 +4,24 @@
 // k_r candidates with the largest float32 score, ties to the lower index; R = base rows (I_nr,
 // overflow, tail fallback: precomputed plan flags) U S_key, ascending.
 //
-// Every request is cut into chunks of CHUNK tokens, one 256-thread workgroup per chunk, so a
-// request's selection runs on many CUs:
+// Every request is cut into chunks of kTopkChunk tokens, one 256-thread workgroup per chunk, so a
+// request's selection runs on many CUs, in five launches with no counters or waits between
+// workgroups:
 //   passes 0-2  radix select of the k_r-th largest score among the candidates, 11 + 11 + 10 bits from
 //               the most significant (scores are >= 0, so the IEEE bit pattern orders them): each
-//               workgroup builds an LDS histogram of its candidates that match the digits found so
-//               far and adds it to the request's histogram in plan scratch.  The workgroup that
-//               finishes last (a per-request arrival counter) picks the digit, updates the
-//               request's state (digits, candidates still needed) and clears the histogram and
-//               the counter for the next pass, so the scratch is clean again without a fill.
-//   count       per chunk: rows surely in R (base rows and candidates above the threshold), and
-//               candidates equal to the threshold (ties).  The last workgroup turns the counts into
-//               each chunk's output offset and tie rank (rescanning the one chunk in which the
-//               tie budget runs out) and writes n_rows.
-//   write       per chunk: an ordered compaction of its rows of R at the chunk's offset; a tie is in
-//               R when its rank among the request's ties (index order) is below the tie budget.
-// Scratch (plan-owned, zeroed once when the plan is made): the histograms and counters, the
-// per-request state and the per-chunk counts and offsets.  Calls sharing a plan must be
-// stream-ordered.
+//               workgroup adds the LDS histogram of its candidates that match the digits found so far
+//               to the request's histogram of the pass.  Pass p first finds digit p-1 itself from
+//               pass p-1's histogram (complete once the previous launch ended); its first workgroup
+//               stores the digits for the later launches.
+//   count       the last digit from pass 2's histogram, then per chunk the rows surely in R (base rows
+//               and candidates above the threshold), the candidates equal to it (ties) and the ties
+//               that are not sure rows.
+//   write       per chunk: its offset in R and first tie rank from the counts of the chunks before it
+//               (the chunks after the one in which the tie budget runs out rescan that chunk), then
+//               an ordered compaction of its rows of R; a tie is in R when its rank among the
+//               request's ties (index order) is below the tie budget.  The first chunk clears the
+//               request's histograms for the next call.
+// Scratch is plan-owned; calls sharing a plan must be stream-ordered.
 #include "sx_device.h"
 #include "sx_internal.h"
 
@@ -98,23 +98,6 @@ __device__ __forceinline__ int block_excl_sum(int v, int* wsum, int& total) {
   return before + x - v;
 }
 
-// Arrival of this workgroup at the request's counter; true in the last one (after the fence, it
-// sees every other workgroup's scratch writes).  The last one resets the counter.
-__device__ __forceinline__ bool arrive_last(uint32_t* ctr, uint32_t n_blocks, int* s_flag) {
-  __threadfence();
-  __syncthreads();
-  if (threadIdx.x == 0) {
-    const uint32_t old = atomicAdd(ctr, 1u);
-    const bool last = old == n_blocks - 1;
-    if (last) *ctr = 0u;
-    *s_flag = last ? 1 : 0;
-  }
-  __syncthreads();
-  const bool last = *s_flag != 0;
-  if (last) __threadfence();
-  return last;
-}
-
 struct TopkArgs {
   const ReqDev* reqs;
   const uint8_t* flags;
@@ -125,58 +108,27 @@ struct TopkArgs {
   int32_t* n_rows;
 };
 
-// Radix pass p over every chunk of every request (blockIdx.y = request, blockIdx.x = chunk).
-__global__ __launch_bounds__(NT) void topk_hist_kernel(TopkArgs a, int p) {
-  __shared__ uint32_t hist[NBINS];
-  __shared__ int wsum[NWV];
-  __shared__ int s_flag;
-  __shared__ uint32_t s_digit;
-  __shared__ int s_rem;
-  const int r = blockIdx.y;
-  const ReqDev rq = a.reqs[r];
-  const int T = rq.T;
-  const uint32_t nb = (uint32_t)((T + kTopkChunk - 1) / kTopkChunk);
-  if (blockIdx.x >= nb) return;
-  const int64_t n = rq.n_reuse;
-  const int64_t k = budget_dev(n, a.ratio);
-  if (select_mode(k, n) != 2) return;
-  uint32_t prefix = 0, mask = 0;
-  int remaining = (int)k;
-  uint32_t* st = a.sc.state + 4 * r;
-  if (p > 0) {
-    prefix = st[0];
-    mask = st[1];
-    remaining = (int)st[2];
-  }
-  const int shift = pass_shift(p);
-  const uint32_t bins = pass_bins(p);
-  const int tid = threadIdx.x;
-  for (int i = tid; i < NBINS; i += NT) hist[i] = 0u;
-  __syncthreads();
-  uint32_t u[TPT];
-  uint8_t f[TPT];
-  load8(a.scores + rq.tok_off, a.flags + rq.tok_off, blockIdx.x * kTopkChunk + tid * TPT, T, u, f);
-#pragma unroll
-  for (int i = 0; i < TPT; ++i) {
-    if ((f[i] & kFlagCandidate) && (u[i] & mask) == prefix) atomicAdd(&hist[(u[i] >> shift) & (bins - 1)], 1u);
-  }
-  __syncthreads();
-  uint32_t* gh = a.sc.hist + (size_t)r * NBINS;
-  for (int i = tid; i < NBINS; i += NT) {
-    const uint32_t c = hist[i];
-    if (c) atomicAdd(&gh[i], c);
-  }
-  if (!arrive_last(a.sc.ctr + r, nb, &s_flag)) return;
-  // the last workgroup: digit = the largest d with (matching candidates in bins >= d) >= remaining;
-  // thread t holds bins 8t .. 8t+7 (pass 2 has 1024 bins: the upper half stays empty)
+// Selection state after some digits: the digits found (prefix), their bit mask, and how many
+// candidates matching them are still to be selected.
+struct SelState {
+  uint32_t prefix, mask;
+  int remaining;
+};
+
+// The digit of pass p from the request's completed histogram of that pass (every workgroup computes
+// the same answer): the largest d with (matching candidates in bins >= d) >= remaining.  Thread t
+// holds bins 8t .. 8t+7 (pass 2 has 1024 bins: the upper half stays empty).  All threads call it.
+__device__ SelState next_digit(const uint32_t* gh, SelState in, int p, int* wsum) {
   constexpr int per = NBINS / NT;
+  const int tid = threadIdx.x;
   uint32_t c[per];
   int loc = 0;
+  const uint4 a0 = *(const uint4*)(gh + per * tid);
+  const uint4 a1 = *(const uint4*)(gh + per * tid + 4);
+  c[0] = a0.x; c[1] = a0.y; c[2] = a0.z; c[3] = a0.w;
+  c[4] = a1.x; c[5] = a1.y; c[6] = a1.z; c[7] = a1.w;
 #pragma unroll
-  for (int i = 0; i < per; ++i) {
-    c[i] = __hip_atomic_load(&gh[per * tid + i], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    loc += (int)c[i];
-  }
+  for (int i = 0; i < per; ++i) loc += (int)c[i];
   int total;
   const int below = block_excl_sum(loc, wsum, total);   // bins of lower threads
   int ge = total - below - loc;                         // bins above this thread's
@@ -185,13 +137,13 @@ __global__ __launch_bounds__(NT) void topk_hist_kernel(TopkArgs a, int p) {
   for (int i = per - 1; i >= 0; --i) {
     const int gt_i = ge;
     ge += (int)c[i];
-    if (best < 0 && ge >= remaining) {
+    if (best < 0 && ge >= in.remaining) {
       best = per * tid + i;
       best_gt = gt_i;
     }
   }
-  // qualifying digits are exactly those <= the answer, so the answer is the best of the highest
-  // thread that has one
+  // qualifying digits are exactly those <= the answer: it is the best of the highest thread that
+  // has one; broadcast (digit, candidates above it) through LDS
   int top = best >= 0 ? tid : -1;
 #pragma unroll
   for (int o = 1; o < 64; o <<= 1) top = max(top, __shfl_xor(top, o, 64));
@@ -200,30 +152,75 @@ __global__ __launch_bounds__(NT) void topk_hist_kernel(TopkArgs a, int p) {
   top = -1;
 #pragma unroll
   for (int i = 0; i < NWV; ++i) top = max(top, wsum[i]);
-  if (top < 0) {
-    // fewer matching candidates than still needed: impossible when k <= n (kept defensive)
-    if (tid == 0) {
-      s_digit = 0u;
-      s_rem = 0;
-    }
-  } else if (tid == top) {
-    s_digit = (uint32_t)best;
-    s_rem = remaining - best_gt;
+  __syncthreads();
+  if (top >= 0 && tid == top) {
+    wsum[0] = best;
+    wsum[1] = best_gt;
   }
   __syncthreads();
-  for (int i = tid; i < NBINS; i += NT) gh[i] = 0u;   // clean for the next pass or call
-  if (tid == 0) {
-    st[0] = prefix | (s_digit << shift);
-    st[1] = mask | ((bins - 1) << shift);
-    st[2] = (uint32_t)s_rem;
+  // (no qualifying digit means fewer matching candidates than still needed: impossible when
+  // k <= n; kept defensive)
+  const int d = top >= 0 ? wsum[0] : 0;
+  const int gt = top >= 0 ? wsum[1] : in.remaining;
+  __syncthreads();
+  const int shift = pass_shift(p);
+  return SelState{in.prefix | ((uint32_t)d << shift), in.mask | ((pass_bins(p) - 1) << shift), in.remaining - gt};
+}
+
+__device__ __forceinline__ void store_state(uint32_t* st, SelState s) {
+  st[0] = s.prefix;
+  st[1] = s.mask;
+  st[2] = (uint32_t)s.remaining;
+}
+__device__ __forceinline__ SelState load_state(const uint32_t* st) {
+  return SelState{st[0], st[1], (int)st[2]};
+}
+
+// Radix pass p over every chunk of every request (blockIdx.y = request, blockIdx.x = chunk).  The
+// digits of the earlier passes come from the state the previous launch's first workgroup stored
+// and from pass p-1's histogram, completed by the previous launch.
+__global__ __launch_bounds__(NT) void topk_hist_kernel(TopkArgs a, int p) {
+  __shared__ uint32_t hist[NBINS];
+  __shared__ int wsum[2 * NWV];
+  const int r = blockIdx.y;
+  const ReqDev rq = a.reqs[r];
+  const int T = rq.T;
+  const uint32_t nb = (uint32_t)((T + kTopkChunk - 1) / kTopkChunk);
+  if (blockIdx.x >= nb) return;
+  const int64_t n = rq.n_reuse;
+  const int64_t k = budget_dev(n, a.ratio);
+  if (select_mode(k, n) != 2) return;
+  const int tid = threadIdx.x;
+  uint32_t u[TPT];
+  uint8_t f[TPT];
+  load8(a.scores + rq.tok_off, a.flags + rq.tok_off, blockIdx.x * kTopkChunk + tid * TPT, T, u, f);
+  for (int i = tid; i < NBINS; i += NT) hist[i] = 0u;
+  SelState s{0u, 0u, (int)k};
+  if (p > 0) {
+    if (p == 2) s = load_state(a.sc.state + (r * 3 + 0) * 4);   // digit 0, stored by pass 1
+    s = next_digit(a.sc.hist + ((size_t)r * 3 + (p - 1)) * NBINS, s, p - 1, wsum);
+    if (blockIdx.x == 0 && tid == 0) store_state(a.sc.state + (r * 3 + (p - 1)) * 4, s);
+  }
+  __syncthreads();
+  const int shift = pass_shift(p);
+  const uint32_t bins = pass_bins(p);
+#pragma unroll
+  for (int i = 0; i < TPT; ++i) {
+    if ((f[i] & kFlagCandidate) && (u[i] & s.mask) == s.prefix) atomicAdd(&hist[(u[i] >> shift) & (bins - 1)], 1u);
+  }
+  __syncthreads();
+  uint32_t* gh = a.sc.hist + ((size_t)r * 3 + p) * NBINS;
+  for (int i = tid; i < (int)bins; i += NT) {
+    const uint32_t c = hist[i];
+    if (c) atomicAdd(&gh[i], c);
   }
 }
 
-// Per chunk: rows surely in R, ties and ties that are not sure rows; the last workgroup derives
-// every chunk's output offset and tie rank and the request's |R|.
+// Per chunk: rows surely in R (base rows, candidates above the threshold), ties (candidates equal
+// to it) and ties that are not sure rows.  The threshold's last digit comes from pass 2's
+// histogram; the first workgroup stores the final state.
 __global__ __launch_bounds__(NT) void topk_count_kernel(TopkArgs a) {
-  __shared__ int wsum[NWV];
-  __shared__ int s_flag;
+  __shared__ int wsum[2 * NWV];
   const int r = blockIdx.y;
   const ReqDev rq = a.reqs[r];
   const int T = rq.T;
@@ -232,26 +229,23 @@ __global__ __launch_bounds__(NT) void topk_count_kernel(TopkArgs a) {
   const int64_t n = rq.n_reuse;
   const int64_t k = budget_dev(n, a.ratio);
   const int mode = select_mode(k, n);
-  const uint32_t* st = a.sc.state + 4 * r;
-  const uint32_t thr = mode == 2 ? st[0] : 0u;
-  const int need_eq = mode == 2 ? (int)st[2] : 0;
   const int tid = threadIdx.x;
-  const uint32_t* sb = a.scores + rq.tok_off;
-  const uint8_t* fl = a.flags + rq.tok_off;
-  auto classify = [&](uint32_t u, uint8_t f, bool& sure, bool& eq) {
-    const bool cand = f & kFlagCandidate;
-    const bool gt = mode == 2 && cand && u > thr;
-    eq = mode == 2 && cand && u == thr;
-    sure = (f & kFlagBase) || (mode == 1 ? cand : gt);
-  };
   uint32_t u[TPT];
   uint8_t f[TPT];
-  load8(sb, fl, blockIdx.x * kTopkChunk + tid * TPT, T, u, f);
+  load8(a.scores + rq.tok_off, a.flags + rq.tok_off, blockIdx.x * kTopkChunk + tid * TPT, T, u, f);
+  SelState s{0u, 0u, 0};
+  if (mode == 2) {
+    s = next_digit(a.sc.hist + ((size_t)r * 3 + 2) * NBINS, load_state(a.sc.state + (r * 3 + 1) * 4), 2, wsum);
+    if (blockIdx.x == 0 && tid == 0) store_state(a.sc.state + (r * 3 + 2) * 4, s);
+  }
+  const uint32_t thr = s.prefix;
   int ns = 0, ne = 0, nens = 0;
 #pragma unroll
   for (int i = 0; i < TPT; ++i) {
-    bool sure, eq;
-    classify(u[i], f[i], sure, eq);
+    const bool cand = f[i] & kFlagCandidate;
+    const bool gt = mode == 2 && cand && u[i] > thr;
+    const bool eq = mode == 2 && cand && u[i] == thr;
+    const bool sure = (f[i] & kFlagBase) || (mode == 1 ? cand : gt);
     ns += sure;
     ne += eq;
     nens += eq && !sure;
@@ -260,39 +254,90 @@ __global__ __launch_bounds__(NT) void topk_count_kernel(TopkArgs a) {
   block_excl_sum(ns, wsum, ts);
   block_excl_sum(ne, wsum, te);
   block_excl_sum(nens, wsum, tens);
-  int32_t* cnt = a.sc.cnt + (size_t)r * a.sc.max_chunks * 3;
   if (tid == 0) {
-    cnt[3 * blockIdx.x + 0] = ts;
-    cnt[3 * blockIdx.x + 1] = te;
-    cnt[3 * blockIdx.x + 2] = tens;
+    int32_t* cnt = a.sc.cnt + ((size_t)r * a.sc.max_chunks + blockIdx.x) * 3;
+    cnt[0] = ts;
+    cnt[1] = te;
+    cnt[2] = tens;
   }
-  if (!arrive_last(a.sc.ctr + r, nb, &s_flag)) return;
-  // last workgroup: walk the chunks in order (thread 0), finding the one chunk whose ties straddle
-  // the tie budget; that chunk's count of selected ties that are not sure rows needs a rescan
-  __shared__ int s_bchunk, s_blim;
+}
+
+// Per chunk: the chunk's offset in R and its first tie rank from the counts of the chunks before it
+// (the one chunk in which the tie budget runs out is rescanned by the chunks after it), then an
+// ordered compaction of its rows of R.  The last chunk writes n_rows; the first clears the
+// request's histograms for the next call.
+__global__ __launch_bounds__(NT) void topk_write_kernel(TopkArgs a) {
+  __shared__ int wsum[2 * NWV];
+  __shared__ int s_pre[4];
+  const int r = blockIdx.y;
+  const ReqDev rq = a.reqs[r];
+  const int T = rq.T;
+  const uint32_t nb = (uint32_t)((T + kTopkChunk - 1) / kTopkChunk);
+  const uint32_t b = blockIdx.x;
+  if (b >= nb) return;
+  const int64_t n = rq.n_reuse;
+  const int64_t k = budget_dev(n, a.ratio);
+  const int mode = select_mode(k, n);
+  const int tid = threadIdx.x;
+  const uint32_t* sb = a.scores + rq.tok_off;
+  const uint8_t* fl = a.flags + rq.tok_off;
+  const SelState s = mode == 2 ? load_state(a.sc.state + (r * 3 + 2) * 4) : SelState{0u, 0u, 0};
+  const uint32_t thr = s.prefix;
+  const int need_eq = s.remaining;
+  auto classify = [&](uint32_t u, uint8_t f, bool& sure, bool& eq) {
+    const bool cand = f & kFlagCandidate;
+    const bool gt = mode == 2 && cand && u > thr;
+    eq = mode == 2 && cand && u == thr;
+    sure = (f & kFlagBase) || (mode == 1 ? cand : gt);
+  };
+  uint32_t u[TPT];
+  uint8_t f[TPT];
+  load8(sb, fl, b * kTopkChunk + tid * TPT, T, u, f);
+  // counts of the chunks before this one (this chunk's own counts past the end of the loop)
+  const int32_t* cnt = a.sc.cnt + (size_t)r * a.sc.max_chunks * 3;
+  int sure_before = 0, eq_before = 0, ens_before = 0;
+  for (uint32_t c = tid; c < nb; c += NT) {
+    if (c < b) {
+      sure_before += cnt[3 * c + 0];
+      eq_before += cnt[3 * c + 1];
+    }
+  }
+  int tot;
+  block_excl_sum(sure_before, wsum, tot);
+  sure_before = tot;
+  block_excl_sum(eq_before, wsum, tot);
+  eq_before = tot;
+  // selected ties of earlier chunks that are not sure rows: every such tie of a chunk wholly under
+  // the budget, none of a chunk wholly over it, and in the straddling chunk those of rank < budget
+  // (found by rescanning it)
   if (tid == 0) {
-    int eb = 0, bchunk = -1, blim = 0;
-    for (uint32_t b = 0; b < nb; ++b) {
-      const int e = __hip_atomic_load(&cnt[3 * b + 1], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    int eb = 0, add = 0, bchunk = -1, blim = 0;
+    for (uint32_t c = 0; c < b; ++c) {
+      const int e = cnt[3 * c + 1];
       const int lim = min(max(need_eq - eb, 0), e);
-      if (lim > 0 && lim < e) {
-        bchunk = (int)b;
+      if (lim == e) add += cnt[3 * c + 2];
+      else if (lim > 0) {
+        bchunk = (int)c;
         blim = lim;
       }
       eb += e;
     }
-    s_bchunk = bchunk;
-    s_blim = blim;
+    s_pre[0] = add;
+    s_pre[1] = bchunk;
+    s_pre[2] = blim;
   }
   __syncthreads();
-  int bsel = 0;   // ties of the boundary chunk with rank < blim that are not sure rows
-  if (s_bchunk >= 0) {
-    load8(sb, fl, s_bchunk * kTopkChunk + tid * TPT, T, u, f);
-    int e_loc = 0;
+  ens_before = s_pre[0];
+  const int bchunk = s_pre[1], blim = s_pre[2];
+  if (bchunk >= 0) {   // block-uniform
+    uint32_t ub[TPT];
+    uint8_t fb[TPT];
+    load8(sb, fl, bchunk * kTopkChunk + tid * TPT, T, ub, fb);
     bool se[TPT], ee[TPT];
+    int e_loc = 0;
 #pragma unroll
     for (int i = 0; i < TPT; ++i) {
-      classify(u[i], f[i], se[i], ee[i]);
+      classify(ub[i], fb[i], se[i], ee[i]);
       e_loc += ee[i];
     }
     int e_tot;
@@ -301,63 +346,25 @@ __global__ __launch_bounds__(NT) void topk_count_kernel(TopkArgs a) {
 #pragma unroll
     for (int i = 0; i < TPT; ++i) {
       if (ee[i]) {
-        mine += (!se[i] && rank < s_blim) ? 1 : 0;
+        mine += (!se[i] && rank < blim) ? 1 : 0;
         ++rank;
       }
     }
+    int bsel;
     block_excl_sum(mine, wsum, bsel);
+    ens_before += bsel;
   }
-  if (tid == 0) {
-    int out = 0, eb = 0;
-    int32_t* pre = a.sc.pre + (size_t)r * a.sc.max_chunks * 2;
-    for (uint32_t b = 0; b < nb; ++b) {
-      const int s = __hip_atomic_load(&cnt[3 * b + 0], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      const int e = __hip_atomic_load(&cnt[3 * b + 1], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      const int ens = __hip_atomic_load(&cnt[3 * b + 2], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      pre[2 * b + 0] = out;
-      pre[2 * b + 1] = eb;
-      const int lim = min(max(need_eq - eb, 0), e);
-      out += s + (lim == e ? ens : ((int)b == s_bchunk ? bsel : 0));
-      eb += e;
-    }
-    a.n_rows[r] = out;
-  }
-}
-
-// Per chunk: ordered compaction of its rows of R at the chunk's offset.
-__global__ __launch_bounds__(NT) void topk_write_kernel(TopkArgs a) {
-  __shared__ int wsum[NWV];
-  const int r = blockIdx.y;
-  const ReqDev rq = a.reqs[r];
-  const int T = rq.T;
-  const uint32_t nb = (uint32_t)((T + kTopkChunk - 1) / kTopkChunk);
-  if (blockIdx.x >= nb) return;
-  const int64_t n = rq.n_reuse;
-  const int64_t k = budget_dev(n, a.ratio);
-  const int mode = select_mode(k, n);
-  const uint32_t* st = a.sc.state + 4 * r;
-  const uint32_t thr = mode == 2 ? st[0] : 0u;
-  const int need_eq = mode == 2 ? (int)st[2] : 0;
-  const int32_t* pre = a.sc.pre + (size_t)r * a.sc.max_chunks * 2;
-  const int out0 = pre[2 * blockIdx.x + 0];
-  const int eq0 = pre[2 * blockIdx.x + 1];
-  const int tid = threadIdx.x;
-  const int t0 = blockIdx.x * kTopkChunk + tid * TPT;
-  uint32_t u[TPT];
-  uint8_t f[TPT];
-  load8(a.scores + rq.tok_off, a.flags + rq.tok_off, t0, T, u, f);
+  const int out0 = sure_before + ens_before;
+  // this chunk
   bool sure[TPT], eq[TPT];
   int ne = 0;
 #pragma unroll
   for (int i = 0; i < TPT; ++i) {
-    const bool cand = f[i] & kFlagCandidate;
-    const bool gt = mode == 2 && cand && u[i] > thr;
-    eq[i] = mode == 2 && cand && u[i] == thr;
-    sure[i] = (f[i] & kFlagBase) || (mode == 1 ? cand : gt);
+    classify(u[i], f[i], sure[i], eq[i]);
     ne += eq[i];
   }
   int te;
-  int erank = eq0 + block_excl_sum(ne, wsum, te);
+  int erank = eq_before + block_excl_sum(ne, wsum, te);
   bool in[TPT];
   int ni = 0;
 #pragma unroll
@@ -369,10 +376,17 @@ __global__ __launch_bounds__(NT) void topk_write_kernel(TopkArgs a) {
   int ti;
   int pos = out0 + block_excl_sum(ni, wsum, ti);
   int32_t* out = a.rows + rq.tok_off;
+  const int t0 = b * kTopkChunk + tid * TPT;
 #pragma unroll
   for (int i = 0; i < TPT; ++i) {
     if (in[i] && pos < T) out[pos] = t0 + i;   // (pos < T always holds; it keeps a write in the request)
     pos += in[i];
+  }
+  if (b == nb - 1 && tid == 0) a.n_rows[r] = out0 + ti;
+  if (b == 0 && mode == 2) {
+    // every launch that reads the histograms has finished: clear them for the next call
+    uint32_t* gh = a.sc.hist + (size_t)r * 3 * NBINS;
+    for (int i = tid; i < 3 * NBINS; i += NT) gh[i] = 0u;
   }
 }
 

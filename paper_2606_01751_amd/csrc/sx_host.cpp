@@ -351,9 +351,9 @@ sx_status sx_plan_create(const sx_layer_desc* desc, const sx_request* requests, 
   if (st == SX_OK) st = dev_alloc(p, &p->d_lse, (size_t)total * desc->n_q_heads);
   if (st == SX_OK) st = dev_alloc(p, &p->d_colsum, (size_t)total * desc->n_kv_heads);
   if (st == SX_OK) {
-    // selection scratch, zeroed once: every call leaves the histograms and counters at zero
+    // selection scratch, zeroed once: every call leaves the histograms at zero
     const int64_t chunks = (p->max_T + sx::kTopkChunk - 1) / sx::kTopkChunk;
-    const size_t words = (size_t)n_requests * (sx::kTopkBins + 1 + 4 + 5 * chunks);
+    const size_t words = (size_t)n_requests * (3 * sx::kTopkBins + 12 + 3 * chunks);
     st = dev_alloc(p, &p->d_topk, words);
     if (st == SX_OK) {
       hipError_t e = hipMemset(p->d_topk, 0, words * sizeof(uint32_t));
@@ -361,15 +361,11 @@ sx_status sx_plan_create(const sx_layer_desc* desc, const sx_request* requests, 
     }
     if (st == SX_OK) {
       uint32_t* w = p->d_topk;
-      p->topk.hist = w;
-      w += (size_t)n_requests * sx::kTopkBins;
-      p->topk.ctr = w;
-      w += n_requests;
+      p->topk.hist = w;   // 16-byte aligned rows: 3 x 2048 words per request
+      w += (size_t)n_requests * 3 * sx::kTopkBins;
       p->topk.state = w;
-      w += (size_t)n_requests * 4;
+      w += (size_t)n_requests * 12;
       p->topk.cnt = (int32_t*)w;
-      w += (size_t)n_requests * 3 * chunks;
-      p->topk.pre = (int32_t*)w;
       p->topk.max_chunks = (int32_t)chunks;
     }
   }

@@ -35,18 +35,16 @@ struct RealignRow {
   int32_t pad;
 };
 
-// Selection scratch (plan-owned, zeroed when the plan is made; every pass leaves it clean): per
-// request a radix histogram [kTopkBins] and an arrival counter, the selection state (digits found,
-// digit mask, ties still needed) [4], and per chunk of kTopkChunk tokens the counts (sure rows,
-// ties, ties that are not sure rows) [3] and the output offset and tie rank [2].
+// Selection scratch (plan-owned; the histograms are zeroed when the plan is made and cleared again
+// by every call's last pass): per request the radix histograms of the three passes [3][kTopkBins],
+// the selection state (digits found, digit mask, candidates still needed) after each pass [3][4], and
+// per chunk of kTopkChunk tokens the counts (sure rows, ties, ties that are not sure rows) [3].
 constexpr int kTopkChunk = 2048;
 constexpr int kTopkBins = 2048;
 struct TopkScratch {
-  uint32_t* hist;    // [n_req][kTopkBins]
-  uint32_t* ctr;     // [n_req]
-  uint32_t* state;   // [n_req][4]
+  uint32_t* hist;    // [n_req][3][kTopkBins]
+  uint32_t* state;   // [n_req][3][4]
   int32_t* cnt;      // [n_req][max_chunks][3]
-  int32_t* pre;      // [n_req][max_chunks][2]
   int32_t max_chunks;
 };
 
