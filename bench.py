@@ -83,7 +83,8 @@ KERNELS = {
     # two-pass scoring only (layers without a preceding full layer)
     "attn_mfma_kernel<128, true, false>": ("sx_sparseq_score", "k_attn.hip", False),
     "lse_merge_kernel": ("sx_sparseq_score", "k_attn.hip", False),
-    "colsum2_kernel<128>": ("sx_sparseq_score", "k_attn.hip", True),
+    "colsum_kernel<128, 2>": ("sx_sparseq_score", "k_attn.hip", True),
+    "colsum_kernel<128, 1>": ("sx_sparseq_score", "k_attn.hip", True),
     "probe_gather_kernel<128>": ("sx_sparseq_score", "k_attn.hip", False),
     "head_reduce_kernel": ("sx_sparseq_score", "k_copy.hip", False),
     "realign_kernel": ("sx_rope_realign", "k_copy.hip", True),

@@ -617,11 +617,12 @@ __global__ __launch_bounds__(256) void lse_merge_kernel(const ReqDev* __restrict
   lse[(int64_t)(rq.tok_off + i) * Hq + h] = lse_base2 ? lse2 : lse2 * 0.69314718055994531f;
 }
 
-constexpr int CS_KEYS = 256;   // keys per column-sum workgroup (8 waves x 32)
+constexpr int CS_WAVE_KEYS = 32;   // keys per key tile of a column-sum wave
 
-// Gather of the Sparse-Q probe columns for colsum2_kernel: the query rows of every probe row
-// (all heads) and the base-2 log-sum-exp of every (probe row, query head), in probe order, so
-// that the column-sum kernel computes every address from its registers (no load chains).
+// Gather of the Sparse-Q probe columns for colsum_kernel: the query rows of every probe row
+// and the base-2 log-sum-exp of every (probe row, query head), in probe order and grouped by KV
+// head ([Hkv][probe row][G] for both, so a chunk of one KV head's columns is contiguous), so that
+// the column-sum kernel computes every address from its registers (no load chains).
 // Thread: one 16-byte piece of one (probe row, head); blockIdx.y = request.
 template <int D>
 __global__ __launch_bounds__(256) void probe_gather_kernel(const uint16_t* __restrict__ q, const float* __restrict__ lse,
@@ -640,25 +641,29 @@ __global__ __launch_bounds__(256) void probe_gather_kernel(const uint16_t* __res
   const int pc = rem - h * PPH;
   const int pos = probe[rq.tok_off + i];
   const int64_t prow = (int64_t)rq.p_off + i;
-  ((uint4*)qp)[(prow * Hq + h) * PPH + pc] = ((const uint4*)q)[((int64_t)(rq.tok_off + pos) * Hq + h) * PPH + pc];
+  const int G = Hq / Hkv;
+  const int kvh = h / G;
+  ((uint4*)qp)[(((int64_t)kvh * (n_probe_total + kProbePad) + prow) * G + (h - kvh * G)) * PPH + pc] =
+      ((const uint4*)q)[((int64_t)(rq.tok_off + pos) * Hq + h) * PPH + pc];
   if (pc == 0) {
-    const int G = Hq / Hkv;
-    const int kvh = h / G;
     const float l2 = lse_tok ? lse[(int64_t)(rq.tok_off + pos) * Hq + h] * 1.4426950408889634f
                              : lse[(int64_t)(rq.tok_off + i) * Hq + h];
     lse2p[((int64_t)kvh * (n_probe_total + kProbePad) + prow) * G + (h - kvh * G)] = l2;
   }
 }
 
-// Sparse-Q column sums from the gathered probe columns, key-stationary: a workgroup owns 256 keys
-// of one KV head (8 waves x 32, a wave's 32 keys held as the MFMA A operand) and computes
-// S^T = K Q^T, p = 2^(scale*log2e*s - lse2) masked causally, summed per key.  The probe columns
-// (probe row x query head of the group) stream in chunks of RC probe rows x G heads (at most 64
-// columns, two 32-column MFMA groups) that move global -> LDS directly: the query rows (16 bytes
-// per lane, XOR-swizzled 16-byte chunks), the chunk's 64 log-sum-exps and its RC probe positions
-// (4 bytes per lane), triple-buffered and issued two chunks ahead.  No global load in the loop
+// Sparse-Q column sums from the gathered probe columns, key-stationary: a workgroup owns
+// 8 x 32 x NKT keys of one KV head (a wave's NKT tiles of 32 keys held in registers as the MFMA B
+// operand) and computes S = Q K^T, p = 2^(scale*log2e*s - lse2) masked causally, summed per key.
+// In this orientation a lane's accumulator elements all belong to one key (its lane) and 16 probe
+// columns, so a key's sum is a per-lane sum: one fp32 partial per key tile, flushed every chunk
+// into an fp64 total.  Each query-operand read from LDS feeds NKT MFMAs.  The probe columns (probe
+// row x query head of the group) stream in chunks of RC probe rows x G heads (at most 64 columns,
+// two 32-column MFMA groups) that move global -> LDS directly: the query rows (16 bytes per lane,
+// XOR-swizzled 16-byte chunks), the chunk's 64 log-sum-exps and 64 probe positions (one per column
+// slot, 4 bytes per lane), triple-buffered and issued two chunks ahead.  No global load in the loop
 // feeds an address, so the loop waits only for transfers issued two chunks earlier.
-struct Colsum2K {
+struct ColsumK {
   const uint16_t* k;
   const uint16_t* qp;
   const float* lse2p;
@@ -671,9 +676,10 @@ struct Colsum2K {
   float scale_log2;
 };
 
-template <int D>
-__global__ __launch_bounds__(512, 1) void colsum2_kernel(Colsum2K a) {
+template <int D, int NKT>
+__global__ __launch_bounds__(512, 1) void colsum_kernel(ColsumK a) {
   constexpr int NW = 8;
+  constexpr int KEYS = NW * CS_WAVE_KEYS * NKT;   // keys per workgroup
   constexpr int ROWB = D * 2;                 // bytes of one query row (one column)
   constexpr int NCH = ROWB / 16;              // 16-byte chunks per column
   constexpr int CPP = 1024 / ROWB;            // columns per 1 KB transfer
@@ -698,20 +704,22 @@ __global__ __launch_bounds__(512, 1) void colsum2_kernel(Colsum2K a) {
   // stream the same request's probe columns
   int r, kt;
   locate_request((int)(blockIdx.x / (unsigned)a.Hkv), a.n_req,
-                 [&](int rr) { return (a.reqs[rr].T + CS_KEYS - 1) / CS_KEYS; }, &r, &kt);
+                 [&](int rr) { return (a.reqs[rr].T + KEYS - 1) / KEYS; }, &r, &kt);
   if (r < 0) return;
   r = __builtin_amdgcn_readfirstlane(r);
   kt = __builtin_amdgcn_readfirstlane(kt);
   const ReqDev rq = a.reqs[r];
   const int T = rq.T;
-  const int j0 = kt * CS_KEYS;
-  const int jw = j0 + w * 32;
+  const int j0 = kt * KEYS;
+  const int jw = j0 + w * (CS_WAVE_KEYS * NKT);   // the wave's first key
   const int G = a.G;
   const int RC = a.RC;
   const int ncol = RC * G;                    // columns of a full chunk (<= 64)
-  bf16x8_t ka[D / 16];
-  {
-    const int key = jw + l32;
+  // B operand of key tile t: lane (l32, hg) holds dims 16 s + 8 hg .. + 7 of key jw + 32 t + l32
+  bf16x8_t kb[NKT][D / 16];
+#pragma unroll
+  for (int t = 0; t < NKT; ++t) {
+    const int key = jw + CS_WAVE_KEYS * t + l32;
     const uint16_t* kp = nullptr;
     if (key < T) {
       const int32_t blk = a.bt[rq.bt_off + (key >> 4)];
@@ -720,7 +728,7 @@ __global__ __launch_bounds__(512, 1) void colsum2_kernel(Colsum2K a) {
 #pragma unroll
     for (int s = 0; s < D / 16; ++s) {
       uint4 v = kp ? *(const uint4*)(kp + 16 * s) : make_uint4(0, 0, 0, 0);
-      ka[s] = __builtin_bit_cast(bf16x8_t, v);
+      kb[t][s] = __builtin_bit_cast(bf16x8_t, v);
     }
   }
   const int32_t* probe = a.probe + rq.tok_off;
@@ -732,41 +740,65 @@ __global__ __launch_bounds__(512, 1) void colsum2_kernel(Colsum2K a) {
   }
   const int nchunk = (np - lo + RC - 1) / RC;
   // ---- transfers of chunk k into buffer k mod NBUF (this wave's share).  Rows past the request's
-  // probe rows read the zeroed padding (at most RC - 1 < kProbePad rows), so no clamping ----
+  // probe rows read the padding (at most RC - 1 < kProbePad rows), so no clamping.  A chunk's query
+  // rows are contiguous (column c of the chunk at c * D from its start); each 1 KB query piece is
+  // a wave-uniform chunk base (scalar) plus a fixed per-lane offset. ----
   // query pieces: slot column qc = CPP * piece + lane / NCH, physical chunk lane % NCH holding
   // logical chunk (lane % NCH) ^ (qc mod NCH); slot columns past RC * G repeat column RC * G - 1
-  const uint16_t* q_src[PPW];
+  uint32_t q_voff[PPW];
 #pragma unroll
   for (int i = 0; i < PPW; ++i) {
     const int qc = CPP * (wu + NW * i) + lane / NCH;
     const int cc = min(qc, ncol - 1);
-    const int row = cc / G;
     const int lc = (lane % NCH) ^ (qc & (NCH - 1));
-    q_src[i] = a.qp + (((int64_t)rq.p_off + lo + row) * a.Hq + kvh * G + (cc - row * G)) * D + lc * 8;
+    q_voff[i] = (uint32_t)((cc * D + lc * 8) * 2);
   }
-  const int m_col = min(lane, ncol - 1);       // log-sum-exp transfer (wave NW-1): column
+  const uint16_t* q_base = a.qp + ((int64_t)kvh * (a.n_probe_total + kProbePad) + rq.p_off + lo) * G * D;
+  const int64_t q_step = (int64_t)RC * G * D;   // one chunk further
+  // per-column metadata (column slot = lane): log-sum-exp (wave NW-1) and probe position (wave NW-2).
+  // Slots past RC * G (G not dividing 64) read the log-sum-exp padding, +inf, so they add 0.
+  const int m_col = min(lane, ncol - 1);
   const int m_row = m_col / G;
   const float* l_src =
-      a.lse2p + ((int64_t)kvh * (a.n_probe_total + kProbePad) + rq.p_off + lo + m_row) * G + (m_col - m_row * G);
-  const int32_t* p_src = probe + lo + lane;   // positions transfer (wave NW-2)
-  const int64_t q_step = (int64_t)RC * a.Hq * D;   // one chunk further
+      lane < ncol
+          ? a.lse2p + ((int64_t)kvh * (a.n_probe_total + kProbePad) + rq.p_off + lo + m_row) * G + (m_col - m_row * G)
+          : a.lse2p + ((int64_t)kvh * (a.n_probe_total + kProbePad) + a.n_probe_total) * G;
+  const int l_step = lane < ncol ? RC * G : 0;
+  const uint32_t p_voff = (uint32_t)(m_row * 4);
   const bool lse_wave = wu == NW - 1, pos_wave = wu == NW - 2;
   const int n_mine = PPW + (lse_wave ? 1 : 0) + (pos_wave ? 1 : 0);
-  auto dma16 = [&](const void* src, const char* dst) {
-    const uint32_t m0 = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) const char*)dst;
-    asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(src), "s"(m0) : "m0", "memory");
+  // wave-uniform 64-bit base in an SGPR pair (readfirstlane makes the uniformity visible; each half
+  // goes through uint32_t so that nothing is sign-extended)
+  auto sgpr_base = [](const void* ptr) -> uint64_t {
+    const uint64_t sb = (uint64_t)(uintptr_t)ptr;
+    const uint32_t lo32 = (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)sb);
+    const uint32_t hi32 = (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)(sb >> 32));
+    return ((uint64_t)hi32 << 32) | (uint64_t)lo32;
   };
-  auto dma4 = [&](const void* src, const char* dst) {
-    const uint32_t m0 = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) const char*)dst;
+  // (dst: LDS byte address, wave-uniform)
+  auto dma16_sb = [&](uint64_t sbase, uint32_t voffset, uint32_t dst) {
+    const uint32_t m0 = (uint32_t)__builtin_amdgcn_readfirstlane((int)dst);
+    asm volatile("s_mov_b32 m0, %2\n\tglobal_load_lds_dwordx4 %0, %1" ::"v"(voffset), "s"(sbase), "s"(m0)
+                 : "m0", "memory");
+  };
+  auto dma4_sb = [&](uint64_t sbase, uint32_t voffset, uint32_t dst) {
+    const uint32_t m0 = (uint32_t)__builtin_amdgcn_readfirstlane((int)dst);
+    asm volatile("s_mov_b32 m0, %2\n\tglobal_load_lds_dword %0, %1" ::"v"(voffset), "s"(sbase), "s"(m0)
+                 : "m0", "memory");
+  };
+  auto dma4 = [&](const void* src, uint32_t dst) {
+    const uint32_t m0 = (uint32_t)__builtin_amdgcn_readfirstlane((int)dst);
     asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dword %0, off" ::"v"(src), "s"(m0) : "m0", "memory");
   };
+  const uint32_t smem_lds = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) char*)smem;
   auto issue = [&](int k) {
     if (k >= nchunk) return;
-    char* b = smem + (k % NBUF) * CHB;
+    const uint32_t b = smem_lds + (uint32_t)((k % NBUF) * CHB);
+    const uint64_t qb = sgpr_base(q_base + k * q_step);
 #pragma unroll
-    for (int i = 0; i < PPW; ++i) dma16(q_src[i] + k * q_step, b + (wu + NW * i) * 1024);
-    if (lse_wave) dma4(l_src + k * RC * G, b + QB);
-    if (pos_wave) dma4(p_src + k * RC, b + QB + 256);
+    for (int i = 0; i < PPW; ++i) dma16_sb(qb, q_voff[i], b + (uint32_t)((wu + NW * i) * 1024));
+    if (lse_wave) dma4(l_src + k * l_step, b + QB);
+    if (pos_wave) dma4_sb(sgpr_base(probe + lo + k * RC), p_voff, b + QB + 256);
   };
   auto wait_vm = [&](int n) {
     switch (n) {
@@ -791,26 +823,24 @@ __global__ __launch_bounds__(512, 1) void colsum2_kernel(Colsum2K a) {
     for (int c = 2; c < NBUF; ++c) n += k + c < nchunk ? n_mine : 0;
     return n;
   };
-  // chunks whose first probe row lies before the workgroup's last key may miss keys of a wave
-  // (causal mask); the later ones see all 256 keys.  Probe rows ascend, so the masked chunks come
-  // first: nmask of them.
+  // Chunks whose first probe row lies before the workgroup's last key may miss keys (causal mask),
+  // and the last chunk may hold fewer than RC probe rows; both take the checked path.  Probe rows
+  // ascend, so the masked chunks come first: nmask of them.
   int hm = lo, hx = np;
   while (hm < hx) {
     const int mid = (hm + hx) >> 1;
-    if (probe[mid] < j0 + CS_KEYS - 1) hm = mid + 1; else hx = mid;
+    if (probe[mid] < j0 + KEYS - 1) hm = mid + 1; else hx = mid;
   }
   const int nmask = min(nchunk, (hm - lo + RC - 1) / RC);
+  const bool last_partial = (np - lo) % RC != 0;
+  const int nfast = last_partial ? nchunk - 1 : nchunk;   // chunks [nmask, nfast) take the fast path
 
-  // compute lanes: column 32 gi + l32 of a chunk is probe row (32 gi + l32) / G of it
-  int c_row[2];
+  double acc64[NKT];
+  float acc32[NKT];
 #pragma unroll
-  for (int gi = 0; gi < 2; ++gi) c_row[gi] = (32 * gi + l32) / G;
-  double acc64[16];
-  float acc32[16];
-#pragma unroll
-  for (int e = 0; e < 16; ++e) {
-    acc64[e] = 0.0;
-    acc32[e] = 0.f;
+  for (int t = 0; t < NKT; ++t) {
+    acc64[t] = 0.0;
+    acc32[t] = 0.f;
   }
   // K must be in registers before the first transfer wait (the compiler does not count the
   // transfers, so a later wait of its own for K would also wait for them)
@@ -820,118 +850,143 @@ __global__ __launch_bounds__(512, 1) void colsum2_kernel(Colsum2K a) {
   wait_vm(inflight(-1));   // chunk 0 has landed
   __syncthreads();
   const float c2 = a.scale_log2;
-  // S^T of column group gi of the chunk in buffer b
-  auto s_group = [&](const char* b, int gi) -> f32x16_t {
-    f32x16_t r = {};
-    const int c = 32 * gi + l32;
+  // operand reads add a loop-invariant lane offset to a wave-uniform buffer address (one vector
+  // add per k-step; the column group is an immediate)
+  uint32_t q_off[D / 16];
+#pragma unroll
+  for (int st = 0; st < D / 16; ++st) {
+    const int ci = 2 * st + hg;
+    q_off[st] = (uint32_t)(l32 * ROWB + ((ci ^ (l32 & (NCH - 1))) << 4));
+  }
+  auto lds16 = [](uint32_t addr) -> bf16x8_t {
+    return *(const __attribute__((address_space(3))) bf16x8_t*)(uintptr_t)addr;
+  };
+  // S of the chunk in the buffer at Cb against the NKT key tiles, column group gi in s[gi]: lane
+  // (l32, hg), element e holds column 32 gi + 8 (e / 4) + 4 hg + e % 4 of the chunk and key
+  // jw + 32 t + l32
+  struct SG {
+    f32x16_t s[NKT];
+  };
+  SG sg[2];
+  auto matrix_phase = [&](int j) {
+    if (j >= nchunk) return;
+    uint32_t Cb = (uint32_t)__builtin_amdgcn_readfirstlane((int)(smem_lds + (uint32_t)((j % NBUF) * CHB)));
+    asm volatile("" : "+s"(Cb));
+    __builtin_amdgcn_s_setprio(2);
+#pragma unroll
+    for (int gi = 0; gi < 2; ++gi)
+#pragma unroll
+      for (int t = 0; t < NKT; ++t) sg[gi].s[t] = f32x16_t{};
 #pragma unroll
     for (int st = 0; st < D / 16; ++st) {
-      const int ci = 2 * st + hg;
-      const bf16x8_t bq = *(const bf16x8_t*)(b + c * ROWB + ((ci ^ (c & (NCH - 1))) << 4));
-      r = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka[st], bq, r, 0, 0, 0);
-    }
-    return r;
-  };
-  // column metadata of group gi of chunk k (buffer b): base-2 log-sum-exp (+inf past the chunk,
-  // so those columns add 0) and probe position
-  struct Meta {
-    float l2;
-    int pos;
-  };
-  auto meta = [&](const char* b, int k, int gi) -> Meta {
-    const float* lseb = (const float*)(b + QB);
-    const int* posb = (const int*)(b + QB + 256);
-    const int nvalid = min(RC, np - (lo + k * RC)) * G;
-    const int c = 32 * gi + l32;
-    const bool valid = c < nvalid;
-    return Meta{valid ? lseb[c] : INFINITY, valid ? posb[c_row[gi]] : -1};
-  };
-  auto accumulate = [&](const f32x16_t& sv, const Meta& m, auto masked) {
+      uint32_t qa_addr = Cb + q_off[st];
+      asm volatile("" : "+v"(qa_addr));
 #pragma unroll
-    for (int e = 0; e < 16; ++e) {
-      float p = __builtin_amdgcn_exp2f(__builtin_fmaf(sv[e], c2, -m.l2));
-      if constexpr (decltype(masked)::value) {
-        const int key = jw + (e >> 2) * 8 + hg * 4 + (e & 3);
-        p = key <= m.pos ? p : 0.f;
-      }
-      acc32[e] += p;
-    }
-  };
-  // Software pipeline inside the wave: the MFMAs of one column group run while the vector ALU
-  // takes the exponentials of the previous group.  Iteration k: [S(k, 1) | sums of (k, 0)],
-  // barrier (chunk k + 1 has landed), [S(k + 1, 0) | sums of (k, 1)].  Past the last chunk the
-  // products read a stale buffer whose columns are all masked (never used).
-  auto interleave = [&](auto masked) {
-    constexpr int nv = decltype(masked)::value ? 10 : 6;   // vector instructions per MFMA
-    SX_SG(kSgDsRead, D / 16);
+      for (int gi = 0; gi < 2; ++gi) {
+        const bf16x8_t qa = lds16(qa_addr + (uint32_t)(gi * 32 * ROWB));
 #pragma unroll
-    for (int i = 0; i < D / 16; ++i) {
-      SX_SG(kSgMfma, 1);
-      SX_SG(kSgValu, nv);
-    }
-  };
-  f32x16_t s0 = {}, s1;
-  Meta m0{}, m1{};
-  if (nchunk > 0) {
-    m0 = meta(smem, 0, 0);
-    m1 = meta(smem, 0, 1);
-    s0 = s_group(smem, 0);
-  }
-  // one chunk; `phase` is k mod NBUF when known at compile time (the buffer bases then fold into
-  // the LDS reads' immediate offsets), else -1
-  auto body = [&](int k, auto masked, auto phase) {
-    constexpr int PH = decltype(phase)::value;
-    issue(k + NBUF - 1);
-    const char* b = smem + (PH >= 0 ? PH : k % NBUF) * CHB;
-    s1 = s_group(b, 1);
-    accumulate(s0, m0, masked);
-    interleave(masked);
-    const Meta m1k = m1;
-    wait_vm(inflight(k));   // this wave's transfers of chunk k + 1 have landed
-    __syncthreads();
-    const char* bn = smem + (PH >= 0 ? (PH + 1) % NBUF : (k + 1) % NBUF) * CHB;
-    m0 = meta(bn, k + 1, 0);
-    m1 = meta(bn, k + 1, 1);
-    s0 = s_group(bn, 0);
-    accumulate(s1, m1k, masked);
-    interleave(masked);
-    if ((k & 3) == 3) {
-#pragma unroll
-      for (int e = 0; e < 16; ++e) {
-        acc64[e] += (double)acc32[e];
-        acc32[e] = 0.f;
+        for (int t = 0; t < NKT; ++t)
+          sg[gi].s[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(qa, kb[t][st], sg[gi].s[t], 0, 0, 0);
       }
     }
+    sched_pipelined<2 * NKT * (D / 16), 1, 4>();
+    __builtin_amdgcn_s_setprio(0);
   };
-  using dyn = std::integral_constant<int, -1>;
-  using p0 = std::integral_constant<int, 0>;
-  using p1 = std::integral_constant<int, 1>;
-  using p2 = std::integral_constant<int, 2>;
-  using p3 = std::integral_constant<int, 3>;
-  using p4 = std::integral_constant<int, 4>;
-  int k = 0;
-  for (; k < nmask; ++k) body(k, std::true_type{}, dyn{});
-  for (; k < nchunk && k % NBUF != 0; ++k) body(k, std::false_type{}, dyn{});
-  for (; k + NBUF <= nchunk; k += NBUF) {
-    body(k, std::false_type{}, p0{});
-    body(k + 1, std::false_type{}, p1{});
-    body(k + 2, std::false_type{}, p2{});
-    if constexpr (NBUF > 3) body(k + 3, std::false_type{}, p3{});
-    if constexpr (NBUF > 4) body(k + 4, std::false_type{}, p4{});
-  }
-  for (; k < nchunk; ++k) body(k, std::false_type{}, dyn{});
+  // sums of chunk j.  Fast path: every column valid, no mask.  Checked path: column c counts for
+  // key j when c < nvalid and j <= its probe position.
+  auto vector_phase = [&](int j, auto checked) {
+    uint32_t Mb = (uint32_t)__builtin_amdgcn_readfirstlane((int)(smem_lds + (uint32_t)((j % NBUF) * CHB + QB)));
+    asm volatile("" : "+s"(Mb));
+    const uint32_t lb = Mb + (uint32_t)(16 * hg);
 #pragma unroll
-  for (int e = 0; e < 16; ++e) acc64[e] += (double)acc32[e];
+    for (int gi = 0; gi < 2; ++gi) {
+      float l2[16];
 #pragma unroll
-  for (int e = 0; e < 16; ++e)
+      for (int q = 0; q < 4; ++q) {
+        typedef float f32x4_t __attribute__((ext_vector_type(4)));
+        const f32x4_t v = *(const __attribute__((address_space(3))) f32x4_t*)(uintptr_t)(lb + 4 * (32 * gi + 8 * q));
+        l2[4 * q + 0] = v.x;
+        l2[4 * q + 1] = v.y;
+        l2[4 * q + 2] = v.z;
+        l2[4 * q + 3] = v.w;
+      }
+      if constexpr (decltype(checked)::value) {
+        const int nvalid = min(RC, np - (lo + j * RC)) * G;
+        int pos[16];
 #pragma unroll
-    for (int o = 1; o < 32; o <<= 1) acc64[e] += __shfl_xor(acc64[e], o, 64);
-  if (l32 == 0) {
+        for (int q = 0; q < 4; ++q) {
+          typedef int i32x4_t __attribute__((ext_vector_type(4)));
+          const i32x4_t v = *(const __attribute__((address_space(3))) i32x4_t*)(uintptr_t)(lb + 256 + 4 * (32 * gi + 8 * q));
+          const int c0 = 32 * gi + 8 * q + 4 * hg;
+          pos[4 * q + 0] = c0 + 0 < nvalid ? v.x : -1;
+          pos[4 * q + 1] = c0 + 1 < nvalid ? v.y : -1;
+          pos[4 * q + 2] = c0 + 2 < nvalid ? v.z : -1;
+          pos[4 * q + 3] = c0 + 3 < nvalid ? v.w : -1;
+        }
 #pragma unroll
-    for (int e = 0; e < 16; ++e) {
-      const int key = jw + (e >> 2) * 8 + hg * 4 + (e & 3);
-      if (key < T) a.colsum[(int64_t)kvh * a.total + rq.tok_off + key] = acc64[e];
+        for (int t = 0; t < NKT; ++t) {
+          const int key = jw + CS_WAVE_KEYS * t + l32;
+          float sum = acc32[t];
+#pragma unroll
+          for (int e = 0; e < 16; ++e) {
+            const float p = __builtin_amdgcn_exp2f(__builtin_fmaf(sg[gi].s[t][e], c2, -l2[e]));
+            sum += key <= pos[e] ? p : 0.f;
+          }
+          acc32[t] = sum;
+        }
+      } else {
+#pragma unroll
+        for (int t = 0; t < NKT; ++t) {
+          float sum = acc32[t];
+#pragma unroll
+          for (int e = 0; e < 16; ++e) sum += __builtin_amdgcn_exp2f(__builtin_fmaf(sg[gi].s[t][e], c2, -l2[e]));
+          acc32[t] = sum;
+        }
+      }
     }
+#pragma unroll
+    for (int t = 0; t < NKT; ++t) {
+      acc64[t] += (double)acc32[t];
+      acc32[t] = 0.f;
+    }
+  };
+  auto vphase = [&](int j) {
+    if (j < 0 || j >= nchunk) return;
+    if (j < nmask || j >= nfast) vector_phase(j, std::true_type{});
+    else vector_phase(j, std::false_type{});
+  };
+  // ---- ping-pong: iteration j = 0 .. nchunk has two slots separated by workgroup barriers.  Group
+  // X (waves 0-3) runs the matrix phase of chunk j in slot 1 and its sums in slot 2; group Y (waves
+  // 4-7) the sums of chunk j-1 in slot 1 and the matrix phase of chunk j in slot 2, so in every slot
+  // one wave of each SIMD issues MFMAs while the other exponentiates.  Chunk j + NBUF - 1 is issued
+  // in slot 2 into the buffer of chunk j - 1, whose last reader (Y's sums) ran in slot 1; each wave
+  // waits for its own transfers of chunk j + 1 before the barrier that closes iteration j. ----
+  const int grp = wu >> 2;
+  if (grp == 0) {
+    for (int j = 0; j <= nchunk; ++j) {
+      matrix_phase(j);
+      __syncthreads();
+      issue(j + NBUF - 1);
+      vphase(j);
+      wait_vm(inflight(j));
+      __syncthreads();
+    }
+  } else {
+    for (int j = 0; j <= nchunk; ++j) {
+      vphase(j - 1);
+      __syncthreads();
+      issue(j + NBUF - 1);
+      matrix_phase(j);
+      wait_vm(inflight(j));
+      __syncthreads();
+    }
+  }
+  // the two lane halves hold the same keys (different columns)
+#pragma unroll
+  for (int t = 0; t < NKT; ++t) {
+    const double tot = acc64[t] + __shfl_xor(acc64[t], 32, 64);
+    const int key = jw + CS_WAVE_KEYS * t + l32;
+    if (hg == 0 && key < T) a.colsum[(int64_t)kvh * a.total + rq.tok_off + key] = tot;
   }
 }
 
@@ -1017,7 +1072,7 @@ hipError_t launch_colsum(const sx_plan* p, const ScoreScratch& sc, const void* q
     const hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
-  Colsum2K c{};
+  ColsumK c{};
   c.k = (const uint16_t*)kc;
   c.qp = (const uint16_t*)sc.qp;
   c.lse2p = sc.lse2p;
@@ -1033,11 +1088,18 @@ hipError_t launch_colsum(const sx_plan* p, const ScoreScratch& sc, const void* q
   c.RC = 64 / G;
   c.n_req = p->n_req;
   c.scale_log2 = p->scale * 1.4426950408889634f;
-  const dim3 grid((unsigned)(((p->max_T + CS_KEYS - 1) / CS_KEYS) * c.Hkv * p->n_req));
-  if (D == 128)
-    hipLaunchKernelGGL(colsum2_kernel<128>, grid, dim3(512), 0, s, c);
-  else
-    hipLaunchKernelGGL(colsum2_kernel<64>, grid, dim3(512), 0, s, c);
+  // two key tiles per wave (each staged query column feeds twice the MFMAs and the probe columns
+  // stream half as often) while that still leaves two workgroups per CU, else one
+  const int64_t wg2 = ((p->max_T + 511) / 512) * c.Hkv * p->n_req;
+  if (wg2 >= 512) {
+    const dim3 grid((unsigned)wg2);
+    if (D == 128) hipLaunchKernelGGL((colsum_kernel<128, 2>), grid, dim3(512), 0, s, c);
+    else hipLaunchKernelGGL((colsum_kernel<64, 2>), grid, dim3(512), 0, s, c);
+  } else {
+    const dim3 grid((unsigned)(((p->max_T + 255) / 256) * c.Hkv * p->n_req));
+    if (D == 128) hipLaunchKernelGGL((colsum_kernel<128, 1>), grid, dim3(512), 0, s, c);
+    else hipLaunchKernelGGL((colsum_kernel<64, 1>), grid, dim3(512), 0, s, c);
+  }
   return hipGetLastError();
 }
 

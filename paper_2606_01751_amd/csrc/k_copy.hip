@@ -409,18 +409,22 @@ hipError_t launch_head_reduce(const sx_plan* p, const double* colsum, float* sco
 
 hipError_t launch_probe_pad_clear(const sx_plan* p, const ScoreScratch& sc, hipStream_t s) {
   const int64_t G = p->desc.n_q_heads / p->desc.n_kv_heads;
-  // queries: the kProbePad rows after the last probe row, all heads (bf16 zero = 0)
-  const int64_t qrow = (int64_t)p->desc.n_q_heads * p->desc.head_dim * 2;   // bytes per probe row
+  // queries: the kProbePad rows after the last probe row of every KV head (bf16 zero = 0)
+  const int64_t qrow = G * p->desc.head_dim * 2;   // bytes of one probe row of one KV head
   const int64_t qwords = kProbePad * qrow / 4;
-  hipLaunchKernelGGL(fill_u32_kernel, dim3((unsigned)((qwords + 255) / 256)), dim3(256), 0, s,
-                     (uint32_t*)((char*)sc.qp + p->n_probe * qrow), qwords, 0u);
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
-  // log-sum-exps: the kProbePad rows after the last probe row of every KV head
+  hipError_t e = hipSuccess;
+  for (int h = 0; h < p->desc.n_kv_heads; ++h) {
+    char* base = (char*)sc.qp + ((int64_t)h * (p->n_probe + kProbePad) + p->n_probe) * qrow;
+    hipLaunchKernelGGL(fill_u32_kernel, dim3((unsigned)((qwords + 255) / 256)), dim3(256), 0, s, (uint32_t*)base,
+                       qwords, 0u);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  // log-sum-exps: the kProbePad rows after the last probe row of every KV head (+inf)
   for (int h = 0; h < p->desc.n_kv_heads; ++h) {
     float* base = sc.lse2p + ((int64_t)h * (p->n_probe + kProbePad) + p->n_probe) * G;
     hipLaunchKernelGGL(fill_u32_kernel, dim3((unsigned)((kProbePad * G + 255) / 256)), dim3(256), 0, s,
-                       (uint32_t*)base, (int64_t)kProbePad * G, 0u);
+                       (uint32_t*)base, (int64_t)kProbePad * G, kProbePadLse);
     e = hipGetLastError();
     if (e != hipSuccess) return e;
   }

@@ -370,8 +370,9 @@ sx_status sx_plan_create(const sx_layer_desc* desc, const sx_request* requests, 
     }
   }
   if (st == SX_OK && desc->dtype == SX_BF16) {
-    // gathered probe columns, kProbePad zeroed rows past the last probe row (per KV head for the
-    // log-sum-exps) so that a chunk read past the end stays in bounds and finite
+    // gathered probe columns, kProbePad padding rows past the last probe row (per KV head for the
+    // log-sum-exps) so that a chunk read past the end stays in bounds: zero queries, +inf
+    // log-sum-exps
     const size_t rows = (size_t)p->n_probe + sx::kProbePad;
     uint16_t* qp = nullptr;
     st = dev_alloc(p, &qp, rows * desc->n_q_heads * d);
@@ -384,6 +385,10 @@ sx_status sx_plan_create(const sx_layer_desc* desc, const sx_request* requests, 
     if (st == SX_OK) {
       hipError_t e = hipMemset(p->d_qp, 0, rows * desc->n_q_heads * d * sizeof(uint16_t));
       if (e == hipSuccess) e = hipMemset(p->d_lse2p, 0, rows * desc->n_q_heads * sizeof(float));
+      const int64_t G = desc->n_q_heads / desc->n_kv_heads;
+      for (int h = 0; h < desc->n_kv_heads && e == hipSuccess; ++h)
+        e = hipMemsetD32((hipDeviceptr_t)(p->d_lse2p + ((int64_t)h * rows + p->n_probe) * G), (int)sx::kProbePadLse,
+                         (size_t)sx::kProbePad * G);
       if (e != hipSuccess) st = hip_fail(e, "hipMemset (plan scratch)");
     }
   }
@@ -734,7 +739,8 @@ sx_status sx_sparseq_score_static(const sx_plan* p, const void* q, const void* k
                             bf16 ? (float*)(b + colsum_b + qp_b) : nullptr};
   hipStream_t s = (hipStream_t)stream;
   if (bf16) {
-    // the gathered probe columns' padding rows must be finite: an earlier call may have left anything
+    // the gathered probe columns' padding rows (zero queries, +inf log-sum-exps): an earlier call may
+    // have left anything
     st = check_launch(sx::launch_probe_pad_clear(p, sc, s), "sx_sparseq_score_static padding clear");
     if (st != SX_OK) return st;
   }

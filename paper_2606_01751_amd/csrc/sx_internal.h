@@ -89,7 +89,7 @@ struct sx_plan {
   double* d_colsum = nullptr;     // scratch [Hkv][sum T]
   int32_t* d_tok_pos = nullptr;   // [sum T] RoPE position of every token in the new sequence
   double* d_theta = nullptr;      // [d/2] RoPE frequencies base^(-2i/d), float64
-  void* d_qp = nullptr;           // scratch [n_probe][Hq][d]: query rows of the probe rows (bf16 plans)
+  void* d_qp = nullptr;           // scratch [Hkv][n_probe][Hq / Hkv][d]: query rows of the probe rows (bf16 plans)
   float* d_lse2p = nullptr;       // scratch [Hkv][n_probe][Hq / Hkv]: their base-2 log-sum-exp
   float2* d_lsep = nullptr;       // scratch [kLseSplit][n_probe][Hq]: partials of the split pass (bf16 plans)
   uint32_t* d_topk = nullptr;     // selection scratch, carved into `topk`
@@ -104,15 +104,17 @@ hipError_t launch_realign(const sx_plan* p, const void* src_k, const void* src_v
 hipError_t launch_scatter(const sx_plan* p, const void* k_new, const void* v_new, const int32_t* rows,
                           const int32_t* n_rows, int32_t max_rows, void* kc, void* vc, hipStream_t s);
 // Scratch of the Sparse-Q column sums: per-KV-head float64 sums [Hkv][sum T]; (bf16 plans) the
-// gathered probe columns, queries [n_probe + kProbePad][Hq][d] and base-2 log-sum-exps
-// [Hkv][n_probe + kProbePad][Hq / Hkv], whose kProbePad padding rows must hold finite values.
+// gathered probe columns, queries [Hkv][n_probe + kProbePad][Hq / Hkv][d] and base-2 log-sum-exps
+// [Hkv][n_probe + kProbePad][Hq / Hkv], whose kProbePad padding rows must hold zero queries and
+// +inf log-sum-exps (a column read there adds exp2(-inf) = 0).
+constexpr uint32_t kProbePadLse = 0x7f800000u;   // +inf
 struct ScoreScratch {
   double* colsum;
   void* qp;
   float* lse2p;
 };
 hipError_t launch_head_reduce(const sx_plan* p, const double* colsum, float* scores, hipStream_t s);
-// zeroes the padding rows of the gathered probe columns in `sc`
+// sets the padding rows of the gathered probe columns in `sc` (zero queries, +inf log-sum-exps)
 hipError_t launch_probe_pad_clear(const sx_plan* p, const ScoreScratch& sc, hipStream_t s);
 // fused re-alignment + KV write of n_layers layers (host array of per-layer pointers): marks the
 // rows with `gen` (after clearing every mark when clear_marks), then writes every token's slot of
