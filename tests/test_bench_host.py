@@ -30,7 +30,7 @@ def _setup(tmp_path, monkeypatch, kernels, sources=("k_attn.hip", "k_copy.hip"))
 def test_kernels_inside_a_call_add_up(tmp_path, monkeypatch):
     # the scoring call runs the probe gather, the column sums and the head sum: bytes per call are
     # the sum of the three
-    _setup(tmp_path, monkeypatch, {"colsum2_kernel<128>": (3, 100.0, False),
+    _setup(tmp_path, monkeypatch, {"colsum_kernel<128, 2>": (3, 100.0, False),
                                    "probe_gather_kernel<128>": (3, 20.0, False),
                                    "head_reduce_kernel": (3, 5.0, False)})
     assert bench.load_traffic("w") == pytest.approx({"sx_sparseq_score": 125.0})
