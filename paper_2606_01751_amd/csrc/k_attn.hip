@@ -339,8 +339,11 @@ __global__ __launch_bounds__(512, 1) void attn_mfma_kernel(AttnK a) {
   int k_off[D / 16];
 #pragma unroll
   for (int s = 0; s < D / 16; ++s) k_off[s] = l32 * ROWB + (((2 * s + hg) ^ (l32 & (NCH - 1))) << 4);
-  auto s_body = [&](uint32_t Kb) {
-    asm volatile("" : "+s"(Kb));   // opaque: one add per k-slice, no strength-reduced variants
+  // Kb: the tile's LDS address; `fixed` when it is a compile-time constant (the buffer offset then
+  // folds into the reads' immediate offsets), else made opaque (one add per k-slice, no
+  // strength-reduced variants)
+  auto s_body = [&](uint32_t Kb, auto fixed) {
+    if constexpr (!decltype(fixed)::value) asm volatile("" : "+s"(Kb));
 #pragma unroll
     for (int mt = 0; mt < 2; ++mt)
 #pragma unroll
@@ -348,7 +351,7 @@ __global__ __launch_bounds__(512, 1) void attn_mfma_kernel(AttnK a) {
 #pragma unroll
     for (int s = 0; s < D / 16; ++s) {
       uint32_t kbase = Kb + (uint32_t)k_off[s];
-      asm volatile("" : "+v"(kbase));
+      if constexpr (!decltype(fixed)::value) asm volatile("" : "+v"(kbase));
 #pragma unroll
       for (int mt = 0; mt < 2; ++mt) {
         const bf16x8_t ka = *(const __attribute__((address_space(3))) bf16x8_t*)(uintptr_t)(kbase + (uint32_t)(mt * 32 * ROWB));
@@ -356,8 +359,8 @@ __global__ __launch_bounds__(512, 1) void attn_mfma_kernel(AttnK a) {
       }
     }
   };
-  auto s_tile = [&](uint32_t Kb) {
-    s_body(Kb);
+  auto s_tile = [&](uint32_t Kb, auto fixed) {
+    s_body(Kb, fixed);
     sched_pipelined<D / 8, 1, 4>();
   };
   // online softmax of the tile in sacc (lane value e of M tile mt is key
@@ -447,9 +450,9 @@ __global__ __launch_bounds__(512, 1) void attn_mfma_kernel(AttnK a) {
     const int dchunk = 4 * dt + 2 * (tg & 1) + (tc >> 1);
     vtr_off[dt] = (4 * (tg >> 1) + tk) * ROWB + ((dchunk ^ v_swz<NCH>(tk)) << 4) + (tc & 1) * 8;
   }
-  auto pv_body = [&](uint32_t Vb) {
+  auto pv_body = [&](uint32_t Vb, auto fixed) {
     if constexpr (PV) {
-      asm volatile("" : "+s"(Vb));
+      if constexpr (!decltype(fixed)::value) asm volatile("" : "+s"(Vb));
       // one base address per 32-dim tile for this tile's buffer (the empty asm keeps the compiler
       // from re-associating the sums into one precomputed register per read); every read then
       // adds its row constant as an immediate offset
@@ -457,7 +460,7 @@ __global__ __launch_bounds__(512, 1) void attn_mfma_kernel(AttnK a) {
 #pragma unroll
       for (int dt = 0; dt < D / 32; ++dt) {
         vbase[dt] = Vb + (uint32_t)vtr_off[dt];
-        asm volatile("" : "+v"(vbase[dt]));
+        if constexpr (!decltype(fixed)::value) asm volatile("" : "+v"(vbase[dt]));
       }
 #pragma unroll
       for (int kk = 0; kk < 4; ++kk)
@@ -477,9 +480,9 @@ __global__ __launch_bounds__(512, 1) void attn_mfma_kernel(AttnK a) {
         }
     }
   };
-  auto pv_tile = [&](uint32_t Vb) {
+  auto pv_tile = [&](uint32_t Vb, auto fixed) {
     if constexpr (PV) {
-      pv_body(Vb);
+      pv_body(Vb, fixed);
       sched_pipelined<D / 8, 2, 4>();
     }
   };
@@ -517,18 +520,27 @@ __global__ __launch_bounds__(512, 1) void attn_mfma_kernel(AttnK a) {
   }
   wait_vm(inflight(-1));   // K(0) has landed
   __syncthreads();
-  auto matrix_phase = [&](int j) {
+  // `ph` is j mod NBUF when known at compile time (integral constant >= 0), else -1: the tile
+  // buffers of the iteration are then constants
+  auto matrix_phase = [&](int j, auto ph) {
+    constexpr int PH = decltype(ph)::value;
+    constexpr bool FX = PH >= 0;
     // the wave in its matrix phase issues first: its MFMAs are not held back by the other
     // wave's softmax on the same SIMD
     __builtin_amdgcn_s_setprio(2);
-    if (j >= 1 && (kt0 + j - 1) * KT <= wave_max) pv_tile(vtile_lds(j - 1));
-    if (j < nkt && (kt0 + j) * KT <= wave_max) s_tile(ktile_lds(j));
+    if (j >= 1 && (kt0 + j - 1) * KT <= wave_max)
+      pv_tile(FX ? vbuf_lds + (uint32_t)(((PH + NBUF - 1) % NBUF) * TILEB) : vtile_lds(j - 1),
+              std::integral_constant<bool, FX>{});
+    if (j < nkt && (kt0 + j) * KT <= wave_max)
+      s_tile(FX ? kbuf_lds + (uint32_t)(PH * TILEB) : ktile_lds(j), std::integral_constant<bool, FX>{});
     __builtin_amdgcn_s_setprio(0);
   };
-  auto transfer_phase = [&](int j) {   // this wave's share of K(j+KD) and V(j+VD)
-    if (j + KD < nkt) issue(a.k, k_last, kt0 + j + KD, ktile(j + KD), false);
+  auto transfer_phase = [&](int j, auto ph) {   // this wave's share of K(j+KD) and V(j+VD)
+    constexpr int PH = decltype(ph)::value;
+    if (j + KD < nkt) issue(a.k, k_last, kt0 + j + KD, PH >= 0 ? kbuf + ((PH + KD) % NBUF) * TILEB : ktile(j + KD), false);
     if constexpr (PV) {
-      if (j + VD < nkt) issue(a.v, v_last, kt0 + j + VD, vtile(j + VD), true);
+      if (j + VD < nkt)
+        issue(a.v, v_last, kt0 + j + VD, PH >= 0 ? vbuf + ((PH + VD) % NBUF) * TILEB : vtile(j + VD), true);
     }
     if constexpr (PAGED) {
       // (kt0 is a multiple of 16: local and absolute tile indices agree mod 16.)  Tile j + KD opens
@@ -543,25 +555,39 @@ __global__ __launch_bounds__(512, 1) void attn_mfma_kernel(AttnK a) {
   auto vector_phase = [&](int j) {   // softmax of tile j
     if (j >= 0 && j < nkt && (kt0 + j) * KT <= wave_max) softmax_tile((kt0 + j) * KT);
   };
-  if (grp == 0) {
-    for (int j = 0; j <= nkt; ++j) {
-      matrix_phase(j);
-      __syncthreads();
-      transfer_phase(j);
-      vector_phase(j);
-      wait_vm(inflight(j));   // this wave's transfers of iteration j - NBUF + 3 have landed
-      __syncthreads();
+  auto iter_x = [&](int j, auto ph) {
+    matrix_phase(j, ph);
+    __syncthreads();
+    transfer_phase(j, ph);
+    vector_phase(j);
+    wait_vm(inflight(j));   // this wave's transfers of iteration j - NBUF + 3 have landed
+    __syncthreads();
+  };
+  auto iter_y = [&](int j, auto ph) {
+    transfer_phase(j, ph);
+    vector_phase(j - 1);
+    __syncthreads();
+    matrix_phase(j, ph);
+    wait_vm(inflight(j));
+    __syncthreads();
+  };
+  // The dense kernel runs NBUF iterations per loop trip with static buffer phases (every LDS
+  // offset an immediate); the paged kernel keeps one dynamic iteration (its larger body unrolled
+  // would overflow the instruction cache that two CUs share).
+  auto run = [&](auto iter) {
+    int j = 0;
+    if constexpr (!PAGED) {
+      for (; j + NBUF - 1 <= nkt; j += NBUF) {
+        iter(j, std::integral_constant<int, 0>{});
+        iter(j + 1, std::integral_constant<int, 1>{});
+        iter(j + 2, std::integral_constant<int, 2>{});
+        if constexpr (NBUF == 4) iter(j + 3, std::integral_constant<int, 3>{});
+      }
     }
-  } else {
-    for (int j = 0; j <= nkt; ++j) {
-      transfer_phase(j);
-      vector_phase(j - 1);
-      __syncthreads();
-      matrix_phase(j);
-      wait_vm(inflight(j));
-      __syncthreads();
-    }
-  }
+    for (; j <= nkt; ++j) iter(j, std::integral_constant<int, -1>{});
+  };
+  if (grp == 0) run(iter_x);
+  else run(iter_y);
 
   const float l_tot = l_run + __shfl_xor(l_run, 32, 64);
   if constexpr (PV) {
