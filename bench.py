@@ -93,8 +93,8 @@ KERNELS = {
     "mark_rows_kernel": ("sx_realign_scatter", "k_copy.hip", False),   # (also sx_realign_scatter_layers)
     "fill_u8_kernel": ("sx_rows_mask", "k_copy.hip", True),
     "mask_rows_kernel": ("sx_rows_mask", "k_copy.hip", False),
-    "topk_hist_kernel": ("sx_topk_select", "k_topk.hip", False),   # three radix passes per call
-    "topk_count_kernel": ("sx_topk_select", "k_topk.hip", False),
+    "topk_hist_kernel": ("sx_topk_select", "k_topk.hip", False),
+    "topk_bound_kernel": ("sx_topk_select", "k_topk.hip", False),
     "topk_write_kernel": ("sx_topk_select", "k_topk.hip", True),
 }
 

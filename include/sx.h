@@ -144,6 +144,8 @@ typedef struct sx_plan_info {
  * min(64, len) tokens of the final segment when that segment is reused, Section 3.2), and the
  * float64 cos/sin tables of every cached segment's shift (rounded to float32).
  * n_dst_blocks / n_src_blocks are the pool sizes used to range-check block ids.
+ * Limits (SX_EUNSUPPORTED beyond them): at most 2^31 - 1 tokens in one plan and 2^21 tokens
+ * in one request.
  * Allocates device memory (owned by the plan).  *out is set only on success. */
 sx_status sx_plan_create(const sx_layer_desc* desc, const sx_request* requests, int32_t n_requests,
                          int64_t n_dst_blocks, int64_t n_src_blocks, sx_plan** out);

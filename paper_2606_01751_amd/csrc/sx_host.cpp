@@ -218,6 +218,9 @@ sx_status sx_plan_create(const sx_layer_desc* desc, const sx_request* requests, 
     }
     total += q.n_tokens;
     if (total > INT32_MAX) return fail(SX_EUNSUPPORTED, "more than 2^31 tokens in one plan");
+    if (q.n_tokens > (int64_t)sx::kTopkMaxChunks * sx::kTopkChunk)
+      return fail(SX_EUNSUPPORTED, "request %d: %d tokens; the selection handles up to %d per request", r, q.n_tokens,
+                  sx::kTopkMaxChunks * sx::kTopkChunk);
   }
   {
     // the element-wise kernels give each thread one 16-byte piece of a token row (queries have the
@@ -353,7 +356,7 @@ sx_status sx_plan_create(const sx_layer_desc* desc, const sx_request* requests, 
   if (st == SX_OK) {
     // selection scratch, zeroed once: every call leaves the histograms at zero
     const int64_t chunks = (p->max_T + sx::kTopkChunk - 1) / sx::kTopkChunk;
-    const size_t words = (size_t)n_requests * (3 * sx::kTopkBins + 12 + 3 * chunks);
+    const size_t words = (size_t)n_requests * (sx::kTopkFine + 256 + 4 + 2 * chunks) + 2 * (size_t)total;
     st = dev_alloc(p, &p->d_topk, words);
     if (st == SX_OK) {
       hipError_t e = hipMemset(p->d_topk, 0, words * sizeof(uint32_t));
@@ -361,10 +364,12 @@ sx_status sx_plan_create(const sx_layer_desc* desc, const sx_request* requests, 
     }
     if (st == SX_OK) {
       uint32_t* w = p->d_topk;
-      p->topk.hist = w;   // 16-byte aligned rows: 3 x 2048 words per request
-      w += (size_t)n_requests * 3 * sx::kTopkBins;
+      p->topk.hist = w;   // 16-byte aligned rows of 65536 + 256 words
+      w += (size_t)n_requests * (sx::kTopkFine + 256);
+      p->topk.list = (uint2*)w;   // (8-byte aligned: the histograms fill a multiple of 16 bytes)
+      w += 2 * (size_t)total;
       p->topk.state = w;
-      w += (size_t)n_requests * 12;
+      w += (size_t)n_requests * 4;
       p->topk.cnt = (int32_t*)w;
       p->topk.max_chunks = (int32_t)chunks;
     }

@@ -36,15 +36,19 @@ struct RealignRow {
 };
 
 // Selection scratch (plan-owned; the histograms are zeroed when the plan is made and cleared again
-// by every call's last pass): per request the radix histograms of the three passes [3][kTopkBins],
-// the selection state (digits found, digit mask, candidates still needed) after each pass [3][4], and
-// per chunk of kTopkChunk tokens the counts (sure rows, ties, ties that are not sure rows) [3].
+// by every call's last pass): per request the fine and coarse histograms of the first digit
+// [kTopkFine + 256] and the selection state (first digit, candidates still needed) [4]; per chunk
+// of kTopkChunk tokens the rows surely in R and the number of boundary entries [2]; per token a
+// boundary-list slot (index with a base-row flag, key), a chunk's list filling the slots of its own
+// tokens.
 constexpr int kTopkChunk = 2048;
-constexpr int kTopkBins = 2048;
+constexpr int kTopkFine = 65536;       // first digit: the top 16 bits of a 32-bit key
+constexpr int kTopkMaxChunks = 1024;   // chunks per request: requests up to 2097152 tokens
 struct TopkScratch {
-  uint32_t* hist;    // [n_req][3][kTopkBins]
-  uint32_t* state;   // [n_req][3][4]
-  int32_t* cnt;      // [n_req][max_chunks][3]
+  uint32_t* hist;    // [n_req][kTopkFine + 256]
+  uint32_t* state;   // [n_req][4]
+  int32_t* cnt;      // [n_req][max_chunks][2]
+  uint2* list;       // [sum T]
   int32_t max_chunks;
 };
 

@@ -167,3 +167,12 @@ def test_checked_library_exports_the_same_abi():
         assert _status(_desc(head_dim=96), [_good()])[0] == sx.SX_EUNSUPPORTED
     finally:
         sx.use_checked(False)
+
+
+def test_plan_rejects_requests_beyond_the_selection_limit():
+    # the selection cuts a request into at most 1024 chunks of 2048 tokens
+    d = _desc(n_q_heads=2, n_kv_heads=1, head_dim=64, dtype="bf16")
+    T = (1 << 21) + 16
+    nblk = T // 16
+    st, msg = _status(d, [_Req(T, [_Seg(0, T, 0)], np.arange(nblk), [])], ndst=nblk, nsrc=1)
+    assert st == sx.SX_EUNSUPPORTED and "per request" in msg

@@ -37,12 +37,13 @@ def test_kernels_inside_a_call_add_up(tmp_path, monkeypatch):
 
 
 def test_several_dispatches_of_one_kernel_per_call_add_up(tmp_path, monkeypatch):
-    # a selection call runs three radix passes, a count pass and a write pass: with per-dispatch
-    # means of 10, 20 and 30 bytes over 3 calls, a call moves 3 x 10 + 20 + 30 = 80 bytes
-    _setup(tmp_path, monkeypatch, {"topk_hist_kernel": (9, 10.0, False), "topk_count_kernel": (3, 20.0, False),
+    # dispatches per call come from the dispatch count over the calls: with the histogram kernel
+    # dispatched twice per call (6 over 3 calls) and per-dispatch means of 10, 20 and 30 bytes, a
+    # call moves 2 x 10 + 20 + 30 = 70 bytes
+    _setup(tmp_path, monkeypatch, {"topk_hist_kernel": (6, 10.0, False), "topk_bound_kernel": (3, 20.0, False),
                                    "topk_write_kernel": (3, 30.0, False)},
            sources=("k_topk.hip",))
-    assert bench.load_traffic("w") == pytest.approx({"sx_topk_select": 80.0})
+    assert bench.load_traffic("w") == pytest.approx({"sx_topk_select": 70.0})
 
 
 def test_entry_without_counted_calls_or_with_stale_source_is_dropped(tmp_path, monkeypatch):
