@@ -120,7 +120,10 @@ __global__ __launch_bounds__(512, 1) void attn_mfma_kernel(AttnK a) {
   const int grp = wu >> 2;                    // 0: group X, 1: group Y
   const int l32 = lane & 31;
   const int hg = lane >> 5;
-  const int kvh = (int)(blockIdx.x % (unsigned)a.Hkv);
+  // (the remainder is formed on the vector unit; in the paged kernel the empty asm keeps the uniform
+  // result in a scalar register, so the block addresses built from it stay on the scalar unit)
+  int kvh = __builtin_amdgcn_readfirstlane((int)(blockIdx.x % (unsigned)a.Hkv));
+  if constexpr (PAGED) asm("" : "+s"(kvh));
   const int rpw = a.rpw;
   const int nsplit = (PAGED && !PV) ? a.nsplit : 1;
   // rows of request rr that are processed: the first min(n_rows, max_rows) rows (the rows the KV
@@ -152,6 +155,14 @@ __global__ __launch_bounds__(512, 1) void attn_mfma_kernel(AttnK a) {
   } else {
     tok_off = a.cu[r];
     T = a.cu[r + 1] - tok_off;
+  }
+  if constexpr (PAGED) {
+    // (request fields are workgroup-uniform: scalar registers keep the block address math on the
+    // scalar unit)
+    T = __builtin_amdgcn_readfirstlane(T);
+    tok_off = __builtin_amdgcn_readfirstlane(tok_off);
+    bt_off = __builtin_amdgcn_readfirstlane(bt_off);
+    p_off = __builtin_amdgcn_readfirstlane(p_off);
   }
   nrows = rows_of(r);
   const int ntiles = (nrows + rpw - 1) / rpw;
@@ -194,19 +205,18 @@ __global__ __launch_bounds__(512, 1) void attn_mfma_kernel(AttnK a) {
       qb[s] = __builtin_bit_cast(bf16x8_t, v);
     }
   }
-  // Block table (paged caches): lane l of a wave holds the block of logical block 64 c + l of
-  // window c.  A wave moves rows 8 wu .. 8 wu + 7 of every tile, all inside logical block
-  // 4 t + wu / 2 of tile t, so one readlane per matrix and tile gives the block, with no memory
-  // access in the loop.  Windows c and c + 1 are held; window c + 2 is loaded 16 tiles before its
-  // first use.
+  // Block table (paged caches): a wave moves rows 8 wu .. 8 wu + 7 of every tile, all inside
+  // logical block 4 t + wu / 2 of tile t, so one block id per wave and tile (a scalar load through
+  // the constant address space, clamped to the request's last block for tiles past the end).
   const int nblk = (T + 15) >> 4;
-  int win_c = kt0 >> 4;   // window c: blocks of key tiles 16 c .. 16 c + 15 (kt0 is a multiple of 16)
-  int32_t win0 = 0, win1 = 0;
-  auto load_win = [&](int c) -> int32_t { return a.bt[bt_off + min(64 * c + lane, nblk - 1)]; };
-  if constexpr (PAGED) {
-    win0 = load_win(win_c);
-    win1 = load_win(win_c + 1);
-  }
+  auto blk_of = [&](int kt) -> int32_t {
+    if constexpr (PAGED) {
+      const __attribute__((address_space(4))) int32_t* btc = (const __attribute__((address_space(4))) int32_t*)a.bt;
+      return btc[__builtin_amdgcn_readfirstlane(bt_off + min(4 * kt + (wu >> 1), nblk - 1))];
+    } else {
+      return 0;
+    }
+  };
   // Q must be complete before any tile transfer is issued: the compiler does not see those
   // transfers, so a later wait of its own for Q would also wait for them.
   SX_WAIT_VMCNT(0);
@@ -236,15 +246,11 @@ __global__ __launch_bounds__(512, 1) void attn_mfma_kernel(AttnK a) {
       return base + ((int64_t)(tok_off + key16 * 16) * a.Hkv + kvh) * D;
     }
   };
-  // base of the (block, head) run of logical block key16 (inside windows win_c, win_c + 1)
-  auto block_base_w = [&](const uint16_t* base, int key16) -> const uint16_t* {
-    if constexpr (PAGED) {
-      const int32_t wv = (key16 >> 6) == win_c ? win0 : win1;
-      const int32_t blk = __builtin_amdgcn_readlane(wv, key16 & 63);
-      return base + (((int64_t)blk * a.Hkv + kvh) * 16) * D;
-    } else {
-      return block_base(base, key16);
-    }
+  // base of the rows this wave moves in key tile kt: the (block, head) run of block blk (paged), or
+  // the tile's 16-row group of this wave (dense; rows past the end are not read through it)
+  auto wave_base = [&](const uint16_t* base, int kt, int32_t blk) -> const uint16_t* {
+    if constexpr (PAGED) return base + (((int64_t)blk * a.Hkv + kvh) * 16) * D;
+    else return block_base(base, ((kt * KT) >> 4) + (wu >> 1));
   };
   constexpr int64_t kRowPaged = D;
   const int64_t rstride = PAGED ? kRowPaged : (int64_t)a.Hkv * D;   // elements between rows of a block
@@ -280,11 +286,11 @@ __global__ __launch_bounds__(512, 1) void attn_mfma_kernel(AttnK a) {
     koff[i] = (uint32_t)(((rr & 15) * rstride + (pchunk ^ (rr & (NCH - 1))) * 8) * 2);
     voff[i] = (uint32_t)(((rr & 15) * rstride + (pchunk ^ v_swz<NCH>(rr)) * 8) * 2);
   }
-  // transfer of this wave's share of one matrix (K or V) tile kt into dst
-  auto issue = [&](const uint16_t* base, const uint16_t* row_last, int kt, char* dst, bool is_v) {
+  // transfer of this wave's share of one matrix (K or V) tile kt into dst; blk = blk_of(kt)
+  auto issue = [&](const uint16_t* base, const uint16_t* row_last, int kt, char* dst, bool is_v, int32_t blk) {
     const int kbase = kt * KT;
     if (kbase + KT - 1 <= last_key) {
-      const uint16_t* b = block_base_w(base, (kbase >> 4) + (wu >> 1));
+      const uint16_t* b = wave_base(base, kt, blk);
 #pragma unroll
       for (int i = 0; i < IPW; ++i) {
         const int q = wu * IPW + i;
@@ -292,15 +298,17 @@ __global__ __launch_bounds__(512, 1) void attn_mfma_kernel(AttnK a) {
       }
       return;
     }
+    // the tile crosses the end: the wave's rows past the last key read row T-1 (when the wave's
+    // whole block is past the end, its block is clamped to the last one and every row reads row T-1)
 #pragma unroll
     for (int i = 0; i < IPW; ++i) {
       const int q = wu * IPW + i;
       const int rr = q * RPK + lrow_in;
       const int key = kbase + rr;
-      const int kb16 = __builtin_amdgcn_readfirstlane(min((kbase + q * RPK) >> 4, last_key >> 4));
       const int c = pchunk ^ (is_v ? v_swz<NCH>(rr) : (rr & (NCH - 1)));
-      const uint16_t* blk = block_base_w(base, kb16);
-      const uint16_t* row = key > last_key ? row_last : blk + (int64_t)(key & 15) * rstride;
+      const uint16_t* b = PAGED ? wave_base(base, kt, blk)
+                                : block_base(base, __builtin_amdgcn_readfirstlane(min((kbase + q * RPK) >> 4, last_key >> 4)));
+      const uint16_t* row = key > last_key ? row_last : b + (int64_t)(key & 15) * rstride;
       dma16(row + c * 8, dst + q * 1024);
     }
   };
@@ -498,9 +506,8 @@ __global__ __launch_bounds__(512, 1) void attn_mfma_kernel(AttnK a) {
   // unit then delays vector work, not MFMAs); they have NBUF - 2 iterations to land (waited for at
   // the end of iteration j + NBUF - 3) before they are read, and their buffers were last read in
   // iteration j-1. ----
-  auto ncur = [&](int j) {   // transfers (and window loads) this wave issues in iteration j
-    return (j + KD >= 0 && j + KD < nkt ? IPW : 0) + (PV && j + VD >= 0 && j + VD < nkt ? IPW : 0) +
-           ((PAGED && j >= 0 && ((j + KD) & 15) == 0) ? 1 : 0);
+  auto ncur = [&](int j) {   // transfers this wave issues in iteration j
+    return (j + KD >= 0 && j + KD < nkt ? IPW : 0) + (PV && j + VD >= 0 && j + VD < nkt ? IPW : 0);
   };
   // transfers of iterations j - NBUF + 4 .. j may still be in flight at the end of iteration j
   auto inflight = [&](int j) {
@@ -510,14 +517,18 @@ __global__ __launch_bounds__(512, 1) void attn_mfma_kernel(AttnK a) {
   };
   // (iteration j works on key tile kt0 + j; the LDS buffers rotate with j.)  Prologue: K(0), then
   // the transfers that iterations -(NBUF-2) .. -1 would have issued.
-  issue(a.k, k_last, kt0, ktile(0), false);
+  issue(a.k, k_last, kt0, ktile(0), false, blk_of(kt0));
 #pragma unroll
   for (int jj = -(NBUF - 2); jj < 0; ++jj) {
-    if (jj + KD < nkt) issue(a.k, k_last, kt0 + jj + KD, ktile(jj + KD), false);
+    if (jj + KD < nkt) issue(a.k, k_last, kt0 + jj + KD, ktile(jj + KD), false, blk_of(kt0 + jj + KD));
     if constexpr (PV) {
-      if (jj + VD < nkt) issue(a.v, v_last, kt0 + jj + VD, vtile(jj + VD), true);
+      if (jj + VD < nkt) issue(a.v, v_last, kt0 + jj + VD, vtile(jj + VD), true, blk_of(kt0 + jj + VD));
     }
   }
+  // block ids of the next transfer phase (scalar loads one iteration ahead, so their wait is never
+  // on the loop's critical path): V(j + VD) is the tile of the previous phase's K (VD = KD - 1)
+  static_assert(VD == KD - 1, "the V tile of a transfer phase is the K tile of the one before");
+  int32_t blk_k = blk_of(kt0 + KD), blk_v = blk_of(kt0 + KD - 1);
   wait_vm(inflight(-1));   // K(0) has landed
   __syncthreads();
   // `ph` is j mod NBUF when known at compile time (integral constant >= 0), else -1: the tile
@@ -528,66 +539,60 @@ __global__ __launch_bounds__(512, 1) void attn_mfma_kernel(AttnK a) {
     // the wave in its matrix phase issues first: its MFMAs are not held back by the other
     // wave's softmax on the same SIMD
     __builtin_amdgcn_s_setprio(2);
-    if (j >= 1 && (kt0 + j - 1) * KT <= wave_max)
+    if (j >= 1 && j - 1 < nkt && (kt0 + j - 1) * KT <= wave_max)
       pv_tile(FX ? vbuf_lds + (uint32_t)(((PH + NBUF - 1) % NBUF) * TILEB) : vtile_lds(j - 1),
               std::integral_constant<bool, FX>{});
     if (j < nkt && (kt0 + j) * KT <= wave_max)
       s_tile(FX ? kbuf_lds + (uint32_t)(PH * TILEB) : ktile_lds(j), std::integral_constant<bool, FX>{});
     __builtin_amdgcn_s_setprio(0);
   };
-  auto transfer_phase = [&](int j, auto ph) {   // this wave's share of K(j+KD) and V(j+VD)
-    constexpr int PH = decltype(ph)::value;
-    if (j + KD < nkt) issue(a.k, k_last, kt0 + j + KD, PH >= 0 ? kbuf + ((PH + KD) % NBUF) * TILEB : ktile(j + KD), false);
+  // this wave's share of K(j+KD) and V(j+VD); tph = j mod NBUF (wave-uniform)
+  auto transfer_phase = [&](int j, int tph) {
+    const int kb = tph + KD >= NBUF ? tph + KD - NBUF : tph + KD;
+    const int vb = tph + VD >= NBUF ? tph + VD - NBUF : tph + VD;
+    if (j + KD < nkt) issue(a.k, k_last, kt0 + j + KD, kbuf + kb * TILEB, false, blk_k);
     if constexpr (PV) {
-      if (j + VD < nkt)
-        issue(a.v, v_last, kt0 + j + VD, PH >= 0 ? vbuf + ((PH + VD) % NBUF) * TILEB : vtile(j + VD), true);
+      if (j + VD < nkt) issue(a.v, v_last, kt0 + j + VD, vbuf + vb * TILEB, true, blk_v);
     }
     if constexpr (PAGED) {
-      // (kt0 is a multiple of 16: local and absolute tile indices agree mod 16.)  Tile j + KD opens
-      // window win_c + 1: the later iterations issue tiles of windows win_c + 1 and win_c + 2.
-      if (((j + KD) & 15) == 0) {
-        win0 = win1;
-        win1 = load_win(win_c + 2);
-        ++win_c;
-      }
+      // a wave calls this once per iteration, in order: prefetch the next call's K block
+      blk_v = blk_k;
+      blk_k = blk_of(kt0 + j + 1 + KD);
     }
   };
   auto vector_phase = [&](int j) {   // softmax of tile j
     if (j >= 0 && j < nkt && (kt0 + j) * KT <= wave_max) softmax_tile((kt0 + j) * KT);
   };
-  auto iter_x = [&](int j, auto ph) {
-    matrix_phase(j, ph);
+  // Both groups run one loop body, U(j) = M(j) | barrier | T(j + grp), softmax of tile j | barrier.
+  // Group Y (grp = 1) is half an iteration ahead: it issues T(0) and passes one barrier before its
+  // first U, so its matrix phase M(j) runs beside group X's softmax of tile j - 1 and its softmax of
+  // tile j beside X's M(j + 1).  A wave waits for its transfers of iteration j - NBUF + 3 (all but
+  // those of T(j), the youngest) before the barrier that precedes its next matrix phase.  Every loop
+  // trip runs NBUF iterations with static buffer phases (every LDS offset of the matrix phase an
+  // immediate); iterations past nkt only pass their barriers.  Both groups pass the same number of
+  // barriers: Y's extra one at the start, X's at the end.
+  const int g1 = __builtin_amdgcn_readfirstlane(grp);
+  if (g1) {
+    transfer_phase(0, 0);
     __syncthreads();
-    transfer_phase(j, ph);
+  }
+  auto iter_u = [&](int j, auto ph) {
+    constexpr int PH = decltype(ph)::value;
+    matrix_phase(j, ph);
+    if (g1) wait_vm(inflight(j));
+    __syncthreads();
+    transfer_phase(j + g1, PH + g1 >= NBUF ? PH + g1 - NBUF : PH + g1);
     vector_phase(j);
-    wait_vm(inflight(j));   // this wave's transfers of iteration j - NBUF + 3 have landed
+    if (!g1) wait_vm(inflight(j));
     __syncthreads();
   };
-  auto iter_y = [&](int j, auto ph) {
-    transfer_phase(j, ph);
-    vector_phase(j - 1);
-    __syncthreads();
-    matrix_phase(j, ph);
-    wait_vm(inflight(j));
-    __syncthreads();
-  };
-  // The dense kernel runs NBUF iterations per loop trip with static buffer phases (every LDS
-  // offset an immediate); the paged kernel keeps one dynamic iteration (its larger body unrolled
-  // would overflow the instruction cache that two CUs share).
-  auto run = [&](auto iter) {
-    int j = 0;
-    if constexpr (!PAGED) {
-      for (; j + NBUF - 1 <= nkt; j += NBUF) {
-        iter(j, std::integral_constant<int, 0>{});
-        iter(j + 1, std::integral_constant<int, 1>{});
-        iter(j + 2, std::integral_constant<int, 2>{});
-        if constexpr (NBUF == 4) iter(j + 3, std::integral_constant<int, 3>{});
-      }
-    }
-    for (; j <= nkt; ++j) iter(j, std::integral_constant<int, -1>{});
-  };
-  if (grp == 0) run(iter_x);
-  else run(iter_y);
+  for (int j = 0; j <= nkt; j += NBUF) {
+    iter_u(j, std::integral_constant<int, 0>{});
+    iter_u(j + 1, std::integral_constant<int, 1>{});
+    iter_u(j + 2, std::integral_constant<int, 2>{});
+    if constexpr (NBUF == 4) iter_u(j + 3, std::integral_constant<int, 3>{});
+  }
+  if (!g1) __syncthreads();
 
   const float l_tot = l_run + __shfl_xor(l_run, 32, 64);
   if constexpr (PV) {
