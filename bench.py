@@ -534,22 +534,32 @@ def measured_peaks(torch):
 
 
 def cpu_model() -> str:
-    """The host CPU's model name as lscpu reports it (or /proc/cpuinfo)."""
+    """The host CPU as lscpu reports it: model name, with family / model / stepping and the max clock
+    when the model name alone is terse (some virtual machines report only the vendor's product line),
+    and /proc/cpuinfo's model name when it says more."""
     import subprocess
+    fields = {}
     try:
         out = subprocess.run(["lscpu"], capture_output=True, text=True, timeout=10).stdout
         for line in out.splitlines():
-            if line.strip().startswith("Model name:"):
-                return line.split(":", 1)[1].strip()
+            if ":" in line:
+                k, v = line.split(":", 1)
+                fields.setdefault(k.strip(), v.strip())
     except (OSError, subprocess.SubprocessError):
         pass
+    proc = ""
     try:
         for line in open("/proc/cpuinfo"):
             if line.startswith("model name"):
-                return line.split(":", 1)[1].strip()
+                proc = line.split(":", 1)[1].strip()
+                break
     except OSError:
         pass
-    return "unknown"
+    name = fields.get("Model name") or proc or "unknown"
+    extra = [f"{k.lower()} {fields[k]}" for k in ("CPU family", "Model", "Stepping", "CPU max MHz") if fields.get(k)]
+    if proc and proc != name:
+        extra.append(f"/proc/cpuinfo: {proc}")
+    return name + (f" ({', '.join(extra)})" if extra else "")
 
 
 def cpu_baseline(w, layers, R, nfull, L, ratio, torch, n_sample=512):
