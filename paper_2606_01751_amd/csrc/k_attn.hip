@@ -56,7 +56,7 @@ struct AttnK {
   float scale_log2;
   int lse_base2;
   // log-sum-exp pass (paged, no P.V): each row tile's keys in nsplit pieces of whole 16-tile
-  // windows; with nsplit > 1 every piece writes its (max, sum) to lse_part[piece][probe row][Hq]
+  // groups; with nsplit > 1 every piece writes its (max, sum) to lse_part[piece][probe row][Hq]
   // (probe rows of all requests concatenated) and lse_merge_kernel forms the log-sum-exp
   int nsplit;
   float2* lse_part;
@@ -181,7 +181,7 @@ __global__ __launch_bounds__(512, 1) void attn_mfma_kernel(AttnK a) {
   const int wave_min = wave_min_i(valid ? pos : 0x7fffffff);
   const int qh = kvh * a.G + hh;
   const float c2 = a.scale_log2;
-  // key tiles [kt0, kt0 + nkt) of this workgroup: all of them, or one piece of whole 16-tile windows
+  // key tiles [kt0, kt0 + nkt) of this workgroup: all of them, or one piece of whole 16-tile groups
   const int nkt_all = wg_max / KT + 1;
   int kt0 = 0, nkt = nkt_all;
   if (nsplit > 1) {
@@ -503,9 +503,10 @@ __global__ __launch_bounds__(512, 1) void attn_mfma_kernel(AttnK a) {
   // issues MFMAs while the other runs the softmax on the vector ALU.
   // Tiles rotate through NBUF buffers: at the start of its softmax slot of iteration j each wave
   // issues its share of the transfers of K(j+KD) and V(j+VD) (an issue that waits for the address
-  // unit then delays vector work, not MFMAs); they have NBUF - 2 iterations to land (waited for at
-  // the end of iteration j + NBUF - 3) before they are read, and their buffers were last read in
-  // iteration j-1. ----
+  // unit then delays vector work, not MFMAs; issued at the end of the matrix phase instead they cost
+  // both attention kernels about 6 %); they have NBUF - 2 iterations to land (waited for at the end
+  // of iteration j + NBUF - 3) before they are read, and their buffers were last read in iteration
+  // j-1. ----
   auto ncur = [&](int j) {   // transfers this wave issues in iteration j
     return (j + KD >= 0 && j + KD < nkt ? IPW : 0) + (PV && j + VD >= 0 && j + VD < nkt ? IPW : 0);
   };
