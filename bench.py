@@ -99,10 +99,20 @@ KERNELS = {
 }
 
 
+def source_code(text):
+    """A kernel source with its comments and blank space removed: what the compiler sees of it."""
+    import re
+    text = re.sub(r"/\*.*?\*/", " ", text, flags=re.S)
+    text = re.sub(r"//[^\n]*", " ", text)
+    return " ".join(text.split())
+
+
 def source_hash(fname):
+    """Hash of a kernel source's code (comments and layout do not count): traffic counters taken on
+    one version of the code stay valid while the code is unchanged."""
     import hashlib
     path = os.path.join(ROOT, "paper_2606_01751_amd", "csrc", fname)
-    return hashlib.sha256(open(path, "rb").read()).hexdigest()[:16]
+    return hashlib.sha256(source_code(open(path).read()).encode()).hexdigest()[:16]
 
 
 def record_traffic(fetch_csv, write_csv, workload):

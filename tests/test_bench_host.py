@@ -74,3 +74,11 @@ def test_more_than_one_gpu_is_refused_with_a_message():
     assert r.returncode == 2
     assert "one GPU" in r.stderr
     assert r.stdout == ""
+
+
+def test_source_hash_ignores_comments_and_layout_but_not_code():
+    a = "// kernel\nint f(int x) {  /* block\n comment */ return x + 1; }\n"
+    b = "int f(int x) {\n  return x + 1;   // trailing\n}\n"
+    c = "int f(int x) { return x + 2; }"
+    assert bench.source_code(a) == bench.source_code(b)
+    assert bench.source_code(a) != bench.source_code(c)
