@@ -279,7 +279,8 @@ sx_status sx_topk_select(const sx_plan* plan, const float* scores, double ratio,
  * with K/V read from the paged cache of request r.  bfloat16 runs on matrix cores with float32
  * accumulation and bfloat16 probabilities; float32 runs on vector ALUs.  max_rows as in
  * sx_kv_scatter: the rows n >= min(n_rows[r], max_rows) are neither computed nor written, so the
- * attention covers exactly the rows whose K/V sx_kv_scatter writes for the same list. */
+ * attention covers exactly the rows whose K/V sx_kv_scatter writes for the same list.  Uses the
+ * plan's work-queue counters (bfloat16), so calls sharing a plan must be stream-ordered. */
 sx_status sx_sparse_attn(const sx_plan* plan, const void* q, const int32_t* rows, const int32_t* n_rows,
                          int32_t max_rows, const void* k_cache, const void* v_cache, void* out,
                          void* stream);

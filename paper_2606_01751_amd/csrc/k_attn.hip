@@ -21,8 +21,11 @@
 //     the latest rows (most keys) to the earliest, then request 1, ...  With 8 KV heads the
 //     round-robin dispatch keeps all tiles of one head on one XCD (one L2), and the workgroups
 //     running there at one time mostly belong to one request, so they share its K/V tiles.
+//     Sparse attention takes the same order from a per-KV-head work queue in a persistent grid
+//     (about one workgroup per compute unit and KV head).
 //   * Softmax in the log2 domain; the running max is raised only when a probability would reach
 //     2^64, so the O^T rescale is rare and there is no max reduction on the common path.
+#include <algorithm>
 #include <type_traits>
 
 #include "sx_device.h"
@@ -61,6 +64,9 @@ struct AttnK {
   int nsplit;
   float2* lse_part;
   int64_t n_part_rows;
+  // sparse attention (paged, P.V): per-KV-head work queues, [0, Hkv) items taken and [Hkv, 2 Hkv)
+  // workgroups finished, zero between launches
+  int32_t* queue;
 };
 
 typedef short shortx4_t __attribute__((ext_vector_type(4)));
@@ -94,8 +100,23 @@ __device__ __forceinline__ void sched_pipelined() {
   SX_SG(kSgMfma, PRE);
 }
 
+// The kernel arguments for one item of a persistent kernel: read from the kernel-argument segment
+// (where the by-value argument sits at offset 0) through a pointer the compiler cannot follow, so
+// the loads stay inside the item and nothing of them is kept across items.
+template <bool RELOAD>
+__device__ __forceinline__ AttnK item_args(const AttnK& k) {
+  if constexpr (RELOAD) {
+    typedef const __attribute__((address_space(4))) char* ArgPtr;
+    ArgPtr p = (ArgPtr)__builtin_amdgcn_kernarg_segment_ptr();
+    asm volatile("" : "+s"(p));
+    return *(const AttnK*)(const char*)p;
+  } else {
+    return k;
+  }
+}
+
 template <int D, bool PAGED, bool PV>
-__global__ __launch_bounds__(512, 1) void attn_mfma_kernel(AttnK a) {
+__global__ __launch_bounds__(512, 1) void attn_mfma_kernel(AttnK ka) {
   constexpr int NW = 8;                       // waves: two groups of 4
   constexpr int ROWB = D * 2;                 // bytes of one key row
   constexpr int NCH = ROWB / 16;              // 16-byte chunks per row
@@ -113,511 +134,546 @@ __global__ __launch_bounds__(512, 1) void attn_mfma_kernel(AttnK a) {
   char* const kbuf = smem;
   char* const vbuf = smem + (PV ? NBUF * TILEB : 0);
 
-  const int tid = threadIdx.x;
-  const int lane = tid & 63;
-  const int w = tid >> 6;
-  const int wu = __builtin_amdgcn_readfirstlane(w);
-  const int grp = wu >> 2;                    // 0: group X, 1: group Y
-  const int l32 = lane & 31;
-  const int hg = lane >> 5;
   // (the remainder is formed on the vector unit; in the paged kernel the empty asm keeps the uniform
   // result in a scalar register, so the block addresses built from it stay on the scalar unit)
-  int kvh = __builtin_amdgcn_readfirstlane((int)(blockIdx.x % (unsigned)a.Hkv));
+  int kvh = __builtin_amdgcn_readfirstlane((int)(blockIdx.x % (unsigned)ka.Hkv));
   if constexpr (PAGED) asm("" : "+s"(kvh));
-  const int rpw = a.rpw;
-  const int nsplit = (PAGED && !PV) ? a.nsplit : 1;
-  // rows of request rr that are processed: the first min(n_rows, max_rows) rows (the rows the KV
-  // write of the same row list covers), or every row of a dense request
-  auto rows_of = [&](int rr) -> int {
-    if constexpr (PAGED) return min(a.n_rows[rr], a.grid_rows);
-    else return a.cu[rr + 1] - a.cu[rr];
-  };
-  // Request-major grid: for each KV head, the row tiles of request 0 (latest rows, i.e. most keys,
+  // Request-major order: for each KV head, the row tiles of request 0 (latest rows, i.e. most keys,
   // first), then those of request 1, ...  The workgroups running together on one XCD then mostly
   // belong to one request and share its K/V tiles through that XCD's L2.  (Pieces of one row tile
-  // are adjacent.)
-  int r, qi;
-  locate_request((int)(blockIdx.x / (unsigned)a.Hkv), a.n_req,
-                 [&](int rr) { return (rows_of(rr) + rpw - 1) / rpw * nsplit; }, &r, &qi);
-  if (r < 0) return;
-  r = __builtin_amdgcn_readfirstlane(r);
-  qi = __builtin_amdgcn_readfirstlane(qi);
-  const int rank = qi / nsplit;
-  const int piece = qi - rank * nsplit;
-
-  int T, tok_off, bt_off = 0, nrows, p_off = 0;
-  if constexpr (PAGED) {
-    const ReqDev rq = a.reqs[r];
-    T = rq.T;
-    tok_off = rq.tok_off;
-    bt_off = rq.bt_off;
-    p_off = rq.p_off;
-  } else {
-    tok_off = a.cu[r];
-    T = a.cu[r + 1] - tok_off;
-  }
-  if constexpr (PAGED) {
-    // (request fields are workgroup-uniform: scalar registers keep the block address math on the
-    // scalar unit)
-    T = __builtin_amdgcn_readfirstlane(T);
-    tok_off = __builtin_amdgcn_readfirstlane(tok_off);
-    bt_off = __builtin_amdgcn_readfirstlane(bt_off);
-    p_off = __builtin_amdgcn_readfirstlane(p_off);
-  }
-  nrows = rows_of(r);
-  const int ntiles = (nrows + rpw - 1) / rpw;
-  const int row_tile = ntiles - 1 - rank;
-  const int row0 = row_tile * rpw;
-  const int col = w * 32 + l32;
-  const int lrow = col / a.G;
-  const int hh = col - lrow * a.G;
-  const int ridx = row0 + lrow;
-  const bool valid = lrow < rpw && ridx < nrows;
-  int pos = -1;
-  if (valid) pos = PAGED ? a.rows[tok_off + ridx] : ridx;
-  const int last = min(row0 + rpw, nrows) - 1;
-  const int wg_max = PAGED ? a.rows[tok_off + last] : last;
-  const int wave_max = wave_max_i(pos);
-  const int wave_min = wave_min_i(valid ? pos : 0x7fffffff);
-  const int qh = kvh * a.G + hh;
-  const float c2 = a.scale_log2;
-  // key tiles [kt0, kt0 + nkt) of this workgroup: all of them, or one piece of whole 16-tile groups
-  const int nkt_all = wg_max / KT + 1;
-  int kt0 = 0, nkt = nkt_all;
-  if (nsplit > 1) {
-    const int tpp = ((nkt_all + nsplit - 1) / nsplit + 15) & ~15;
-    kt0 = piece * tpp;
-    nkt = min(tpp, nkt_all - kt0);
-    if (nkt <= 0) {   // no keys in this piece: an empty partial (uniform over the workgroup)
-      if (valid && hg == 0)
-        a.lse_part[((int64_t)piece * a.n_part_rows + p_off + ridx) * a.Hq + qh] = make_float2(-INFINITY, 0.f);
-      return;
+  // are adjacent.)  Dense attention and the log-sum-exp pass launch one workgroup per item.
+  // Sparse attention runs a persistent grid instead: about one workgroup per compute unit and KV
+  // head, each taking the head's next item from a queue whenever it finishes one, until the queue
+  // is empty.  The items then go to whichever compute unit frees first (greedy longest-first), with
+  // no gap for the hardware to dispatch another workgroup; the hardware's own dispatch hands the
+  // workgroups of an XCD to its shader engines in turn and holds the rest back while the next one's
+  // engine is full, which left a tenth of the compute units idle in the tail.  The last workgroup of
+  // a head to find the queue empty resets the head's counters for the next launch.
+  constexpr bool PERSIST = PAGED && PV;
+  __shared__ int s_item;
+  int item = (int)(blockIdx.x / (unsigned)ka.Hkv);
+  for (;;) {
+    if constexpr (PERSIST) {
+      if (threadIdx.x == 0)
+        s_item = __hip_atomic_fetch_add(ka.queue + kvh, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      __syncthreads();
+      item = __builtin_amdgcn_readfirstlane(s_item);
     }
-  }
+    // The kernel arguments and the lane values are formed again for every item (from the argument
+    // segment and the thread index, both through opaque copies) rather than hoisted out of the item
+    // loop and kept live through the tile loop, which would leave no registers for the pipelined
+    // operand reads.
+    const AttnK a = item_args<PERSIST>(ka);
+    int tid = threadIdx.x;
+    if constexpr (PERSIST) asm volatile("" : "+v"(tid));
+    const int lane = tid & 63;
+    const int w = tid >> 6;
+    const int wu = __builtin_amdgcn_readfirstlane(w);
+    const int grp = wu >> 2;                    // 0: group X, 1: group Y
+    const int l32 = lane & 31;
+    const int hg = lane >> 5;
+    const int rpw = a.rpw;
+    const int nsplit = (PAGED && !PV) ? a.nsplit : 1;
+    // rows of request rr that are processed: the first min(n_rows, max_rows) rows (the rows the KV
+    // write of the same row list covers), or every row of a dense request
+    auto rows_of = [&](int rr) -> int {
+      if constexpr (PAGED) return min(a.n_rows[rr], a.grid_rows);
+      else return a.cu[rr + 1] - a.cu[rr];
+    };
+    int r, qi;
+    locate_request(item, a.n_req, [&](int rr) { return (rows_of(rr) + rpw - 1) / rpw * nsplit; }, &r, &qi, lane);
+    r = __builtin_amdgcn_readfirstlane(r);   // (uniform: the loop exit below is a uniform branch)
+    qi = __builtin_amdgcn_readfirstlane(qi);
+    if (r < 0) break;
+    const int rank = qi / nsplit;
+    const int piece = qi - rank * nsplit;
 
-  // Q^T as the B operand: lane owns column l32, d-slots 16s + 8hg .. +7.
-  bf16x8_t qb[D / 16];
-  {
-    const uint16_t* qp = a.q + ((int64_t)(tok_off + (pos < 0 ? 0 : pos)) * a.Hq + (valid ? qh : 0)) * D + hg * 8;
-#pragma unroll
-    for (int s = 0; s < D / 16; ++s) {
-      uint4 v = valid ? *(const uint4*)(qp + 16 * s) : make_uint4(0, 0, 0, 0);
-      qb[s] = __builtin_bit_cast(bf16x8_t, v);
-    }
-  }
-  // Block table (paged caches): a wave moves rows 8 wu .. 8 wu + 7 of every tile, all inside
-  // logical block 4 t + wu / 2 of tile t, so one block id per wave and tile (a scalar load through
-  // the constant address space, clamped to the request's last block for tiles past the end).
-  const int nblk = (T + 15) >> 4;
-  auto blk_of = [&](int kt) -> int32_t {
+    int T, tok_off, bt_off = 0, nrows, p_off = 0;
     if constexpr (PAGED) {
-      const __attribute__((address_space(4))) int32_t* btc = (const __attribute__((address_space(4))) int32_t*)a.bt;
-      return btc[__builtin_amdgcn_readfirstlane(bt_off + min(4 * kt + (wu >> 1), nblk - 1))];
+      const ReqDev rq = a.reqs[r];
+      T = rq.T;
+      tok_off = rq.tok_off;
+      bt_off = rq.bt_off;
+      p_off = rq.p_off;
     } else {
-      return 0;
+      tok_off = a.cu[r];
+      T = a.cu[r + 1] - tok_off;
     }
-  };
-  // Q must be complete before any tile transfer is issued: the compiler does not see those
-  // transfers, so a later wait of its own for Q would also wait for them.
-  SX_WAIT_VMCNT(0);
-
-  f32x16_t o[PV ? D / 32 : 1];
-#pragma unroll
-  for (int i = 0; i < (PV ? D / 32 : 1); ++i)
-#pragma unroll
-    for (int e = 0; e < 16; ++e) o[i][e] = 0.f;
-  // running max (log2 domain); columns without a row start at 0 so their (unused) sums stay finite
-  float m_run = valid ? -INFINITY : 0.f;
-  float l_run = 0.f;
-
-  // ---- global -> LDS tile transfers (16 bytes per lane, all 8 waves share each tile).
-  // Transfer q (1 KB) of a tile holds rows RPK*q .. RPK*q + RPK - 1, all inside one 16-key block;
-  // keys past the end read row T-1 (they are masked: every query row is < T). ----
-  const int last_key = T - 1;
-  const int lrow_in = lane / NCH;     // row of this lane inside its 1 KB piece
-  const int pchunk = lane % NCH;      // physical chunk this lane fills
-  auto block_base = [&](const uint16_t* base, int key16) -> const uint16_t* {
     if constexpr (PAGED) {
-      // the block table is read-only here: read it through the constant address space (scalar loads)
-      const __attribute__((address_space(4))) int32_t* btc = (const __attribute__((address_space(4))) int32_t*)a.bt;
-      const int32_t blk = btc[__builtin_amdgcn_readfirstlane(bt_off + key16)];
-      return base + (((int64_t)blk * a.Hkv + kvh) * 16) * D;
-    } else {
-      return base + ((int64_t)(tok_off + key16 * 16) * a.Hkv + kvh) * D;
+      // (request fields are workgroup-uniform: scalar registers keep the block address math on the
+      // scalar unit)
+      T = __builtin_amdgcn_readfirstlane(T);
+      tok_off = __builtin_amdgcn_readfirstlane(tok_off);
+      bt_off = __builtin_amdgcn_readfirstlane(bt_off);
+      p_off = __builtin_amdgcn_readfirstlane(p_off);
     }
-  };
-  // base of the rows this wave moves in key tile kt: the (block, head) run of block blk (paged), or
-  // the tile's 16-row group of this wave (dense; rows past the end are not read through it)
-  auto wave_base = [&](const uint16_t* base, int kt, int32_t blk) -> const uint16_t* {
-    if constexpr (PAGED) return base + (((int64_t)blk * a.Hkv + kvh) * 16) * D;
-    else return block_base(base, ((kt * KT) >> 4) + (wu >> 1));
-  };
-  constexpr int64_t kRowPaged = D;
-  const int64_t rstride = PAGED ? kRowPaged : (int64_t)a.Hkv * D;   // elements between rows of a block
-  const uint16_t* k_last = block_base(a.k, last_key >> 4) + (last_key & 15) * rstride;
-  const uint16_t* v_last = PV ? block_base(a.v, last_key >> 4) + (last_key & 15) * rstride : nullptr;
-  // One 16-byte global -> LDS transfer per lane; the destination (M0) is wave-uniform and lane l
-  // lands at dst + 16 l.  Issued as inline assembly so the compiler does not order every later
-  // LDS read behind it: the wait for these transfers is explicit (vmcnt + barrier before a tile
-  // is read).  The statement is volatile, so it stays between the barriers around it; it
-  // declares no memory clobber, which keeps the read-only index loads on the scalar unit.
-  auto dma16 = [&](const void* src, const char* dst) {
-    const uint32_t m0 = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) const char*)dst;
-    asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(src), "s"(m0) : "m0", "memory");
-  };
-  auto dma16_sb = [&](const uint16_t* sbase, uint32_t voffset, const char* dst) {
-    const uint32_t m0 = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) const char*)dst;
-    // the base is wave-uniform; readfirstlane makes that visible where the compiler cannot prove it
-    // (the instruction takes its base from an SGPR pair)
-    // (the builtin returns a signed int: each half goes through uint32_t so that nothing is sign-extended)
-    const uint64_t sb = (uint64_t)(uintptr_t)sbase;
-    const uint32_t lo = (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)sb);
-    const uint32_t hi = (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)(sb >> 32));
-    const uint64_t sbu = ((uint64_t)hi << 32) | (uint64_t)lo;
-    asm volatile("s_mov_b32 m0, %2\n\tglobal_load_lds_dwordx4 %0, %1" ::"v"(voffset), "s"(sbu), "s"(m0)
-                 : "m0", "memory");
-  };
-  // per-lane byte offsets of the transfers inside a (block, head) run; tiles start at multiples
-  // of 64 keys, so they are the same for every tile
-  uint32_t koff[IPW], voff[IPW];
+    nrows = rows_of(r);
+    const int ntiles = (nrows + rpw - 1) / rpw;
+    const int row_tile = ntiles - 1 - rank;
+    const int row0 = row_tile * rpw;
+    const int col = w * 32 + l32;
+    const int lrow = col / a.G;
+    const int hh = col - lrow * a.G;
+    const int ridx = row0 + lrow;
+    const bool valid = lrow < rpw && ridx < nrows;
+    int pos = -1;
+    if (valid) pos = PAGED ? a.rows[tok_off + ridx] : ridx;
+    const int last = min(row0 + rpw, nrows) - 1;
+    const int wg_max = PAGED ? a.rows[tok_off + last] : last;
+    const int wave_max = wave_max_i(pos, lane);
+    const int wave_min = wave_min_i(valid ? pos : 0x7fffffff, lane);
+    const int qh = kvh * a.G + hh;
+    const float c2 = a.scale_log2;
+    // key tiles [kt0, kt0 + nkt) of this workgroup: all of them, or one piece of whole 16-tile groups
+    const int nkt_all = wg_max / KT + 1;
+    int kt0 = 0, nkt = nkt_all;
+    if (nsplit > 1) {
+      const int tpp = ((nkt_all + nsplit - 1) / nsplit + 15) & ~15;
+      kt0 = piece * tpp;
+      nkt = min(tpp, nkt_all - kt0);
+      if (nkt <= 0) {   // no keys in this piece: an empty partial (uniform over the workgroup)
+        if (valid && hg == 0)
+          a.lse_part[((int64_t)piece * a.n_part_rows + p_off + ridx) * a.Hq + qh] = make_float2(-INFINITY, 0.f);
+        return;
+      }
+    }
+
+    // Q^T as the B operand: lane owns column l32, d-slots 16s + 8hg .. +7.
+    bf16x8_t qb[D / 16];
+    {
+      const uint16_t* qp = a.q + ((int64_t)(tok_off + (pos < 0 ? 0 : pos)) * a.Hq + (valid ? qh : 0)) * D + hg * 8;
 #pragma unroll
-  for (int i = 0; i < IPW; ++i) {
-    const int rr = (wu * IPW + i) * RPK + lrow_in;
-    koff[i] = (uint32_t)(((rr & 15) * rstride + (pchunk ^ (rr & (NCH - 1))) * 8) * 2);
-    voff[i] = (uint32_t)(((rr & 15) * rstride + (pchunk ^ v_swz<NCH>(rr)) * 8) * 2);
-  }
-  // transfer of this wave's share of one matrix (K or V) tile kt into dst; blk = blk_of(kt)
-  auto issue = [&](const uint16_t* base, const uint16_t* row_last, int kt, char* dst, bool is_v, int32_t blk) {
-    const int kbase = kt * KT;
-    if (kbase + KT - 1 <= last_key) {
-      const uint16_t* b = wave_base(base, kt, blk);
+      for (int s = 0; s < D / 16; ++s) {
+        uint4 v = valid ? *(const uint4*)(qp + 16 * s) : make_uint4(0, 0, 0, 0);
+        qb[s] = __builtin_bit_cast(bf16x8_t, v);
+      }
+    }
+    // Block table (paged caches): a wave moves rows 8 wu .. 8 wu + 7 of every tile, all inside
+    // logical block 4 t + wu / 2 of tile t, so one block id per wave and tile (a scalar load through
+    // the constant address space, clamped to the request's last block for tiles past the end).
+    const int nblk = (T + 15) >> 4;
+    auto blk_of = [&](int kt) -> int32_t {
+      if constexpr (PAGED) {
+        const __attribute__((address_space(4))) int32_t* btc = (const __attribute__((address_space(4))) int32_t*)a.bt;
+        return btc[__builtin_amdgcn_readfirstlane(bt_off + min(4 * kt + (wu >> 1), nblk - 1))];
+      } else {
+        return 0;
+      }
+    };
+    // Q must be complete before any tile transfer is issued: the compiler does not see those
+    // transfers, so a later wait of its own for Q would also wait for them.
+    SX_WAIT_VMCNT(0);
+
+    f32x16_t o[PV ? D / 32 : 1];
+#pragma unroll
+    for (int i = 0; i < (PV ? D / 32 : 1); ++i)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) o[i][e] = 0.f;
+    // running max (log2 domain); columns without a row start at 0 so their (unused) sums stay finite
+    float m_run = valid ? -INFINITY : 0.f;
+    float l_run = 0.f;
+
+    // ---- global -> LDS tile transfers (16 bytes per lane, all 8 waves share each tile).
+    // Transfer q (1 KB) of a tile holds rows RPK*q .. RPK*q + RPK - 1, all inside one 16-key block;
+    // keys past the end read row T-1 (they are masked: every query row is < T). ----
+    const int last_key = T - 1;
+    const int lrow_in = lane / NCH;     // row of this lane inside its 1 KB piece
+    const int pchunk = lane % NCH;      // physical chunk this lane fills
+    auto block_base = [&](const uint16_t* base, int key16) -> const uint16_t* {
+      if constexpr (PAGED) {
+        // the block table is read-only here: read it through the constant address space (scalar loads)
+        const __attribute__((address_space(4))) int32_t* btc = (const __attribute__((address_space(4))) int32_t*)a.bt;
+        const int32_t blk = btc[__builtin_amdgcn_readfirstlane(bt_off + key16)];
+        return base + (((int64_t)blk * a.Hkv + kvh) * 16) * D;
+      } else {
+        return base + ((int64_t)(tok_off + key16 * 16) * a.Hkv + kvh) * D;
+      }
+    };
+    // base of the rows this wave moves in key tile kt: the (block, head) run of block blk (paged), or
+    // the tile's 16-row group of this wave (dense; rows past the end are not read through it)
+    auto wave_base = [&](const uint16_t* base, int kt, int32_t blk) -> const uint16_t* {
+      if constexpr (PAGED) return base + (((int64_t)blk * a.Hkv + kvh) * 16) * D;
+      else return block_base(base, ((kt * KT) >> 4) + (wu >> 1));
+    };
+    constexpr int64_t kRowPaged = D;
+    const int64_t rstride = PAGED ? kRowPaged : (int64_t)a.Hkv * D;   // elements between rows of a block
+    const uint16_t* k_last = block_base(a.k, last_key >> 4) + (last_key & 15) * rstride;
+    const uint16_t* v_last = PV ? block_base(a.v, last_key >> 4) + (last_key & 15) * rstride : nullptr;
+    // One 16-byte global -> LDS transfer per lane; the destination (M0) is wave-uniform and lane l
+    // lands at dst + 16 l.  Issued as inline assembly so the compiler does not order every later
+    // LDS read behind it: the wait for these transfers is explicit (vmcnt + barrier before a tile
+    // is read).  The statement is volatile, so it stays between the barriers around it; it
+    // declares no memory clobber, which keeps the read-only index loads on the scalar unit.
+    auto dma16 = [&](const void* src, const char* dst) {
+      const uint32_t m0 = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) const char*)dst;
+      asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(src), "s"(m0) : "m0", "memory");
+    };
+    auto dma16_sb = [&](const uint16_t* sbase, uint32_t voffset, const char* dst) {
+      const uint32_t m0 = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) const char*)dst;
+      // the base is wave-uniform; readfirstlane makes that visible where the compiler cannot prove it
+      // (the instruction takes its base from an SGPR pair)
+      // (the builtin returns a signed int: each half goes through uint32_t so that nothing is sign-extended)
+      const uint64_t sb = (uint64_t)(uintptr_t)sbase;
+      const uint32_t lo = (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)sb);
+      const uint32_t hi = (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)(sb >> 32));
+      const uint64_t sbu = ((uint64_t)hi << 32) | (uint64_t)lo;
+      asm volatile("s_mov_b32 m0, %2\n\tglobal_load_lds_dwordx4 %0, %1" ::"v"(voffset), "s"(sbu), "s"(m0)
+                   : "m0", "memory");
+    };
+    // per-lane byte offsets of the transfers inside a (block, head) run; tiles start at multiples
+    // of 64 keys, so they are the same for every tile
+    uint32_t koff[IPW], voff[IPW];
+#pragma unroll
+    for (int i = 0; i < IPW; ++i) {
+      const int rr = (wu * IPW + i) * RPK + lrow_in;
+      koff[i] = (uint32_t)(((rr & 15) * rstride + (pchunk ^ (rr & (NCH - 1))) * 8) * 2);
+      voff[i] = (uint32_t)(((rr & 15) * rstride + (pchunk ^ v_swz<NCH>(rr)) * 8) * 2);
+    }
+    // transfer of this wave's share of one matrix (K or V) tile kt into dst; blk = blk_of(kt)
+    auto issue = [&](const uint16_t* base, const uint16_t* row_last, int kt, char* dst, bool is_v, int32_t blk) {
+      const int kbase = kt * KT;
+      if (kbase + KT - 1 <= last_key) {
+        const uint16_t* b = wave_base(base, kt, blk);
+#pragma unroll
+        for (int i = 0; i < IPW; ++i) {
+          const int q = wu * IPW + i;
+          dma16_sb(b, is_v ? voff[i] : koff[i], dst + q * 1024);
+        }
+        return;
+      }
+      // the tile crosses the end: the wave's rows past the last key read row T-1 (when the wave's
+      // whole block is past the end, its block is clamped to the last one and every row reads row T-1)
 #pragma unroll
       for (int i = 0; i < IPW; ++i) {
         const int q = wu * IPW + i;
-        dma16_sb(b, is_v ? voff[i] : koff[i], dst + q * 1024);
+        const int rr = q * RPK + lrow_in;
+        const int key = kbase + rr;
+        const int c = pchunk ^ (is_v ? v_swz<NCH>(rr) : (rr & (NCH - 1)));
+        const uint16_t* b =
+            PAGED ? wave_base(base, kt, blk)
+                  : block_base(base, __builtin_amdgcn_readfirstlane(min((kbase + q * RPK) >> 4, last_key >> 4)));
+        const uint16_t* row = key > last_key ? row_last : b + (int64_t)(key & 15) * rstride;
+        dma16(row + c * 8, dst + q * 1024);
       }
-      return;
-    }
-    // the tile crosses the end: the wave's rows past the last key read row T-1 (when the wave's
-    // whole block is past the end, its block is clamped to the last one and every row reads row T-1)
-#pragma unroll
-    for (int i = 0; i < IPW; ++i) {
-      const int q = wu * IPW + i;
-      const int rr = q * RPK + lrow_in;
-      const int key = kbase + rr;
-      const int c = pchunk ^ (is_v ? v_swz<NCH>(rr) : (rr & (NCH - 1)));
-      const uint16_t* b = PAGED ? wave_base(base, kt, blk)
-                                : block_base(base, __builtin_amdgcn_readfirstlane(min((kbase + q * RPK) >> 4, last_key >> 4)));
-      const uint16_t* row = key > last_key ? row_last : b + (int64_t)(key & 15) * rstride;
-      dma16(row + c * 8, dst + q * 1024);
-    }
-  };
-  auto ktile = [&](int t) { return kbuf + (t % NBUF) * TILEB; };
-  auto vtile = [&](int t) { return vbuf + (t % NBUF) * TILEB; };
-  constexpr int KD = NBUF - 1, VD = NBUF - 2;   // issue distances of K and V tiles (iterations)
-  // the same buffers as LDS byte addresses (wave-uniform: the operand reads add a lane offset)
-  const uint32_t kbuf_lds = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) char*)kbuf;
-  const uint32_t vbuf_lds = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) char*)vbuf;
-  auto ktile_lds = [&](int t) { return kbuf_lds + (uint32_t)((t % NBUF) * TILEB); };
-  auto vtile_lds = [&](int t) { return vbuf_lds + (uint32_t)((t % NBUF) * TILEB); };
-  // wait until at most n of this wave's tile transfers (the youngest) are still in flight
-  auto wait_vm = [&](int n) {
-    switch (n) {
-      case 0: SX_WAIT_VMCNT(0); break;
-      case 1: SX_WAIT_VMCNT(1); break;
-      case 2: SX_WAIT_VMCNT(2); break;
-      case 3: SX_WAIT_VMCNT(3); break;
-      case 4: SX_WAIT_VMCNT(4); break;
-      case 5: SX_WAIT_VMCNT(5); break;
-      case 6: SX_WAIT_VMCNT(6); break;
-      case 7: SX_WAIT_VMCNT(7); break;
-      case 8: SX_WAIT_VMCNT(8); break;
-      case 9: SX_WAIT_VMCNT(9); break;
-      default: SX_WAIT_VMCNT(10); break;
-    }
-  };
-  static_assert((NBUF - 2) * (2 * IPW + 1) <= 10, "transfers in flight exceed the wait table");
+    };
+    auto ktile = [&](int t) { return kbuf + (t % NBUF) * TILEB; };
+    auto vtile = [&](int t) { return vbuf + (t % NBUF) * TILEB; };
+    constexpr int KD = NBUF - 1, VD = NBUF - 2;   // issue distances of K and V tiles (iterations)
+    // the same buffers as LDS byte addresses (wave-uniform: the operand reads add a lane offset)
+    const uint32_t kbuf_lds = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) char*)kbuf;
+    const uint32_t vbuf_lds = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) char*)vbuf;
+    auto ktile_lds = [&](int t) { return kbuf_lds + (uint32_t)((t % NBUF) * TILEB); };
+    auto vtile_lds = [&](int t) { return vbuf_lds + (uint32_t)((t % NBUF) * TILEB); };
+    // wait until at most n of this wave's tile transfers (the youngest) are still in flight
+    auto wait_vm = [&](int n) {
+      switch (n) {
+        case 0: SX_WAIT_VMCNT(0); break;
+        case 1: SX_WAIT_VMCNT(1); break;
+        case 2: SX_WAIT_VMCNT(2); break;
+        case 3: SX_WAIT_VMCNT(3); break;
+        case 4: SX_WAIT_VMCNT(4); break;
+        case 5: SX_WAIT_VMCNT(5); break;
+        case 6: SX_WAIT_VMCNT(6); break;
+        case 7: SX_WAIT_VMCNT(7); break;
+        case 8: SX_WAIT_VMCNT(8); break;
+        case 9: SX_WAIT_VMCNT(9); break;
+        default: SX_WAIT_VMCNT(10); break;
+      }
+    };
+    static_assert((NBUF - 2) * (2 * IPW + 1) <= 10, "transfers in flight exceed the wait table");
 
-  // ---- tile computations ----
-  // S^T = K Q^T for the 64 keys of a tile (two 32-key M tiles)
-  f32x16_t sacc[2];
-  // K operand addressing: lane reads row 32 mt + l32, logical chunk 2 s + hg.  The swizzle depends
-  // on the row only through l32 mod NCH, so the lane part of the address is one value per k-slice
-  // s (computed once) and the second row block adds a constant (an immediate offset).
-  int k_off[D / 16];
+    // ---- tile computations ----
+    // S^T = K Q^T for the 64 keys of a tile (two 32-key M tiles)
+    f32x16_t sacc[2];
+    // K operand addressing: lane reads row 32 mt + l32, logical chunk 2 s + hg.  The swizzle depends
+    // on the row only through l32 mod NCH, so the lane part of the address is one value per k-slice
+    // s (computed once) and the second row block adds a constant (an immediate offset).
+    int k_off[D / 16];
 #pragma unroll
-  for (int s = 0; s < D / 16; ++s) k_off[s] = l32 * ROWB + (((2 * s + hg) ^ (l32 & (NCH - 1))) << 4);
-  // Kb: the tile's LDS address; `fixed` when it is a compile-time constant (the buffer offset then
-  // folds into the reads' immediate offsets), else made opaque (one add per k-slice, no
-  // strength-reduced variants)
-  auto s_body = [&](uint32_t Kb, auto fixed) {
-    if constexpr (!decltype(fixed)::value) asm volatile("" : "+s"(Kb));
+    for (int s = 0; s < D / 16; ++s) k_off[s] = l32 * ROWB + (((2 * s + hg) ^ (l32 & (NCH - 1))) << 4);
+    // Kb: the tile's LDS address; `fixed` when it is a compile-time constant (the buffer offset then
+    // folds into the reads' immediate offsets), else made opaque (one add per k-slice, no
+    // strength-reduced variants)
+    auto s_body = [&](uint32_t Kb, auto fixed) {
+      if constexpr (!decltype(fixed)::value) asm volatile("" : "+s"(Kb));
 #pragma unroll
-    for (int mt = 0; mt < 2; ++mt)
+      for (int mt = 0; mt < 2; ++mt)
 #pragma unroll
-      for (int e = 0; e < 16; ++e) sacc[mt][e] = 0.f;
+        for (int e = 0; e < 16; ++e) sacc[mt][e] = 0.f;
 #pragma unroll
-    for (int s = 0; s < D / 16; ++s) {
-      uint32_t kbase = Kb + (uint32_t)k_off[s];
-      if constexpr (!decltype(fixed)::value) asm volatile("" : "+v"(kbase));
+      for (int s = 0; s < D / 16; ++s) {
+        uint32_t kbase = Kb + (uint32_t)k_off[s];
+        if constexpr (!decltype(fixed)::value) asm volatile("" : "+v"(kbase));
 #pragma unroll
-      for (int mt = 0; mt < 2; ++mt) {
-        const bf16x8_t ka = *(const __attribute__((address_space(3))) bf16x8_t*)(uintptr_t)(kbase + (uint32_t)(mt * 32 * ROWB));
-        sacc[mt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka, qb[s], sacc[mt], 0, 0, 0);
+        for (int mt = 0; mt < 2; ++mt) {
+          const bf16x8_t ka =
+              *(const __attribute__((address_space(3))) bf16x8_t*)(uintptr_t)(kbase + (uint32_t)(mt * 32 * ROWB));
+          sacc[mt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka, qb[s], sacc[mt], 0, 0, 0);
+        }
+      }
+    };
+    auto s_tile = [&](uint32_t Kb, auto fixed) {
+      s_body(Kb, fixed);
+      sched_pipelined<D / 8, 1, 4>();
+    };
+    // online softmax of the tile in sacc (lane value e of M tile mt is key
+    // kbase + 32 mt + 8 (e / 4) + 4 hg + e % 4 of the lane's column) -> P^T operands.
+    // The running max m_run is not raised tile by tile: p is formed against the current m_run and
+    // m_run is raised (with the O^T / l rescale) only when some p of the wave reaches 2^64 or is not
+    // finite -- on the first tile of a column and when scores grow by more than about 59 in log2
+    // units.  Every p then stays below 2^64, so P, l and O^T keep their float32 / bfloat16
+    // relative precision and cannot overflow; the result is the same softmax.
+    bf16x8_t pb[4];
+    auto softmax_tile = [&](int kbase) {
+      if (kbase + KT - 1 > wave_min) {
+        // keys with offset > lim get -inf; a per-element bit select (no lane-mask registers)
+        const int lim = pos - kbase - hg * 4;
+#pragma unroll
+        for (int mt = 0; mt < 2; ++mt)
+#pragma unroll
+          for (int e = 0; e < 16; ++e) {
+            const int koff = mt * 32 + (e >> 2) * 8 + (e & 3);
+            const uint32_t m = (uint32_t)((lim - koff) >> 31);   // all ones where koff > lim
+            sacc[mt][e] = __uint_as_float((__float_as_uint(sacc[mt][e]) & ~m) | (0xff800000u & m));
+          }
+      }
+      float psum = 0.f;
+      // 8 probabilities of slot group kk -> packed P^T operand, added to psum
+      auto emit = [&](int kk, const float* x) {
+        uint4 u;
+        u.x = pack_bf16x2(x[0], x[1]);
+        u.y = pack_bf16x2(x[2], x[3]);
+        u.z = pack_bf16x2(x[4], x[5]);
+        u.w = pack_bf16x2(x[6], x[7]);
+        pb[kk] = __builtin_bit_cast(bf16x8_t, u);
+        // l sums the float32 probabilities (exact denominators, also for the log-sum-exp output)
+#pragma unroll
+        for (int t = 0; t < 8; ++t) psum += x[t];
+      };
+      auto tile_max = [&]() {
+        float mx = sacc[0][0];
+#pragma unroll
+        for (int mt = 0; mt < 2; ++mt)
+#pragma unroll
+          for (int e = 0; e < 16; ++e) mx = fmaxf(mx, sacc[mt][e]);
+        return fmaxf(mx, __shfl_xor(mx, 32, 64));
+      };
+      auto rescale = [&](float alpha) {
+        l_run *= alpha;
+        if constexpr (PV) {
+#pragma unroll
+          for (int dt = 0; dt < D / 32; ++dt)
+#pragma unroll
+            for (int e = 0; e < 16; ++e) o[dt][e] *= alpha;
+        }
+      };
+      // p = 2^(c2 s - m_run)
+      auto expo = [&](float mneg) {
+        psum = 0.f;
+#pragma unroll
+        for (int kk = 0; kk < 4; ++kk) {
+          float x[8];
+#pragma unroll
+          for (int t = 0; t < 8; ++t)
+            x[t] = __builtin_amdgcn_exp2f(__builtin_fmaf(sacc[kk >> 1][(kk & 1) * 8 + t], c2, mneg));
+          emit(kk, x);
+        }
+      };
+      expo(-m_run);
+      if (__ballot(!(psum < 0x1p64f))) {
+        const float m_new = fmaxf(m_run, tile_max() * c2);          // c2 > 0
+        rescale(m_new == -INFINITY ? 1.f : __builtin_amdgcn_exp2f(m_run - m_new));
+        m_run = m_new;
+        expo(m_new == -INFINITY ? 0.f : -m_new);
+      }
+      l_run += psum;
+    };
+    // V^T operand addressing (transposed 8-byte reads): lane 4k + c of each 16-lane group points
+    // at row k, dims 4c .. 4c+3 of its 16-dim slice; the group's lane j receives dim j of 4 rows.
+    const int tg = lane >> 4;
+    const int tk = (lane & 15) >> 2;
+    const int tc = lane & 3;
+    // O^T += V^T P^T
+    // Lane part of the V^T read offsets, one per 32-dim tile: row 4 (tg >> 1) + tk of an 8-row
+    // group, dims 32 dt + 16 (tg & 1) + 4 tc .. +3 (16-byte chunk, 8-byte half).  The swizzle
+    // depends on the row only through row mod 4 = tk, so rows 16 kk + 8 h add a constant.
+    int vtr_off[D / 32];
+#pragma unroll
+    for (int dt = 0; dt < D / 32; ++dt) {
+      const int dchunk = 4 * dt + 2 * (tg & 1) + (tc >> 1);
+      vtr_off[dt] = (4 * (tg >> 1) + tk) * ROWB + ((dchunk ^ v_swz<NCH>(tk)) << 4) + (tc & 1) * 8;
+    }
+    auto pv_body = [&](uint32_t Vb, auto fixed) {
+      if constexpr (PV) {
+        if constexpr (!decltype(fixed)::value) asm volatile("" : "+s"(Vb));
+        // one base address per 32-dim tile for this tile's buffer (the empty asm keeps the compiler
+        // from re-associating the sums into one precomputed register per read); every read then
+        // adds its row constant as an immediate offset
+        uint32_t vbase[D / 32];
+#pragma unroll
+        for (int dt = 0; dt < D / 32; ++dt) {
+          vbase[dt] = Vb + (uint32_t)vtr_off[dt];
+          if constexpr (!decltype(fixed)::value) asm volatile("" : "+v"(vbase[dt]));
+        }
+#pragma unroll
+        for (int kk = 0; kk < 4; ++kk)
+#pragma unroll
+          for (int dt = 0; dt < D / 32; ++dt) {
+            shortx4_t h2[2];
+#pragma unroll
+            for (int h = 0; h < 2; ++h) {
+              // slots 8 hg + 4h + k <-> key 16 kk + 8 h + 4 hg + k (the P^T operand order)
+              h2[h] = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+                  (lds_shortx4_t*)(uintptr_t)(vbase[dt] + (uint32_t)((16 * kk + 8 * h) * ROWB)));
+            }
+            const bf16x8_t va = __builtin_bit_cast(
+                bf16x8_t, make_uint4(__builtin_bit_cast(uint2, h2[0]).x, __builtin_bit_cast(uint2, h2[0]).y,
+                                     __builtin_bit_cast(uint2, h2[1]).x, __builtin_bit_cast(uint2, h2[1]).y));
+            o[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, pb[kk], o[dt], 0, 0, 0);
+          }
+      }
+    };
+    auto pv_tile = [&](uint32_t Vb, auto fixed) {
+      if constexpr (PV) {
+        pv_body(Vb, fixed);
+        sched_pipelined<D / 8, 2, 4>();
+      }
+    };
+
+
+    // ---- ping-pong schedule over iterations j = 0 .. nkt.  Iteration j has two slots separated by
+    // workgroup barriers.  Group X (waves 0-3) runs its matrix phase M(j) = [P.V of tile j-1, S of
+    // tile j] in the first slot and the softmax of tile j in the second; group Y runs the softmax of
+    // tile j-1 in the first slot and M(j) in the second.  So in every slot one wave of each SIMD
+    // issues MFMAs while the other runs the softmax on the vector ALU.
+    // Tiles rotate through NBUF buffers: at the start of its softmax slot of iteration j each wave
+    // issues its share of the transfers of K(j+KD) and V(j+VD) (an issue that waits for the address
+    // unit then delays vector work, not MFMAs; issued at the end of the matrix phase instead they cost
+    // both attention kernels about 6 %); they have NBUF - 2 iterations to land (waited for at the end
+    // of iteration j + NBUF - 3) before they are read, and their buffers were last read in iteration
+    // j-1. ----
+    auto ncur = [&](int j) {   // transfers this wave issues in iteration j
+      return (j + KD >= 0 && j + KD < nkt ? IPW : 0) + (PV && j + VD >= 0 && j + VD < nkt ? IPW : 0);
+    };
+    // transfers of iterations j - NBUF + 4 .. j may still be in flight at the end of iteration j
+    auto inflight = [&](int j) {
+      int n = ncur(j);
+      if constexpr (NBUF == 4) n += ncur(j - 1);
+      return n;
+    };
+    // (iteration j works on key tile kt0 + j; the LDS buffers rotate with j.)  Prologue: K(0), then
+    // the transfers that iterations -(NBUF-2) .. -1 would have issued.
+    issue(a.k, k_last, kt0, ktile(0), false, blk_of(kt0));
+#pragma unroll
+    for (int jj = -(NBUF - 2); jj < 0; ++jj) {
+      if (jj + KD < nkt) issue(a.k, k_last, kt0 + jj + KD, ktile(jj + KD), false, blk_of(kt0 + jj + KD));
+      if constexpr (PV) {
+        if (jj + VD < nkt) issue(a.v, v_last, kt0 + jj + VD, vtile(jj + VD), true, blk_of(kt0 + jj + VD));
       }
     }
-  };
-  auto s_tile = [&](uint32_t Kb, auto fixed) {
-    s_body(Kb, fixed);
-    sched_pipelined<D / 8, 1, 4>();
-  };
-  // online softmax of the tile in sacc (lane value e of M tile mt is key
-  // kbase + 32 mt + 8 (e / 4) + 4 hg + e % 4 of the lane's column) -> P^T operands.
-  // The running max m_run is not raised tile by tile: p is formed against the current m_run and
-  // m_run is raised (with the O^T / l rescale) only when some p of the wave reaches 2^64 or is not
-  // finite -- on the first tile of a column and when scores grow by more than about 59 in log2
-  // units.  Every p then stays below 2^64, so P, l and O^T keep their float32 / bfloat16
-  // relative precision and cannot overflow; the result is the same softmax.
-  bf16x8_t pb[4];
-  auto softmax_tile = [&](int kbase) {
-    if (kbase + KT - 1 > wave_min) {
-      // keys with offset > lim get -inf; a per-element bit select (no lane-mask registers)
-      const int lim = pos - kbase - hg * 4;
-#pragma unroll
-      for (int mt = 0; mt < 2; ++mt)
-#pragma unroll
-        for (int e = 0; e < 16; ++e) {
-          const int koff = mt * 32 + (e >> 2) * 8 + (e & 3);
-          const uint32_t m = (uint32_t)((lim - koff) >> 31);   // all ones where koff > lim
-          sacc[mt][e] = __uint_as_float((__float_as_uint(sacc[mt][e]) & ~m) | (0xff800000u & m));
-        }
-    }
-    float psum = 0.f;
-    // 8 probabilities of slot group kk -> packed P^T operand, added to psum
-    auto emit = [&](int kk, const float* x) {
-      uint4 u;
-      u.x = pack_bf16x2(x[0], x[1]);
-      u.y = pack_bf16x2(x[2], x[3]);
-      u.z = pack_bf16x2(x[4], x[5]);
-      u.w = pack_bf16x2(x[6], x[7]);
-      pb[kk] = __builtin_bit_cast(bf16x8_t, u);
-      // l sums the float32 probabilities (exact denominators, also for the log-sum-exp output)
-#pragma unroll
-      for (int t = 0; t < 8; ++t) psum += x[t];
+    // block ids of the next transfer phase (scalar loads one iteration ahead, so their wait is never
+    // on the loop's critical path): V(j + VD) is the tile of the previous phase's K (VD = KD - 1)
+    static_assert(VD == KD - 1, "the V tile of a transfer phase is the K tile of the one before");
+    int32_t blk_k = blk_of(kt0 + KD), blk_v = blk_of(kt0 + KD - 1);
+    wait_vm(inflight(-1));   // K(0) has landed
+    __syncthreads();
+    // `ph` is j mod NBUF when known at compile time (integral constant >= 0), else -1: the tile
+    // buffers of the iteration are then constants
+    auto matrix_phase = [&](int j, auto ph) {
+      constexpr int PH = decltype(ph)::value;
+      constexpr bool FX = PH >= 0;
+      // the wave in its matrix phase issues first: its MFMAs are not held back by the other
+      // wave's softmax on the same SIMD
+      __builtin_amdgcn_s_setprio(2);
+      if (j >= 1 && j - 1 < nkt && (kt0 + j - 1) * KT <= wave_max)
+        pv_tile(FX ? vbuf_lds + (uint32_t)(((PH + NBUF - 1) % NBUF) * TILEB) : vtile_lds(j - 1),
+                std::integral_constant<bool, FX>{});
+      if (j < nkt && (kt0 + j) * KT <= wave_max)
+        s_tile(FX ? kbuf_lds + (uint32_t)(PH * TILEB) : ktile_lds(j), std::integral_constant<bool, FX>{});
+      __builtin_amdgcn_s_setprio(0);
     };
-    auto tile_max = [&]() {
-      float mx = sacc[0][0];
-#pragma unroll
-      for (int mt = 0; mt < 2; ++mt)
-#pragma unroll
-        for (int e = 0; e < 16; ++e) mx = fmaxf(mx, sacc[mt][e]);
-      return fmaxf(mx, __shfl_xor(mx, 32, 64));
-    };
-    auto rescale = [&](float alpha) {
-      l_run *= alpha;
+    // this wave's share of K(j+KD) and V(j+VD); tph = j mod NBUF (wave-uniform)
+    auto transfer_phase = [&](int j, int tph) {
+      const int kb = tph + KD >= NBUF ? tph + KD - NBUF : tph + KD;
+      const int vb = tph + VD >= NBUF ? tph + VD - NBUF : tph + VD;
+      if (j + KD < nkt) issue(a.k, k_last, kt0 + j + KD, kbuf + kb * TILEB, false, blk_k);
       if constexpr (PV) {
+        if (j + VD < nkt) issue(a.v, v_last, kt0 + j + VD, vbuf + vb * TILEB, true, blk_v);
+      }
+      if constexpr (PAGED) {
+        // a wave calls this once per iteration, in order: prefetch the next call's K block
+        blk_v = blk_k;
+        blk_k = blk_of(kt0 + j + 1 + KD);
+      }
+    };
+    auto vector_phase = [&](int j) {   // softmax of tile j
+      if (j >= 0 && j < nkt && (kt0 + j) * KT <= wave_max) softmax_tile((kt0 + j) * KT);
+    };
+    // Both groups run one loop body, U(j) = M(j) | barrier | T(j + grp), softmax of tile j | barrier.
+    // Group Y (grp = 1) is half an iteration ahead: it issues T(0) and passes one barrier before its
+    // first U, so its matrix phase M(j) runs beside group X's softmax of tile j - 1 and its softmax of
+    // tile j beside X's M(j + 1).  A wave waits for its transfers of iteration j - NBUF + 3 (all but
+    // those of T(j), the youngest) before the barrier that precedes its next matrix phase.  Every loop
+    // trip runs NBUF iterations with static buffer phases (every LDS offset of the matrix phase an
+    // immediate); iterations past nkt only pass their barriers.  Both groups pass the same number of
+    // barriers: Y's extra one at the start, X's at the end.
+    const int g1 = __builtin_amdgcn_readfirstlane(grp);
+    if (g1) {
+      transfer_phase(0, 0);
+      __syncthreads();
+    }
+    auto iter_u = [&](int j, auto ph) {
+      constexpr int PH = decltype(ph)::value;
+      matrix_phase(j, ph);
+      if (g1) wait_vm(inflight(j));
+      __syncthreads();
+      transfer_phase(j + g1, PH + g1 >= NBUF ? PH + g1 - NBUF : PH + g1);
+      vector_phase(j);
+      if (!g1) wait_vm(inflight(j));
+      __syncthreads();
+    };
+    for (int j = 0; j <= nkt; j += NBUF) {
+      iter_u(j, std::integral_constant<int, 0>{});
+      iter_u(j + 1, std::integral_constant<int, 1>{});
+      iter_u(j + 2, std::integral_constant<int, 2>{});
+      if constexpr (NBUF == 4) iter_u(j + 3, std::integral_constant<int, 3>{});
+    }
+    if (!g1) __syncthreads();
+
+    const float l_tot = l_run + __shfl_xor(l_run, 32, 64);
+    if constexpr (PV) {
+      if (valid) {
+        const float inv = 1.f / l_tot;
+        uint16_t* op = a.out + ((int64_t)(tok_off + ridx) * a.Hq + qh) * D;
 #pragma unroll
         for (int dt = 0; dt < D / 32; ++dt)
 #pragma unroll
-          for (int e = 0; e < 16; ++e) o[dt][e] *= alpha;
-      }
-    };
-    // p = 2^(c2 s - m_run)
-    auto expo = [&](float mneg) {
-      psum = 0.f;
-#pragma unroll
-      for (int kk = 0; kk < 4; ++kk) {
-        float x[8];
-#pragma unroll
-        for (int t = 0; t < 8; ++t)
-          x[t] = __builtin_amdgcn_exp2f(__builtin_fmaf(sacc[kk >> 1][(kk & 1) * 8 + t], c2, mneg));
-        emit(kk, x);
-      }
-    };
-    expo(-m_run);
-    if (__ballot(!(psum < 0x1p64f))) {
-      const float m_new = fmaxf(m_run, tile_max() * c2);          // c2 > 0
-      rescale(m_new == -INFINITY ? 1.f : __builtin_amdgcn_exp2f(m_run - m_new));
-      m_run = m_new;
-      expo(m_new == -INFINITY ? 0.f : -m_new);
-    }
-    l_run += psum;
-  };
-  // V^T operand addressing (transposed 8-byte reads): lane 4k + c of each 16-lane group points
-  // at row k, dims 4c .. 4c+3 of its 16-dim slice; the group's lane j receives dim j of 4 rows.
-  const int tg = lane >> 4;
-  const int tk = (lane & 15) >> 2;
-  const int tc = lane & 3;
-  // O^T += V^T P^T
-  // Lane part of the V^T read offsets, one per 32-dim tile: row 4 (tg >> 1) + tk of an 8-row
-  // group, dims 32 dt + 16 (tg & 1) + 4 tc .. +3 (16-byte chunk, 8-byte half).  The swizzle
-  // depends on the row only through row mod 4 = tk, so rows 16 kk + 8 h add a constant.
-  int vtr_off[D / 32];
-#pragma unroll
-  for (int dt = 0; dt < D / 32; ++dt) {
-    const int dchunk = 4 * dt + 2 * (tg & 1) + (tc >> 1);
-    vtr_off[dt] = (4 * (tg >> 1) + tk) * ROWB + ((dchunk ^ v_swz<NCH>(tk)) << 4) + (tc & 1) * 8;
-  }
-  auto pv_body = [&](uint32_t Vb, auto fixed) {
-    if constexpr (PV) {
-      if constexpr (!decltype(fixed)::value) asm volatile("" : "+s"(Vb));
-      // one base address per 32-dim tile for this tile's buffer (the empty asm keeps the compiler
-      // from re-associating the sums into one precomputed register per read); every read then
-      // adds its row constant as an immediate offset
-      uint32_t vbase[D / 32];
-#pragma unroll
-      for (int dt = 0; dt < D / 32; ++dt) {
-        vbase[dt] = Vb + (uint32_t)vtr_off[dt];
-        if constexpr (!decltype(fixed)::value) asm volatile("" : "+v"(vbase[dt]));
-      }
-#pragma unroll
-      for (int kk = 0; kk < 4; ++kk)
-#pragma unroll
-        for (int dt = 0; dt < D / 32; ++dt) {
-          shortx4_t h2[2];
-#pragma unroll
-          for (int h = 0; h < 2; ++h) {
-            // slots 8 hg + 4h + k <-> key 16 kk + 8 h + 4 hg + k (the P^T operand order)
-            h2[h] = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-                (lds_shortx4_t*)(uintptr_t)(vbase[dt] + (uint32_t)((16 * kk + 8 * h) * ROWB)));
+          for (int j = 0; j < 4; ++j) {
+            const int d = dt * 32 + j * 8 + hg * 4;
+            uint2 t;
+            t.x = pack_bf16x2(o[dt][4 * j + 0] * inv, o[dt][4 * j + 1] * inv);
+            t.y = pack_bf16x2(o[dt][4 * j + 2] * inv, o[dt][4 * j + 3] * inv);
+            *(uint2*)(op + d) = t;
           }
-          const bf16x8_t va = __builtin_bit_cast(
-              bf16x8_t, make_uint4(__builtin_bit_cast(uint2, h2[0]).x, __builtin_bit_cast(uint2, h2[0]).y,
-                                   __builtin_bit_cast(uint2, h2[1]).x, __builtin_bit_cast(uint2, h2[1]).y));
-          o[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, pb[kk], o[dt], 0, 0, 0);
-        }
+      }
     }
-  };
-  auto pv_tile = [&](uint32_t Vb, auto fixed) {
-    if constexpr (PV) {
-      pv_body(Vb, fixed);
-      sched_pipelined<D / 8, 2, 4>();
+    if (nsplit > 1) {
+      if (valid && hg == 0)
+        a.lse_part[((int64_t)piece * a.n_part_rows + p_off + ridx) * a.Hq + qh] = make_float2(m_run, l_tot);
+    } else if (a.lse && valid && hg == 0) {
+      const float lse2 = m_run + __log2f(l_tot);
+      a.lse[(int64_t)(tok_off + ridx) * a.Hq + qh] = a.lse_base2 ? lse2 : lse2 * 0.69314718055994531f;
     }
-  };
-
-
-  // ---- ping-pong schedule over iterations j = 0 .. nkt.  Iteration j has two slots separated by
-  // workgroup barriers.  Group X (waves 0-3) runs its matrix phase M(j) = [P.V of tile j-1, S of
-  // tile j] in the first slot and the softmax of tile j in the second; group Y runs the softmax of
-  // tile j-1 in the first slot and M(j) in the second.  So in every slot one wave of each SIMD
-  // issues MFMAs while the other runs the softmax on the vector ALU.
-  // Tiles rotate through NBUF buffers: at the start of its softmax slot of iteration j each wave
-  // issues its share of the transfers of K(j+KD) and V(j+VD) (an issue that waits for the address
-  // unit then delays vector work, not MFMAs; issued at the end of the matrix phase instead they cost
-  // both attention kernels about 6 %); they have NBUF - 2 iterations to land (waited for at the end
-  // of iteration j + NBUF - 3) before they are read, and their buffers were last read in iteration
-  // j-1. ----
-  auto ncur = [&](int j) {   // transfers this wave issues in iteration j
-    return (j + KD >= 0 && j + KD < nkt ? IPW : 0) + (PV && j + VD >= 0 && j + VD < nkt ? IPW : 0);
-  };
-  // transfers of iterations j - NBUF + 4 .. j may still be in flight at the end of iteration j
-  auto inflight = [&](int j) {
-    int n = ncur(j);
-    if constexpr (NBUF == 4) n += ncur(j - 1);
-    return n;
-  };
-  // (iteration j works on key tile kt0 + j; the LDS buffers rotate with j.)  Prologue: K(0), then
-  // the transfers that iterations -(NBUF-2) .. -1 would have issued.
-  issue(a.k, k_last, kt0, ktile(0), false, blk_of(kt0));
-#pragma unroll
-  for (int jj = -(NBUF - 2); jj < 0; ++jj) {
-    if (jj + KD < nkt) issue(a.k, k_last, kt0 + jj + KD, ktile(jj + KD), false, blk_of(kt0 + jj + KD));
-    if constexpr (PV) {
-      if (jj + VD < nkt) issue(a.v, v_last, kt0 + jj + VD, vtile(jj + VD), true, blk_of(kt0 + jj + VD));
-    }
+    if constexpr (!PERSIST) break;
   }
-  // block ids of the next transfer phase (scalar loads one iteration ahead, so their wait is never
-  // on the loop's critical path): V(j + VD) is the tile of the previous phase's K (VD = KD - 1)
-  static_assert(VD == KD - 1, "the V tile of a transfer phase is the K tile of the one before");
-  int32_t blk_k = blk_of(kt0 + KD), blk_v = blk_of(kt0 + KD - 1);
-  wait_vm(inflight(-1));   // K(0) has landed
-  __syncthreads();
-  // `ph` is j mod NBUF when known at compile time (integral constant >= 0), else -1: the tile
-  // buffers of the iteration are then constants
-  auto matrix_phase = [&](int j, auto ph) {
-    constexpr int PH = decltype(ph)::value;
-    constexpr bool FX = PH >= 0;
-    // the wave in its matrix phase issues first: its MFMAs are not held back by the other
-    // wave's softmax on the same SIMD
-    __builtin_amdgcn_s_setprio(2);
-    if (j >= 1 && j - 1 < nkt && (kt0 + j - 1) * KT <= wave_max)
-      pv_tile(FX ? vbuf_lds + (uint32_t)(((PH + NBUF - 1) % NBUF) * TILEB) : vtile_lds(j - 1),
-              std::integral_constant<bool, FX>{});
-    if (j < nkt && (kt0 + j) * KT <= wave_max)
-      s_tile(FX ? kbuf_lds + (uint32_t)(PH * TILEB) : ktile_lds(j), std::integral_constant<bool, FX>{});
-    __builtin_amdgcn_s_setprio(0);
-  };
-  // this wave's share of K(j+KD) and V(j+VD); tph = j mod NBUF (wave-uniform)
-  auto transfer_phase = [&](int j, int tph) {
-    const int kb = tph + KD >= NBUF ? tph + KD - NBUF : tph + KD;
-    const int vb = tph + VD >= NBUF ? tph + VD - NBUF : tph + VD;
-    if (j + KD < nkt) issue(a.k, k_last, kt0 + j + KD, kbuf + kb * TILEB, false, blk_k);
-    if constexpr (PV) {
-      if (j + VD < nkt) issue(a.v, v_last, kt0 + j + VD, vbuf + vb * TILEB, true, blk_v);
+  if constexpr (PERSIST) {
+    if (threadIdx.x == 0) {
+      const int nwg = (int)(gridDim.x / (unsigned)ka.Hkv);
+      if (__hip_atomic_fetch_add(ka.queue + ka.Hkv + kvh, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == nwg - 1) {
+        __hip_atomic_store(ka.queue + kvh, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        __hip_atomic_store(ka.queue + ka.Hkv + kvh, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      }
     }
-    if constexpr (PAGED) {
-      // a wave calls this once per iteration, in order: prefetch the next call's K block
-      blk_v = blk_k;
-      blk_k = blk_of(kt0 + j + 1 + KD);
-    }
-  };
-  auto vector_phase = [&](int j) {   // softmax of tile j
-    if (j >= 0 && j < nkt && (kt0 + j) * KT <= wave_max) softmax_tile((kt0 + j) * KT);
-  };
-  // Both groups run one loop body, U(j) = M(j) | barrier | T(j + grp), softmax of tile j | barrier.
-  // Group Y (grp = 1) is half an iteration ahead: it issues T(0) and passes one barrier before its
-  // first U, so its matrix phase M(j) runs beside group X's softmax of tile j - 1 and its softmax of
-  // tile j beside X's M(j + 1).  A wave waits for its transfers of iteration j - NBUF + 3 (all but
-  // those of T(j), the youngest) before the barrier that precedes its next matrix phase.  Every loop
-  // trip runs NBUF iterations with static buffer phases (every LDS offset of the matrix phase an
-  // immediate); iterations past nkt only pass their barriers.  Both groups pass the same number of
-  // barriers: Y's extra one at the start, X's at the end.
-  const int g1 = __builtin_amdgcn_readfirstlane(grp);
-  if (g1) {
-    transfer_phase(0, 0);
-    __syncthreads();
-  }
-  auto iter_u = [&](int j, auto ph) {
-    constexpr int PH = decltype(ph)::value;
-    matrix_phase(j, ph);
-    if (g1) wait_vm(inflight(j));
-    __syncthreads();
-    transfer_phase(j + g1, PH + g1 >= NBUF ? PH + g1 - NBUF : PH + g1);
-    vector_phase(j);
-    if (!g1) wait_vm(inflight(j));
-    __syncthreads();
-  };
-  for (int j = 0; j <= nkt; j += NBUF) {
-    iter_u(j, std::integral_constant<int, 0>{});
-    iter_u(j + 1, std::integral_constant<int, 1>{});
-    iter_u(j + 2, std::integral_constant<int, 2>{});
-    if constexpr (NBUF == 4) iter_u(j + 3, std::integral_constant<int, 3>{});
-  }
-  if (!g1) __syncthreads();
-
-  const float l_tot = l_run + __shfl_xor(l_run, 32, 64);
-  if constexpr (PV) {
-    if (valid) {
-      const float inv = 1.f / l_tot;
-      uint16_t* op = a.out + ((int64_t)(tok_off + ridx) * a.Hq + qh) * D;
-#pragma unroll
-      for (int dt = 0; dt < D / 32; ++dt)
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          const int d = dt * 32 + j * 8 + hg * 4;
-          uint2 t;
-          t.x = pack_bf16x2(o[dt][4 * j + 0] * inv, o[dt][4 * j + 1] * inv);
-          t.y = pack_bf16x2(o[dt][4 * j + 2] * inv, o[dt][4 * j + 3] * inv);
-          *(uint2*)(op + d) = t;
-        }
-    }
-  }
-  if (nsplit > 1) {
-    if (valid && hg == 0)
-      a.lse_part[((int64_t)piece * a.n_part_rows + p_off + ridx) * a.Hq + qh] = make_float2(m_run, l_tot);
-  } else if (a.lse && valid && hg == 0) {
-    const float lse2 = m_run + __log2f(l_tot);
-    a.lse[(int64_t)(tok_off + ridx) * a.Hq + qh] = a.lse_base2 ? lse2 : lse2 * 0.69314718055994531f;
   }
 }
 
@@ -736,7 +792,7 @@ __global__ __launch_bounds__(512, 1) void colsum_kernel(ColsumK a) {
   // stream the same request's probe columns
   int r, kt;
   locate_request((int)(blockIdx.x / (unsigned)a.Hkv), a.n_req,
-                 [&](int rr) { return (a.reqs[rr].T + KEYS - 1) / KEYS; }, &r, &kt);
+                 [&](int rr) { return (a.reqs[rr].T + KEYS - 1) / KEYS; }, &r, &kt, lane);
   if (r < 0) return;
   r = __builtin_amdgcn_readfirstlane(r);
   kt = __builtin_amdgcn_readfirstlane(kt);
@@ -1053,7 +1109,14 @@ hipError_t launch_mfma(const AttnLaunch& L, hipStream_t s) {
   a.nsplit = ns;
   a.lse_part = L.lse_part;
   a.n_part_rows = L.n_part_rows;
-  const dim3 grid((unsigned)(ntiles * ns * L.Hkv * L.n_req));
+  a.queue = L.queue;
+  int64_t per_head = ntiles * ns * L.n_req;   // items of one KV head (an upper bound: empty ones end at once)
+  if (PAGED && PV) {
+    // persistent grid: about one workgroup per compute unit and KV head, never more than the items
+    if (!L.queue) return hipErrorInvalidValue;
+    per_head = std::min<int64_t>(per_head, std::max(1, L.n_cu / L.Hkv));
+  }
+  const dim3 grid((unsigned)(per_head * L.Hkv));
   hipLaunchKernelGGL((attn_mfma_kernel<D, PAGED, PV>), grid, dim3(512), 0, s, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || ns == 1) return e;

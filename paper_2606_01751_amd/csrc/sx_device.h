@@ -29,13 +29,17 @@ __device__ __forceinline__ float wave_max(float v) {
   return v;
 }
 
+// Value of v in lane src of the wave (src taken mod 64).
+__device__ __forceinline__ int lane_value(int v, int src) { return __builtin_amdgcn_ds_bpermute(src << 2, v); }
+
 // Request-major position of a workgroup: position idx of the concatenation of every request's
 // items (cnt(r) items of request r, requests in order) -> request *r and item *q inside it; *r = -1
 // past the last item.  Every wave computes the same answer (no LDS, no barrier); cnt is called for
-// requests in runs of 64, one per lane.
+// requests in runs of 64, one per lane.  lane: the caller's lane index (threadIdx.x & 63; a kernel
+// that loops over items passes a copy the compiler cannot hoist, so the shuffle indices built from
+// it are not kept live across the loop).
 template <typename CountF>
-__device__ __forceinline__ void locate_request(int idx, int n_req, CountF cnt, int* r, int* q) {
-  const int lane = threadIdx.x & 63;
+__device__ __forceinline__ void locate_request(int idx, int n_req, CountF cnt, int* r, int* q, int lane) {
   int base = 0;
   for (int c0 = 0; c0 < n_req; c0 += 64) {
     const int rr = c0 + lane;
@@ -43,15 +47,15 @@ __device__ __forceinline__ void locate_request(int idx, int n_req, CountF cnt, i
     int x = c;   // inclusive prefix over the lanes
 #pragma unroll
     for (int o = 1; o < 64; o <<= 1) {
-      const int y = __shfl_up(x, o, 64);
+      const int y = lane_value(x, lane - o);
       if (lane >= o) x += y;
     }
-    const int tot = __shfl(x, 63, 64);
+    const int tot = __builtin_amdgcn_readlane(x, 63);
     if (idx < base + tot) {
       const uint64_t m = __ballot(base + x > idx);
       const int l = __ffsll((unsigned long long)m) - 1;
       *r = c0 + l;
-      *q = idx - (base + __shfl(x, l, 64) - __shfl(c, l, 64));
+      *q = idx - (base + __builtin_amdgcn_readlane(x, l) - __builtin_amdgcn_readlane(c, l));
       return;
     }
     base += tot;
@@ -60,15 +64,16 @@ __device__ __forceinline__ void locate_request(int idx, int n_req, CountF cnt, i
   *q = 0;
 }
 
-__device__ __forceinline__ int wave_max_i(int v) {
+// Largest and smallest v over the wave (lane as for locate_request).
+__device__ __forceinline__ int wave_max_i(int v, int lane) {
 #pragma unroll
-  for (int o = 32; o >= 1; o >>= 1) v = max(v, __shfl_xor(v, o, 64));
+  for (int o = 32; o >= 1; o >>= 1) v = max(v, lane_value(v, lane ^ o));
   return v;
 }
 
-__device__ __forceinline__ int wave_min_i(int v) {
+__device__ __forceinline__ int wave_min_i(int v, int lane) {
 #pragma unroll
-  for (int o = 32; o >= 1; o >>= 1) v = min(v, __shfl_xor(v, o, 64));
+  for (int o = 32; o >= 1; o >>= 1) v = min(v, lane_value(v, lane ^ o));
   return v;
 }
 

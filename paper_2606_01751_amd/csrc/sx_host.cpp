@@ -136,7 +136,7 @@ void free_plan(sx_plan* p) {
   if (!p) return;
   void* bufs[] = {p->d_req, p->d_bt, p->d_ra, p->d_cs, p->d_probe, p->d_nr, p->d_n_nr, p->d_n_probe,
                   p->d_flags, p->d_tok_row, p->d_rmark, p->d_lse, p->d_colsum,
-                  p->d_qp, p->d_lse2p, p->d_lsep, p->d_tok_pos, p->d_theta, p->d_topk};
+                  p->d_qp, p->d_lse2p, p->d_lsep, p->d_tok_pos, p->d_theta, p->d_topk, p->d_queue};
   for (void* b : bufs)
     if (b) (void)hipFree(b);
   delete p;
@@ -239,6 +239,9 @@ sx_status sx_plan_create(const sx_layer_desc* desc, const sx_request* requests, 
   p->n_dst_blocks = n_dst_blocks;
   p->n_src_blocks = n_src_blocks;
   (void)hipGetDevice(&p->device);
+  if (hipDeviceGetAttribute(&p->n_cu, hipDeviceAttributeMultiprocessorCount, p->device) != hipSuccess ||
+      p->n_cu < 1)
+    p->n_cu = 256;
 
   // ---- derive the per-token sets (Sections 3.2-3.3, Algorithm 1 steps 15-16) ----
   std::vector<sx::ReqDev> rdev(n_requests);
@@ -351,6 +354,7 @@ sx_status sx_plan_create(const sx_layer_desc* desc, const sx_request* requests, 
   if (st == SX_OK) st = dev_upload(p, &p->d_tok_pos, tok_pos);
   if (st == SX_OK) st = dev_upload(p, &p->d_theta, theta);
   if (st == SX_OK) st = dev_upload(p, &p->d_rmark, std::vector<uint32_t>((size_t)total, 0u));
+  if (st == SX_OK) st = dev_upload(p, &p->d_queue, std::vector<int32_t>(2 * (size_t)desc->n_kv_heads, 0));
   if (st == SX_OK) st = dev_alloc(p, &p->d_lse, (size_t)total * desc->n_q_heads);
   if (st == SX_OK) st = dev_alloc(p, &p->d_colsum, (size_t)total * desc->n_kv_heads);
   if (st == SX_OK) {
@@ -790,6 +794,8 @@ sx_status sx_sparse_attn(const sx_plan* p, const void* q, const int32_t* rows, c
   a.bt = p->d_bt;
   a.rows = rows;
   a.n_rows = n_rows;
+  a.queue = p->d_queue;
+  a.n_cu = p->n_cu;
   return check_launch(sx::launch_attn_paged(a, (hipStream_t)stream), "sx_sparse_attn launch");
 }
 

@@ -98,6 +98,8 @@ struct sx_plan {
   float2* d_lsep = nullptr;       // scratch [kLseSplit][n_probe][Hq]: partials of the split pass (bf16 plans)
   uint32_t* d_topk = nullptr;     // selection scratch, carved into `topk`
   sx::TopkScratch topk{};
+  int32_t* d_queue = nullptr;     // [2 Hkv] work-queue counters of sparse attention, zero between calls
+  int32_t n_cu = 0;               // compute units of the plan's device
 };
 
 namespace sx {
@@ -183,6 +185,10 @@ struct AttnLaunch {
   // [kLseSplit][n_part_rows][Hq] (n_part_rows = probe rows of all requests); NULL: no split
   float2* lse_part;
   int64_t n_part_rows;
+  // sparse attention (paged, with output): the plan's work-queue counters and its device's compute
+  // units (the persistent grid has about one workgroup per compute unit and KV head)
+  int32_t* queue;
+  int n_cu;
 };
 constexpr int kLseSplit = 4;   // most key pieces per row tile of the log-sum-exp pass
 hipError_t launch_attn_paged(const AttnLaunch& a, hipStream_t s);   // rows over a paged cache
