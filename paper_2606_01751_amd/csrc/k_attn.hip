@@ -64,7 +64,7 @@ struct AttnK {
   int nsplit;
   float2* lse_part;
   int64_t n_part_rows;
-  // sparse attention (paged, P.V): per-KV-head work queues, [0, Hkv) items taken and [Hkv, 2 Hkv)
+  // sparse attention (paged, P.V): per-KV-head work queues, [0, Hkv) items taken and [Hkv] the
   // workgroups finished, zero between launches
   int32_t* queue;
 };
@@ -143,21 +143,69 @@ __global__ __launch_bounds__(512, 1) void attn_mfma_kernel(AttnK ka) {
   // belong to one request and share its K/V tiles through that XCD's L2.  (Pieces of one row tile
   // are adjacent.)  Dense attention and the log-sum-exp pass launch one workgroup per item.
   // Sparse attention runs a persistent grid instead: about one workgroup per compute unit and KV
-  // head, each taking the head's next item from a queue whenever it finishes one, until the queue
-  // is empty.  The items then go to whichever compute unit frees first (greedy longest-first), with
-  // no gap for the hardware to dispatch another workgroup; the hardware's own dispatch hands the
-  // workgroups of an XCD to its shader engines in turn and holds the rest back while the next one's
-  // engine is full, which left a tenth of the compute units idle in the tail.  The last workgroup of
-  // a head to find the queue empty resets the head's counters for the next launch.
+  // head, each taking its head's next item from that head's queue whenever it finishes one.  The
+  // items then go to whichever compute unit frees first (greedy longest-first), with no gap for
+  // the hardware to dispatch another workgroup; the hardware's own dispatch hands the workgroups of
+  // an XCD to its shader engines in turn and holds the rest back while the next one's engine is
+  // full, which left a tenth of the compute units idle in the tail.  A workgroup whose head's queue
+  // is empty moves on to the head whose queue holds the most items (the XCDs do not run at one
+  // speed, so the fast ones finish the slow ones' last, lightest items), and stops when every queue
+  // is empty.  The last workgroup to stop resets the counters for the next launch.
   constexpr bool PERSIST = PAGED && PV;
-  __shared__ int s_item;
+  __shared__ int2 s_take[2];   // (head, item) taken by wave 0, alternating slots
   int item = (int)(blockIdx.x / (unsigned)ka.Hkv);
+  int takes = 0, n_items = 0;
+  if constexpr (PERSIST) {
+    // items of one head (every head has the same): row tiles of all requests
+    for (int c0 = 0; c0 < ka.n_req; c0 += 64) {
+      const int rr = c0 + (int)(threadIdx.x & 63);
+      int c = rr < ka.n_req ? (min(ka.n_rows[rr], ka.grid_rows) + ka.rpw - 1) / ka.rpw : 0;
+#pragma unroll
+      for (int o = 32; o >= 1; o >>= 1) c += __shfl_xor(c, o, 64);
+      n_items += __builtin_amdgcn_readfirstlane(c);
+    }
+  }
   for (;;) {
     if constexpr (PERSIST) {
-      if (threadIdx.x == 0)
-        s_item = __hip_atomic_fetch_add(ka.queue + kvh, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      // wave 0 takes the next item: from head kvh's queue, else from the fullest other queue (the
+      // counters read in one round trip, one lane per head); (-1, -1) when every queue is empty
+      if (threadIdx.x < 64) {
+        int2 t = make_int2(-1, -1);
+        for (;;) {
+          int v = 0;
+          if (threadIdx.x == 0)
+            v = __hip_atomic_fetch_add(ka.queue + kvh, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+          v = __builtin_amdgcn_readfirstlane(v);
+          if (v < n_items) {
+            t = make_int2(kvh, v);
+            break;
+          }
+          int left = 0;
+          for (int h0 = 0; h0 < ka.Hkv; h0 += 64) {
+            const int h = h0 + (int)threadIdx.x;
+            const int cnt =
+                h < ka.Hkv ? __hip_atomic_load(ka.queue + h, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) : n_items;
+            const int rem = n_items - min(cnt, n_items);
+            int mx = rem;
+#pragma unroll
+            for (int o = 32; o >= 1; o >>= 1) mx = max(mx, __shfl_xor(mx, o, 64));
+            mx = __builtin_amdgcn_readfirstlane(mx);
+            if (mx > left) {   // most items left, then the lowest head
+              left = mx;
+              kvh = h0 + (int)__ffsll((unsigned long long)__ballot(rem == mx)) - 1;
+            }
+          }
+          if (left == 0) break;
+        }
+        if (threadIdx.x == 0) s_take[takes & 1] = t;
+      }
       __syncthreads();
-      item = __builtin_amdgcn_readfirstlane(s_item);
+      const int2 t = s_take[takes & 1];
+      ++takes;
+      kvh = __builtin_amdgcn_readfirstlane(t.x);
+      asm("" : "+s"(kvh));
+      item = __builtin_amdgcn_readfirstlane(t.y);
+      if (kvh < 0) break;
     }
     // The kernel arguments and the lane values are formed again for every item (from the argument
     // segment and the thread index, both through opaque copies) rather than hoisted out of the item
@@ -668,11 +716,10 @@ __global__ __launch_bounds__(512, 1) void attn_mfma_kernel(AttnK ka) {
   }
   if constexpr (PERSIST) {
     if (threadIdx.x == 0) {
-      const int nwg = (int)(gridDim.x / (unsigned)ka.Hkv);
-      if (__hip_atomic_fetch_add(ka.queue + ka.Hkv + kvh, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == nwg - 1) {
-        __hip_atomic_store(ka.queue + kvh, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        __hip_atomic_store(ka.queue + ka.Hkv + kvh, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      }
+      const int done = __hip_atomic_fetch_add(ka.queue + ka.Hkv, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      if (done == (int)gridDim.x - 1)
+        for (int h = 0; h <= ka.Hkv; ++h)
+          __hip_atomic_store(ka.queue + h, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     }
   }
 }

@@ -354,7 +354,7 @@ sx_status sx_plan_create(const sx_layer_desc* desc, const sx_request* requests, 
   if (st == SX_OK) st = dev_upload(p, &p->d_tok_pos, tok_pos);
   if (st == SX_OK) st = dev_upload(p, &p->d_theta, theta);
   if (st == SX_OK) st = dev_upload(p, &p->d_rmark, std::vector<uint32_t>((size_t)total, 0u));
-  if (st == SX_OK) st = dev_upload(p, &p->d_queue, std::vector<int32_t>(2 * (size_t)desc->n_kv_heads, 0));
+  if (st == SX_OK) st = dev_upload(p, &p->d_queue, std::vector<int32_t>((size_t)desc->n_kv_heads + 1, 0));
   if (st == SX_OK) st = dev_alloc(p, &p->d_lse, (size_t)total * desc->n_q_heads);
   if (st == SX_OK) st = dev_alloc(p, &p->d_colsum, (size_t)total * desc->n_kv_heads);
   if (st == SX_OK) {

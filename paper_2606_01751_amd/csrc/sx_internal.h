@@ -98,7 +98,7 @@ struct sx_plan {
   float2* d_lsep = nullptr;       // scratch [kLseSplit][n_probe][Hq]: partials of the split pass (bf16 plans)
   uint32_t* d_topk = nullptr;     // selection scratch, carved into `topk`
   sx::TopkScratch topk{};
-  int32_t* d_queue = nullptr;     // [2 Hkv] work-queue counters of sparse attention, zero between calls
+  int32_t* d_queue = nullptr;     // [Hkv + 1] work-queue counters of sparse attention, zero between calls
   int32_t n_cu = 0;               // compute units of the plan's device
 };
 
