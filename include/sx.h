@@ -288,7 +288,10 @@ sx_status sx_sparse_attn(const sx_plan* plan, const void* q, const int32_t* rows
 /* Plain causal attention over dense fresh tensors (the hybrid layers below the threshold,
  * Section 3.4).  cu_seqlens is a DEVICE int32 array [n_requests + 1] of token offsets
  * (cu_seqlens[0] = 0); max_seqlen (host) must be >= every request length.  lse, when not NULL,
- * receives [sum T][Hq] float32 natural-log sums log(sum_j exp(scale * q.k_j)). */
+ * receives [sum T][Hq] float32 natural-log sums log(sum_j exp(scale * q.k_j)).  bfloat16 calls
+ * run a persistent grid whose work-queue counters sit in the library (64 slots per device,
+ * handed out in turn): at most 64 calls may be in flight on one device at a time.  A call made
+ * while its stream is being captured into a graph uses no counters (one workgroup per row tile). */
 sx_status sx_full_attn(const sx_layer_desc* desc, const void* q, const void* k, const void* v,
                        const int32_t* cu_seqlens, int32_t n_requests, int32_t max_seqlen, void* out,
                        float* lse, void* stream);

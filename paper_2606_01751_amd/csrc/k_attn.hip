@@ -64,9 +64,11 @@ struct AttnK {
   int nsplit;
   float2* lse_part;
   int64_t n_part_rows;
-  // sparse attention (paged, P.V): per-KV-head work queues, [0, Hkv) items taken and [Hkv] the
-  // workgroups finished, zero between launches
+  // persistent grids: per-KV-head work queues, [0, Hkv) items taken and [Hkv] the workgroups
+  // finished, zero between launches (sparse attention: the plan's; full attention: slot qslot of
+  // g_dense_queue)
   int32_t* queue;
+  int qslot;
 };
 
 typedef short shortx4_t __attribute__((ext_vector_type(4)));
@@ -115,7 +117,13 @@ __device__ __forceinline__ AttnK item_args(const AttnK& k) {
   }
 }
 
-template <int D, bool PAGED, bool PV>
+// Work-queue counters of persistent full attention, which has no plan: kDenseQueueSlots slots of
+// kDenseQueueStride counters on every device, a launch using slot qslot (the host hands the slots
+// out in turn, so launches that overlap in time use different slots; each launch leaves its slot
+// zero).
+__device__ int32_t g_dense_queue[kDenseQueueSlots * kDenseQueueStride];
+
+template <int D, bool PAGED, bool PV, bool PERSIST>
 __global__ __launch_bounds__(512, 1) void attn_mfma_kernel(AttnK ka) {
   constexpr int NW = 8;                       // waves: two groups of 4
   constexpr int ROWB = D * 2;                 // bytes of one key row
@@ -141,9 +149,10 @@ __global__ __launch_bounds__(512, 1) void attn_mfma_kernel(AttnK ka) {
   // Request-major order: for each KV head, the row tiles of request 0 (latest rows, i.e. most keys,
   // first), then those of request 1, ...  The workgroups running together on one XCD then mostly
   // belong to one request and share its K/V tiles through that XCD's L2.  (Pieces of one row tile
-  // are adjacent.)  Dense attention and the log-sum-exp pass launch one workgroup per item.
-  // Sparse attention runs a persistent grid instead: about one workgroup per compute unit and KV
-  // head, each taking its head's next item from that head's queue whenever it finishes one.  The
+  // are adjacent.)  The log-sum-exp pass launches one workgroup per item.  Attention with output
+  // (sparse, and full attention outside graph capture) runs a persistent grid instead: about one
+  // workgroup per compute unit and KV head, each taking its head's next item from that head's queue
+  // whenever it finishes one.  The
   // items then go to whichever compute unit frees first (greedy longest-first), with no gap for
   // the hardware to dispatch another workgroup; the hardware's own dispatch hands the workgroups of
   // an XCD to its shader engines in turn and holds the rest back while the next one's engine is
@@ -151,7 +160,8 @@ __global__ __launch_bounds__(512, 1) void attn_mfma_kernel(AttnK ka) {
   // is empty moves on to the head whose queue holds the most items (the XCDs do not run at one
   // speed, so the fast ones finish the slow ones' last, lightest items), and stops when every queue
   // is empty.  The last workgroup to stop resets the counters for the next launch.
-  constexpr bool PERSIST = PAGED && PV;
+  static_assert(!PERSIST || PV, "persistent grids run attention with output only");
+  int32_t* const queue = PAGED ? ka.queue : g_dense_queue + ka.qslot * kDenseQueueStride;
   __shared__ int2 s_take[2];   // (head, item) taken by wave 0, alternating slots
   int item = (int)(blockIdx.x / (unsigned)ka.Hkv);
   int takes = 0, n_items = 0;
@@ -159,7 +169,8 @@ __global__ __launch_bounds__(512, 1) void attn_mfma_kernel(AttnK ka) {
     // items of one head (every head has the same): row tiles of all requests
     for (int c0 = 0; c0 < ka.n_req; c0 += 64) {
       const int rr = c0 + (int)(threadIdx.x & 63);
-      int c = rr < ka.n_req ? (min(ka.n_rows[rr], ka.grid_rows) + ka.rpw - 1) / ka.rpw : 0;
+      const int nr = rr >= ka.n_req ? 0 : PAGED ? min(ka.n_rows[rr], ka.grid_rows) : ka.cu[rr + 1] - ka.cu[rr];
+      int c = (nr + ka.rpw - 1) / ka.rpw;
 #pragma unroll
       for (int o = 32; o >= 1; o >>= 1) c += __shfl_xor(c, o, 64);
       n_items += __builtin_amdgcn_readfirstlane(c);
@@ -174,7 +185,7 @@ __global__ __launch_bounds__(512, 1) void attn_mfma_kernel(AttnK ka) {
         for (;;) {
           int v = 0;
           if (threadIdx.x == 0)
-            v = __hip_atomic_fetch_add(ka.queue + kvh, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            v = __hip_atomic_fetch_add(queue + kvh, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
           v = __builtin_amdgcn_readfirstlane(v);
           if (v < n_items) {
             t = make_int2(kvh, v);
@@ -184,7 +195,7 @@ __global__ __launch_bounds__(512, 1) void attn_mfma_kernel(AttnK ka) {
           for (int h0 = 0; h0 < ka.Hkv; h0 += 64) {
             const int h = h0 + (int)threadIdx.x;
             const int cnt =
-                h < ka.Hkv ? __hip_atomic_load(ka.queue + h, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) : n_items;
+                h < ka.Hkv ? __hip_atomic_load(queue + h, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) : n_items;
             const int rem = n_items - min(cnt, n_items);
             int mx = rem;
 #pragma unroll
@@ -716,10 +727,10 @@ __global__ __launch_bounds__(512, 1) void attn_mfma_kernel(AttnK ka) {
   }
   if constexpr (PERSIST) {
     if (threadIdx.x == 0) {
-      const int done = __hip_atomic_fetch_add(ka.queue + ka.Hkv, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      const int done = __hip_atomic_fetch_add(queue + ka.Hkv, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
       if (done == (int)gridDim.x - 1)
         for (int h = 0; h <= ka.Hkv; ++h)
-          __hip_atomic_store(ka.queue + h, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+          __hip_atomic_store(queue + h, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     }
   }
 }
@@ -1127,6 +1138,10 @@ __global__ __launch_bounds__(512, 1) void colsum_kernel(ColsumK a) {
 
 template <int D, bool PAGED, bool PV>
 hipError_t launch_mfma(const AttnLaunch& L, hipStream_t s) {
+  // persistent grid: sparse attention always (the plan's counters), full attention when the host
+  // gave it a queue slot
+  constexpr bool kCanPersist = PV;
+  const bool persist = kCanPersist && (PAGED || L.qslot >= 0);
   AttnK a{};
   a.q = (const uint16_t*)L.q;
   a.k = (const uint16_t*)L.k;
@@ -1157,14 +1172,18 @@ hipError_t launch_mfma(const AttnLaunch& L, hipStream_t s) {
   a.lse_part = L.lse_part;
   a.n_part_rows = L.n_part_rows;
   a.queue = L.queue;
+  a.qslot = L.qslot;
   int64_t per_head = ntiles * ns * L.n_req;   // items of one KV head (an upper bound: empty ones end at once)
-  if (PAGED && PV) {
-    // persistent grid: about one workgroup per compute unit and KV head, never more than the items
-    if (!L.queue) return hipErrorInvalidValue;
+  if (persist) {
+    // about one workgroup per compute unit and KV head, never more than the items
+    if (PAGED ? !L.queue : (L.qslot >= kDenseQueueSlots || L.Hkv >= kDenseQueueStride)) return hipErrorInvalidValue;
     per_head = std::min<int64_t>(per_head, std::max(1, L.n_cu / L.Hkv));
   }
   const dim3 grid((unsigned)(per_head * L.Hkv));
-  hipLaunchKernelGGL((attn_mfma_kernel<D, PAGED, PV>), grid, dim3(512), 0, s, a);
+  if (persist)
+    hipLaunchKernelGGL((attn_mfma_kernel<D, PAGED, PV, kCanPersist>), grid, dim3(512), 0, s, a);
+  else
+    hipLaunchKernelGGL((attn_mfma_kernel<D, PAGED, PV, false>), grid, dim3(512), 0, s, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || ns == 1) return e;
   const dim3 mg((unsigned)((L.grid_rows * (int64_t)L.Hq + 255) / 256), (unsigned)L.n_req);

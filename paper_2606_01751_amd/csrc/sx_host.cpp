@@ -1,5 +1,6 @@
 // Host side of libsx: argument validation, plan construction (segment metadata, probe and base
 // row sets, cos/sin tables) and dispatch of the HIP kernels.  See include/sx.h for the ABI.
+#include <atomic>
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
@@ -799,6 +800,35 @@ sx_status sx_sparse_attn(const sx_plan* p, const void* q, const int32_t* rows, c
   return check_launch(sx::launch_attn_paged(a, (hipStream_t)stream), "sx_sparse_attn launch");
 }
 
+namespace {
+
+// Compute units of the current device (cached per device; 0 if unknown).
+int current_cu_count(int dev) {
+  static std::atomic<int> cache[kMaxDevices];
+  if (dev < 0 || dev >= kMaxDevices) return 0;
+  int n = cache[dev].load(std::memory_order_relaxed);
+  if (n == 0 && hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess && n > 0)
+    cache[dev].store(n, std::memory_order_relaxed);
+  return n > 0 ? n : 0;
+}
+
+// Work-queue slot of a persistent full-attention launch on device dev: the slots are handed out in
+// turn, so launches that overlap in time use different slots as long as fewer than
+// kDenseQueueSlots are in flight on the device.  -1 (one workgroup per item, no counters) while the
+// stream is being captured, since a graph node keeps its slot for every replay.
+int dense_queue_slot(int dev, hipStream_t s) {
+  static std::atomic<uint32_t> next[kMaxDevices];
+  if (dev < 0 || dev >= kMaxDevices) return -1;
+  hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
+  if (hipStreamIsCapturing(s, &cs) != hipSuccess || cs != hipStreamCaptureStatusNone) {
+    (void)hipGetLastError();
+    return -1;
+  }
+  return (int)(next[dev].fetch_add(1, std::memory_order_relaxed) % (uint32_t)sx::kDenseQueueSlots);
+}
+
+}  // namespace
+
 sx_status sx_full_attn(const sx_layer_desc* desc, const void* q, const void* k, const void* v,
                        const int32_t* cu_seqlens, int32_t n_requests, int32_t max_seqlen, void* out, float* lse,
                        void* stream) {
@@ -825,6 +855,11 @@ sx_status sx_full_attn(const sx_layer_desc* desc, const void* q, const void* k, 
   a.lse = lse;
   a.lse_base2 = 0;
   a.cu = cu_seqlens;
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+  a.n_cu = current_cu_count(dev);
+  a.qslot = a.n_cu > 0 && a.Hkv < sx::kDenseQueueStride ? dense_queue_slot(dev, (hipStream_t)stream) : -1;
   return check_launch(sx::launch_attn_dense(a, (hipStream_t)stream), "sx_full_attn launch");
 }
 

@@ -185,11 +185,16 @@ struct AttnLaunch {
   // [kLseSplit][n_part_rows][Hq] (n_part_rows = probe rows of all requests); NULL: no split
   float2* lse_part;
   int64_t n_part_rows;
-  // sparse attention (paged, with output): the plan's work-queue counters and its device's compute
-  // units (the persistent grid has about one workgroup per compute unit and KV head)
+  // persistent attention grids (about one workgroup per compute unit and KV head): sparse
+  // attention's work-queue counters (the plan's), full attention's queue slot (-1: one workgroup per
+  // item, as under graph capture), and the device's compute units
   int32_t* queue;
+  int qslot;
   int n_cu;
 };
+// queue slots of persistent full attention on one device, and counters per slot (KV heads + 1)
+constexpr int kDenseQueueSlots = 64;
+constexpr int kDenseQueueStride = 256;
 constexpr int kLseSplit = 4;   // most key pieces per row tile of the log-sum-exp pass
 hipError_t launch_attn_paged(const AttnLaunch& a, hipStream_t s);   // rows over a paged cache
 hipError_t launch_attn_dense(const AttnLaunch& a, hipStream_t s);   // all rows, dense K/V
