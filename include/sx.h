@@ -222,7 +222,11 @@ sx_status sx_realign_scatter_layers(const sx_plan* plan, int32_t n_layers, const
  * sx_realign_scatter_masked: mask[off_r + t] = 1 for every listed row t of request r
  * (rows[off_r .. off_r + min(n_rows[r], max_rows))), 0 for every other token of the plan.
  * mask is caller-owned DEVICE memory of sum T bytes; rows/n_rows/max_rows as in sx_kv_scatter.
- * Listed values outside [0, T_r) are ignored.  Two kernels on `stream`, no host sync. */
+ * Listed values outside [0, T_r) are ignored.  Two kernels on `stream`, no host sync.  bfloat16
+ * plans: a third kernel plans, in the plan's scratch, the order in which sx_sparse_attn takes its
+ * row tiles (Multifit over their estimated costs); sx_sparse_attn uses it when called with the
+ * same rows, n_rows and max_rows, as the sparse layers that share R are (Section 3.4).  The order
+ * changes only which workgroup computes a row tile, never a result. */
 sx_status sx_rows_mask(const sx_plan* plan, const int32_t* rows, const int32_t* n_rows, int32_t max_rows,
                        uint8_t* mask, void* stream);
 
@@ -280,7 +284,8 @@ sx_status sx_topk_select(const sx_plan* plan, const float* scores, double ratio,
  * accumulation and bfloat16 probabilities; float32 runs on vector ALUs.  max_rows as in
  * sx_kv_scatter: the rows n >= min(n_rows[r], max_rows) are neither computed nor written, so the
  * attention covers exactly the rows whose K/V sx_kv_scatter writes for the same list.  Uses the
- * plan's work-queue counters (bfloat16), so calls sharing a plan must be stream-ordered. */
+ * plan's work-queue counters (bfloat16), so calls sharing a plan must be stream-ordered; takes its
+ * row tiles in the order sx_rows_mask planned for the same row list, if any. */
 sx_status sx_sparse_attn(const sx_plan* plan, const void* q, const int32_t* rows, const int32_t* n_rows,
                          int32_t max_rows, const void* k_cache, const void* v_cache, void* out,
                          void* stream);

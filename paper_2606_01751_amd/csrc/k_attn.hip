@@ -69,6 +69,9 @@ struct AttnK {
   // g_dense_queue)
   int32_t* queue;
   int qslot;
+  // sparse attention: planned order of the queue items (tile_order_kernel; NULL or out[0] != the
+  // item count: the queue's own order)
+  const int32_t* order;
 };
 
 typedef short shortx4_t __attribute__((ext_vector_type(4)));
@@ -176,6 +179,7 @@ __global__ __launch_bounds__(512, 1) void attn_mfma_kernel(AttnK ka) {
       n_items += __builtin_amdgcn_readfirstlane(c);
     }
   }
+  const bool use_order = PERSIST && PAGED && ka.order && ka.order[0] == n_items;
   for (;;) {
     if constexpr (PERSIST) {
       // wave 0 takes the next item: from head kvh's queue, else from the fullest other queue (the
@@ -188,7 +192,7 @@ __global__ __launch_bounds__(512, 1) void attn_mfma_kernel(AttnK ka) {
             v = __hip_atomic_fetch_add(queue + kvh, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
           v = __builtin_amdgcn_readfirstlane(v);
           if (v < n_items) {
-            t = make_int2(kvh, v);
+            t = make_int2(kvh, use_order ? ka.order[1 + v] : v);
             break;
           }
           int left = 0;
@@ -735,6 +739,130 @@ __global__ __launch_bounds__(512, 1) void attn_mfma_kernel(AttnK ka) {
   }
 }
 
+// Order in which persistent sparse attention takes its row tiles (the same for every KV head), from
+// the tiles' estimated costs: key tiles up to the tile's last row plus kOrderCost0 for the work
+// outside the tile loop.  Taking the tiles longest first (the queue's own order) is the greedy
+// longest-processing-time schedule; this kernel plans a tighter one with Multifit (the smallest
+// bin capacity for which first-fit-decreasing packs the tiles into m bins, m being the
+// workgroups per head, found by a parallel search over candidate capacities) and lists the tiles
+// by their planned start, so that the workgroups, each taking the next tile when it finishes one,
+// follow the plan.  One workgroup of 1024 threads; out[0] = number of tiles n, out[1 + k] = the
+// queue item taken k-th; out[0] = -1 (the queue's order) when n > 8 m or m > 64.
+// Every item index of [0, n) appears exactly once, whatever the costs.
+constexpr int kOrderCost0 = 4;
+
+// Position of key[i] among key[0, n) in ascending order (the keys are distinct).
+__device__ __forceinline__ int rank_of(const uint32_t* key, int n, int i) {
+  const uint32_t k = key[i];
+  int r = 0;
+  for (int j = 0; j < n; ++j) r += key[j] < k ? 1 : 0;
+  return r;
+}
+
+__global__ __launch_bounds__(1024) void tile_order_kernel(const ReqDev* __restrict__ reqs,
+                                                          const int32_t* __restrict__ rows,
+                                                          const int32_t* __restrict__ n_rows, int max_rows,
+                                                          int n_req, int rpw, int m, int32_t* __restrict__ out) {
+  constexpr int NMAX = kOrderMax;   // items planned: at most 8 per bin, at most 64 bins
+  static_assert(NMAX == 8 * 64, "eight items per bin, 64 bins");
+  __shared__ uint32_t key[NMAX];
+  __shared__ int32_t item[NMAX];   // queue item of the k-th largest cost
+  __shared__ int32_t cost[NMAX];   // its cost
+  __shared__ int s_n, s_sum, s_max, s_lo, s_hi;
+  __shared__ int s_ok[16];
+  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
+  if (tid == 0) {
+    int n = 0;
+    for (int r = 0; r < n_req; ++r) n += (min(n_rows[r], max_rows) + rpw - 1) / rpw;
+    s_n = n;
+    s_sum = 0;
+    s_max = 0;
+  }
+  __syncthreads();
+  const int n = s_n;
+  if (n > NMAX || n > 8 * m || m > 64 || m < 1) {
+    if (tid == 0) out[0] = -1;
+    return;
+  }
+  // costs in the queue's item order (request-major, each request's last row tile first), keyed for
+  // decreasing cost, then increasing item
+  int base = 0;
+  for (int r = 0; r < n_req; ++r) {
+    const int nr = min(n_rows[r], max_rows);
+    const int t = (nr + rpw - 1) / rpw;
+    const int tok_off = reqs[r].tok_off;
+    for (int rank = tid; rank < t; rank += blockDim.x) {
+      const int row_tile = t - 1 - rank;
+      const int last = min((row_tile + 1) * rpw, nr) - 1;
+      const int c = rows[tok_off + last] / KT + 1 + kOrderCost0;
+      key[base + rank] = ((uint32_t)(0xFFFF - min(c, 0xFFFF)) << 16) | (uint32_t)(base + rank);
+      atomicAdd(&s_sum, c);
+      atomicMax(&s_max, c);
+    }
+    base += t;
+  }
+  __syncthreads();
+  for (int i = tid; i < n; i += blockDim.x) {
+    const int k = rank_of(key, n, i);
+    item[k] = (int)(key[i] & 0xFFFF);
+    cost[k] = 0xFFFF - (int)(key[i] >> 16);
+  }
+  if (tid == 0) {
+    const int lb = max(s_max, (s_sum + m - 1) / m);
+    s_lo = lb - 1;                                   // no packing fits below the lower bound
+    s_hi = max(s_max, (2 * s_sum + m - 1) / m);      // first-fit decreasing always fits here
+  }
+  __syncthreads();
+  // every wave holds the costs in registers: lane l has cost[l + 64 k] in creg[k]
+  int creg[NMAX / 64];
+#pragma unroll
+  for (int k = 0; k < NMAX / 64; ++k) creg[k] = lane + 64 * k < n ? cost[lane + 64 * k] : 0;
+  // first-fit decreasing into m bins of capacity C by one wave (lane b holds bin b's load); returns
+  // whether every item fitted.  With rec, key[i] = (planned start << 6) | bin of the i-th item.
+  auto ffd = [&](int C, bool rec) -> bool {
+    int load = 0;
+#pragma unroll
+    for (int k = 0; k < NMAX / 64; ++k) {
+      for (int j = 0; j < 64; ++j) {
+        const int i = 64 * k + j;
+        if (i >= n) return true;
+        const int c = __builtin_amdgcn_readlane(creg[k], j);
+        const uint64_t fits = __ballot(lane < m && load + c <= C);
+        if (fits == 0) return false;
+        const int b = (int)__ffsll((unsigned long long)fits) - 1;
+        if (lane == b) {
+          if (rec) key[i] = ((uint32_t)load << 6) | (uint32_t)b;
+          load += c;
+        }
+      }
+    }
+    return true;
+  };
+  // parallel search: every wave tries one capacity of (lo, hi], the interval shrinks 16-fold
+  while (s_hi - s_lo > 1) {
+    const int lo = s_lo, hi = s_hi;
+    const int C = lo + (int)(((int64_t)(hi - lo) * (wv + 1) + 15) / 16);
+    const bool ok = ffd(C, false);
+    if (lane == 0) s_ok[wv] = ok ? C : -C;
+    __syncthreads();
+    if (tid == 0) {
+      int nlo = lo, nhi = hi;
+      for (int w = 0; w < 16; ++w) {
+        if (s_ok[w] > 0) nhi = min(nhi, s_ok[w]);
+        else nlo = max(nlo, -s_ok[w]);
+      }
+      s_lo = nlo;
+      s_hi = nhi;
+    }
+    __syncthreads();
+  }
+  // the chosen packing: planned start and bin of every item, then the items in order of start
+  if (wv == 0) ffd(s_hi, true);
+  __syncthreads();
+  for (int i = tid; i < n; i += blockDim.x) out[1 + rank_of(key, n, i)] = item[i];
+  if (tid == 0) out[0] = n;
+}
+
 // Log-sum-exp of the pieces of the split log-sum-exp pass, for one (probe row, query head) per
 // thread: lse2 = m + log2(sum_i l_i 2^(m_i - m)) over the pieces that saw a key (l_i > 0), with m
 // their largest running max, combined in piece order.  blockIdx.y = request.
@@ -1173,6 +1301,7 @@ hipError_t launch_mfma(const AttnLaunch& L, hipStream_t s) {
   a.n_part_rows = L.n_part_rows;
   a.queue = L.queue;
   a.qslot = L.qslot;
+  a.order = L.order;
   int64_t per_head = ntiles * ns * L.n_req;   // items of one KV head (an upper bound: empty ones end at once)
   if (persist) {
     // about one workgroup per compute unit and KV head, never more than the items
@@ -1205,6 +1334,17 @@ hipError_t launch_attn_paged(const AttnLaunch& a, hipStream_t s) {
   if (pv && a.lse != nullptr) return hipErrorInvalidValue;
   if (a.D == 128) return pv ? launch_mfma<128, true, true>(a, s) : launch_mfma<128, true, false>(a, s);
   return pv ? launch_mfma<64, true, true>(a, s) : launch_mfma<64, true, false>(a, s);
+}
+
+hipError_t launch_tile_order(const sx_plan* p, const int32_t* rows, const int32_t* n_rows, int32_t max_rows,
+                             hipStream_t s) {
+  const int G = p->desc.n_q_heads / p->desc.n_kv_heads;
+  const int rpw = COLS / G;
+  const int64_t items = (int64_t)(max_rows + rpw - 1) / rpw * p->n_req;   // as the attention launch bounds them
+  const int m = (int)std::min<int64_t>(items, std::max(1, p->n_cu / p->desc.n_kv_heads));
+  hipLaunchKernelGGL(tile_order_kernel, dim3(1), dim3(1024), 0, s, p->d_req, rows, n_rows, max_rows, p->n_req, rpw,
+                     std::max(m, 1), p->d_order);
+  return hipGetLastError();
 }
 
 hipError_t launch_attn_dense(const AttnLaunch& a, hipStream_t s) {

@@ -137,7 +137,8 @@ void free_plan(sx_plan* p) {
   if (!p) return;
   void* bufs[] = {p->d_req, p->d_bt, p->d_ra, p->d_cs, p->d_probe, p->d_nr, p->d_n_nr, p->d_n_probe,
                   p->d_flags, p->d_tok_row, p->d_rmark, p->d_lse, p->d_colsum,
-                  p->d_qp, p->d_lse2p, p->d_lsep, p->d_tok_pos, p->d_theta, p->d_topk, p->d_queue};
+                  p->d_qp, p->d_lse2p, p->d_lsep, p->d_tok_pos, p->d_theta, p->d_topk, p->d_queue,
+                  p->d_order};
   for (void* b : bufs)
     if (b) (void)hipFree(b);
   delete p;
@@ -356,6 +357,7 @@ sx_status sx_plan_create(const sx_layer_desc* desc, const sx_request* requests, 
   if (st == SX_OK) st = dev_upload(p, &p->d_theta, theta);
   if (st == SX_OK) st = dev_upload(p, &p->d_rmark, std::vector<uint32_t>((size_t)total, 0u));
   if (st == SX_OK) st = dev_upload(p, &p->d_queue, std::vector<int32_t>((size_t)desc->n_kv_heads + 1, 0));
+  if (st == SX_OK) st = dev_upload(p, &p->d_order, std::vector<int32_t>(1 + (size_t)sx::kOrderMax, -1));
   if (st == SX_OK) st = dev_alloc(p, &p->d_lse, (size_t)total * desc->n_q_heads);
   if (st == SX_OK) st = dev_alloc(p, &p->d_colsum, (size_t)total * desc->n_kv_heads);
   if (st == SX_OK) {
@@ -527,8 +529,17 @@ sx_status sx_rows_mask(const sx_plan* p, const int32_t* rows, const int32_t* n_r
     sx_status st = device_rows_ok(p, rows, n_rows, max_rows, stream, "sx_rows_mask");
     if (st != SX_OK) return st;
   }
-  return check_launch(sx::launch_rows_mask(p, rows, n_rows, max_rows, mask, (hipStream_t)stream),
-                      "sx_rows_mask launch");
+  sx_status st = check_launch(sx::launch_rows_mask(p, rows, n_rows, max_rows, mask, (hipStream_t)stream),
+                              "sx_rows_mask launch");
+  if (st != SX_OK || p->desc.dtype != SX_BF16) return st;
+  // the planned row-tile order of sx_sparse_attn for this row list
+  st = check_launch(sx::launch_tile_order(p, rows, n_rows, max_rows, (hipStream_t)stream), "sx_rows_mask order launch");
+  if (st == SX_OK) {
+    p->order_rows = rows;
+    p->order_n_rows = n_rows;
+    p->order_max_rows = max_rows;
+  }
+  return st;
 }
 
 sx_status sx_realign_scatter_masked(const sx_plan* p, const void* src_k, const void* src_v, const void* k_new,
@@ -797,6 +808,7 @@ sx_status sx_sparse_attn(const sx_plan* p, const void* q, const int32_t* rows, c
   a.n_rows = n_rows;
   a.queue = p->d_queue;
   a.n_cu = p->n_cu;
+  a.order = rows == p->order_rows && n_rows == p->order_n_rows && max_rows == p->order_max_rows ? p->d_order : nullptr;
   return check_launch(sx::launch_attn_paged(a, (hipStream_t)stream), "sx_sparse_attn launch");
 }
 

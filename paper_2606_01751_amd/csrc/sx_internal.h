@@ -100,6 +100,12 @@ struct sx_plan {
   sx::TopkScratch topk{};
   int32_t* d_queue = nullptr;     // [Hkv + 1] work-queue counters of sparse attention, zero between calls
   int32_t n_cu = 0;               // compute units of the plan's device
+  // [1 + kOrderMax] planned row-tile order of sparse attention, written by sx_rows_mask for the row
+  // list it was given (bf16 plans); sx_sparse_attn uses it for the same rows / n_rows / max_rows
+  int32_t* d_order = nullptr;
+  mutable const int32_t* order_rows = nullptr;
+  mutable const int32_t* order_n_rows = nullptr;
+  mutable int32_t order_max_rows = -1;
 };
 
 namespace sx {
@@ -191,7 +197,12 @@ struct AttnLaunch {
   int32_t* queue;
   int qslot;
   int n_cu;
+  const int32_t* order;   // sparse attention: the plan's planned tile order, or NULL
 };
+constexpr int kOrderMax = 512;   // most row tiles the tile order is planned for (8 per workgroup, 64 workgroups)
+// planned order of sparse attention's row tiles for the row list (plan->d_order)
+hipError_t launch_tile_order(const sx_plan* p, const int32_t* rows, const int32_t* n_rows, int32_t max_rows,
+                             hipStream_t s);
 // queue slots of persistent full attention on one device, and counters per slot (KV heads + 1)
 constexpr int kDenseQueueSlots = 64;
 constexpr int kDenseQueueStride = 256;

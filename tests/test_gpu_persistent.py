@@ -125,3 +125,38 @@ def test_sparse_attention_graph_replays_and_fewer_rows():
             a, b = offs[r], offs[r] + int(n[r] // 2)
             assert torch.equal(fewer[a:b], want[a:b]), f"request {r} with half its rows before replay {i}"
             assert not fewer[b:offs[r] + int(n[r])].any(), f"request {r}: rows past the bound written"
+
+
+def test_sparse_attention_planned_tile_order():
+    """sx_rows_mask plans the order in which sx_sparse_attn takes its row tiles for the same row list;
+    the result must not change, also when n_rows changes at the same address after the plan was
+    made (the attention then sees a different tile count and keeps the queue's own order)."""
+    w = _workload()
+    log("[persistent] sparse attention with the planned tile order of sx_rows_mask")
+    g = GpuLayer(w, W.layer_tensors(w, 0))
+    ratio = 0.3
+    g.realign()
+    g.scatter_nonreused()
+    g.score()
+    g.select(ratio)
+    g.scatter_rows(ratio)
+    m = g.plan.budget(ratio)[1]
+    want = torch.zeros_like(g.out)
+    sx.sparse_attn(g.plan, g.t["q"], g.rows, g.n_rows, m, g.k_cache, g.v_cache, want)
+    mask = torch.zeros(w.total_tokens, dtype=torch.uint8, device="cuda")
+    sx.rows_mask(g.plan, g.rows, g.n_rows, m, mask)
+    for i in range(2):
+        out = torch.zeros_like(g.out)
+        sx.sparse_attn(g.plan, g.t["q"], g.rows, g.n_rows, m, g.k_cache, g.v_cache, out)
+        torch.cuda.synchronize()
+        assert torch.equal(out, want), f"planned order, call {i}"
+    n = g.n_rows.cpu().numpy()
+    g.n_rows.copy_(torch.from_numpy((n // 2).astype(np.int32)))
+    out = torch.zeros_like(g.out)
+    sx.sparse_attn(g.plan, g.t["q"], g.rows, g.n_rows, m, g.k_cache, g.v_cache, out)
+    torch.cuda.synchronize()
+    offs = w.token_offsets
+    for r in range(len(w.requests)):
+        a, b = offs[r], offs[r] + int(n[r] // 2)
+        assert torch.equal(out[a:b], want[a:b]), f"request {r} with half its rows after the plan"
+        assert not out[b:offs[r] + int(n[r])].any()
