@@ -751,11 +751,16 @@ __global__ __launch_bounds__(512, 1) void attn_mfma_kernel(AttnK ka) {
 // Every item index of [0, n) appears exactly once, whatever the costs.
 constexpr int kOrderCost0 = 4;
 
-// Position of key[i] among key[0, n) in ascending order (the keys are distinct).
+// Position of key[i] among key[0, n) in ascending order (the keys are distinct; key is 16-byte
+// aligned and holds 0xFFFFFFFF from n up to the next multiple of 4).
 __device__ __forceinline__ int rank_of(const uint32_t* key, int n, int i) {
   const uint32_t k = key[i];
   int r = 0;
-  for (int j = 0; j < n; ++j) r += key[j] < k ? 1 : 0;
+#pragma unroll 4
+  for (int j = 0; j < n; j += 4) {
+    const uint4 q = *(const uint4*)(key + j);
+    r += (q.x < k ? 1 : 0) + (q.y < k ? 1 : 0) + (q.z < k ? 1 : 0) + (q.w < k ? 1 : 0);
+  }
   return r;
 }
 
@@ -765,10 +770,11 @@ __global__ __launch_bounds__(1024) void tile_order_kernel(const ReqDev* __restri
                                                           int n_req, int rpw, int m, int32_t* __restrict__ out) {
   constexpr int NMAX = kOrderMax;   // items planned: at most 8 per bin, at most 64 bins
   static_assert(NMAX == 8 * 64, "eight items per bin, 64 bins");
-  __shared__ uint32_t key[NMAX];
+  __shared__ __attribute__((aligned(16))) uint32_t key[NMAX];
   __shared__ int32_t item[NMAX];   // queue item of the k-th largest cost
   __shared__ int32_t cost[NMAX];   // its cost
-  __shared__ int s_n, s_sum, s_max, s_lo, s_hi;
+  __shared__ uint32_t plan[16][NMAX];   // each wave's packing: planned start << 6 | bin per item
+  __shared__ int s_n, s_sum, s_max, s_lo, s_hi, s_hi0, s_best, s_fail;
   __shared__ int s_ok[16];
   const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
   if (tid == 0) {
@@ -780,8 +786,8 @@ __global__ __launch_bounds__(1024) void tile_order_kernel(const ReqDev* __restri
   }
   __syncthreads();
   const int n = s_n;
-  if (n > NMAX || n > 8 * m || m > 64 || m < 1) {
-    if (tid == 0) out[0] = -1;
+  if (n > NMAX || n > 8 * m || m > 64 || m < 1 || n == 0) {
+    if (tid == 0) out[0] = n == 0 ? 0 : -1;
     return;
   }
   // costs in the queue's item order (request-major, each request's last row tile first), keyed for
@@ -801,6 +807,7 @@ __global__ __launch_bounds__(1024) void tile_order_kernel(const ReqDev* __restri
     }
     base += t;
   }
+  for (int i = n + tid; i < ((n + 3) & ~3); i += blockDim.x) key[i] = 0xFFFFFFFFu;
   __syncthreads();
   for (int i = tid; i < n; i += blockDim.x) {
     const int k = rank_of(key, n, i);
@@ -810,7 +817,10 @@ __global__ __launch_bounds__(1024) void tile_order_kernel(const ReqDev* __restri
   if (tid == 0) {
     const int lb = max(s_max, (s_sum + m - 1) / m);
     s_lo = lb - 1;                                   // no packing fits below the lower bound
-    s_hi = max(s_max, (2 * s_sum + m - 1) / m);      // first-fit decreasing always fits here
+    s_hi0 = max(s_max, (2 * s_sum + m - 1) / m);     // first-fit decreasing always fits here
+    s_hi = min(s_hi0, lb + lb / 4 + 1);              // where it usually fits already
+    s_best = -1;
+    s_fail = 0;
   }
   __syncthreads();
   // every wave holds the costs in registers: lane l has cost[l + 64 k] in creg[k]
@@ -820,44 +830,65 @@ __global__ __launch_bounds__(1024) void tile_order_kernel(const ReqDev* __restri
   // first-fit decreasing into m bins of capacity C by one wave (lane b holds bin b's load); returns
   // whether every item fitted.  With rec, key[i] = (planned start << 6) | bin of the i-th item.
   auto ffd = [&](int C, bool rec) -> bool {
-    int load = 0;
+    // branch-free per item (a branch per step made the pass several times slower); lanes past
+    // the bins hold a load no item fits on
+    int load = lane < m ? 0 : 0x3FFFFFFF;
+    bool ok = true;
 #pragma unroll
     for (int k = 0; k < NMAX / 64; ++k) {
-      for (int j = 0; j < 64; ++j) {
-        const int i = 64 * k + j;
-        if (i >= n) return true;
+      const int jn = min(64, n - 64 * k);
+      for (int j = 0; j < jn; ++j) {
         const int c = __builtin_amdgcn_readlane(creg[k], j);
-        const uint64_t fits = __ballot(lane < m && load + c <= C);
-        if (fits == 0) return false;
-        const int b = (int)__ffsll((unsigned long long)fits) - 1;
-        if (lane == b) {
-          if (rec) key[i] = ((uint32_t)load << 6) | (uint32_t)b;
-          load += c;
-        }
+        const int cand = load + c;
+        const uint64_t fits = __ballot(cand <= C);
+        ok = ok && fits != 0;
+        const int b = fits ? (int)__builtin_ctzll(fits) : 64;
+        if (rec) plan[wv][64 * k + j] = ((uint32_t)__builtin_amdgcn_readlane(load, b & 63) << 6) | (uint32_t)b;
+        load = lane == b ? cand : load;
       }
     }
-    return true;
+    return ok;
   };
-  // parallel search: every wave tries one capacity of (lo, hi], the interval shrinks 16-fold
-  while (s_hi - s_lo > 1) {
+  // parallel search: every wave packs at one capacity of (lo, hi] and keeps its packing; the
+  // interval shrinks 16-fold per round, down to a step of 1/256 of the capacity.  If no capacity up
+  // to the first guess fits, the search goes on up to the bound where first fit always fits.
+  while (!s_fail && (s_hi - s_lo > max(1, s_hi >> 8) || s_best < 0)) {
     const int lo = s_lo, hi = s_hi;
     const int C = lo + (int)(((int64_t)(hi - lo) * (wv + 1) + 15) / 16);
-    const bool ok = ffd(C, false);
+    const bool ok = ffd(C, true);
     if (lane == 0) s_ok[wv] = ok ? C : -C;
     __syncthreads();
     if (tid == 0) {
-      int nlo = lo, nhi = hi;
+      int nlo = lo, nhi = hi, best = -1;
       for (int w = 0; w < 16; ++w) {
-        if (s_ok[w] > 0) nhi = min(nhi, s_ok[w]);
-        else nlo = max(nlo, -s_ok[w]);
+        if (s_ok[w] > 0) {
+          if (s_ok[w] <= nhi) {
+            nhi = s_ok[w];
+            best = w;
+          }
+        } else {
+          nlo = max(nlo, -s_ok[w]);
+        }
+      }
+      if (best < 0) {   // nothing fitted up to hi (its packing failed too): search above it
+        if (hi >= s_hi0) s_fail = 1;   // (cannot happen: first fit always fits at s_hi0)
+        nlo = hi;
+        nhi = s_hi0;
       }
       s_lo = nlo;
       s_hi = nhi;
+      s_best = best;
     }
     __syncthreads();
   }
-  // the chosen packing: planned start and bin of every item, then the items in order of start
-  if (wv == 0) ffd(s_hi, true);
+  if (s_fail) {
+    if (tid == 0) out[0] = -1;
+    return;
+  }
+  // the chosen packing, its items in order of planned start
+  const uint32_t* chosen = plan[s_best];
+  for (int i = tid; i < n; i += blockDim.x) key[i] = chosen[i];
+  for (int i = n + tid; i < ((n + 3) & ~3); i += blockDim.x) key[i] = 0xFFFFFFFFu;
   __syncthreads();
   for (int i = tid; i < n; i += blockDim.x) out[1 + rank_of(key, n, i)] = item[i];
   if (tid == 0) out[0] = n;
