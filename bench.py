@@ -76,12 +76,13 @@ def parse():
 
 # kernel symbol -> (entry point, source file holding it, whether each dispatch is one call of the
 # entry point; the others run inside a call beside such a kernel)
-# (attention template arguments: head dim, paged, P.V product)
+# (attention template arguments: head dim, paged, P.V product, persistent grid)
 KERNELS = {
-    "attn_mfma_kernel<128, true, true>": ("sx_sparse_attn", "k_attn.hip", True),
-    "attn_mfma_kernel<128, false, true>": ("sx_full_attn", "k_attn.hip", True),
+    "attn_mfma_kernel<128, true, true, true>": ("sx_sparse_attn", "k_attn.hip", True),
+    "attn_mfma_kernel<128, false, true, true>": ("sx_full_attn", "k_attn.hip", True),
+    "attn_mfma_kernel<128, false, true, false>": ("sx_full_attn", "k_attn.hip", True),   # (under graph capture)
     # two-pass scoring only (layers without a preceding full layer)
-    "attn_mfma_kernel<128, true, false>": ("sx_sparseq_score", "k_attn.hip", False),
+    "attn_mfma_kernel<128, true, false, false>": ("sx_sparseq_score", "k_attn.hip", False),
     "lse_merge_kernel": ("sx_sparseq_score", "k_attn.hip", False),
     "colsum_kernel<128, 2>": ("sx_sparseq_score", "k_attn.hip", True),
     "colsum_kernel<128, 1>": ("sx_sparseq_score", "k_attn.hip", True),
@@ -93,6 +94,7 @@ KERNELS = {
     "mark_rows_kernel": ("sx_realign_scatter", "k_copy.hip", False),   # (also sx_realign_scatter_layers)
     "fill_u8_kernel": ("sx_rows_mask", "k_copy.hip", True),
     "mask_rows_kernel": ("sx_rows_mask", "k_copy.hip", False),
+    "tile_order_kernel": ("sx_rows_mask", "k_attn.hip", False),
     "topk_hist_kernel": ("sx_topk_select", "k_topk.hip", False),
     "topk_bound_kernel": ("sx_topk_select", "k_topk.hip", False),
     "topk_write_kernel": ("sx_topk_select", "k_topk.hip", True),

@@ -51,7 +51,7 @@ def test_entry_without_counted_calls_or_with_stale_source_is_dropped(tmp_path, m
     # since its counters were taken makes its whole entry point unreported
     _setup(tmp_path, monkeypatch, {"mark_rows_kernel": (2, 7.0, False),
                                    "scatter_kernel": (4, 50.0, True),
-                                   "attn_mfma_kernel<128, true, true>": (28, 300.0, False)})
+                                   "attn_mfma_kernel<128, true, true, true>": (28, 300.0, False)})
     assert bench.load_traffic("w") == pytest.approx({"sx_sparse_attn": 300.0})
 
 
@@ -64,6 +64,22 @@ def test_every_kernel_symbol_names_a_source_that_exists():
     for sym, (entry, src, is_call) in bench.KERNELS.items():
         assert entry.startswith("sx_"), sym
         assert os.path.exists(os.path.join(ROOT, "paper_2606_01751_amd", "csrc", src)), sym
+
+
+def test_every_kernel_symbol_matches_a_kernel_of_its_source():
+    # the profiler names a template kernel with all its arguments, so a symbol with too few of them
+    # would match no dispatch: the kernel must be a __global__ of the named file, with as many
+    # template parameters as the symbol has arguments (a symbol without arguments stands for every
+    # instantiation)
+    import re
+    for sym, (entry, src, is_call) in bench.KERNELS.items():
+        text = open(os.path.join(ROOT, "paper_2606_01751_amd", "csrc", src)).read()
+        name, _, args = sym.partition("<")
+        m = re.search(r"(template <([^>]*)>\s*)?__global__\s+(__launch_bounds__\([^)]*\)\s+)?void\s+"
+                      + re.escape(name) + r"\(", text)
+        assert m, sym
+        if args:
+            assert m.group(2) and len(m.group(2).split(",")) == len(args.rstrip(">").split(",")), sym
 
 
 def test_more_than_one_gpu_is_refused_with_a_message():
