@@ -154,15 +154,15 @@ __global__ __launch_bounds__(512, 1) void attn_mfma_kernel(AttnK ka) {
   // belong to one request and share its K/V tiles through that XCD's L2.  (Pieces of one row tile
   // are adjacent.)  The log-sum-exp pass launches one workgroup per item.  Attention with output
   // (sparse, and full attention outside graph capture) runs a persistent grid instead: about one
-  // workgroup per compute unit and KV head, each taking its head's next item from that head's queue
-  // whenever it finishes one.  The
-  // items then go to whichever compute unit frees first (greedy longest-first), with no gap for
-  // the hardware to dispatch another workgroup; the hardware's own dispatch hands the workgroups of
-  // an XCD to its shader engines in turn and holds the rest back while the next one's engine is
-  // full, which left a tenth of the compute units idle in the tail.  A workgroup whose head's queue
-  // is empty moves on to the head whose queue holds the most items (the XCDs do not run at one
-  // speed, so the fast ones finish the slow ones' last, lightest items), and stops when every queue
-  // is empty.  The last workgroup to stop resets the counters for the next launch.
+  // workgroup per compute unit and KV head, each taking its head's next item from that head's
+  // queue whenever it finishes one.  The items then go to whichever compute unit frees first
+  // (greedy longest-first, or the planned order of tile_order_kernel), with no gap for the
+  // hardware to dispatch another workgroup; the hardware's own dispatch hands the workgroups of an
+  // XCD to its shader engines in turn and holds the rest back while the next one's engine is full,
+  // which left a tenth of the compute units idle in the tail.  A workgroup whose head's queue is
+  // empty moves on to the head whose queue holds the most items (the XCDs do not run at one speed,
+  // so the fast ones finish the slow ones' last, lightest items), and stops when every queue is
+  // empty.  The last workgroup to stop resets the counters for the next launch.
   static_assert(!PERSIST || PV, "persistent grids run attention with output only");
   int32_t* const queue = PAGED ? ka.queue : g_dense_queue + ka.qslot * kDenseQueueStride;
   __shared__ int2 s_take[2];   // (head, item) taken by wave 0, alternating slots
