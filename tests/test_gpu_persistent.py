@@ -160,3 +160,58 @@ def test_sparse_attention_planned_tile_order():
         a, b = offs[r], offs[r] + int(n[r] // 2)
         assert torch.equal(out[a:b], want[a:b]), f"request {r} with half its rows after the plan"
         assert not out[b:offs[r] + int(n[r])].any()
+
+
+def test_many_launches_cycle_every_queue_slot():
+    """70 full-attention launches (more than the 64 library queue slots, so every slot is reused)
+    of three sizes in turn, and 30 sparse-attention launches on one plan with three row counts in
+    turn: every result is bit-identical to the first one of its size, so each launch left its
+    counters at zero."""
+    w = _workload()
+    log("[persistent] 70 full-attention and 30 sparse-attention launches in turn")
+    t = W.layer_tensors(w, 0)
+    q, k, v = dev(t["q"], w), dev(t["k"], w), dev(t["v"], w)
+    offs = w.token_offsets
+    n_req = len(w.requests)
+    # full attention over the first 1, 2 and 3 requests
+    sizes = [(torch.tensor(offs[:i + 2], dtype=torch.int32, device="cuda"), i + 1,
+              max(r.n_tokens for r in w.requests[:i + 1])) for i in range(n_req)]
+    want = []
+    for cu, nr, mx in sizes:
+        o = torch.zeros_like(q)
+        sx.full_attn(desc_of(w), q, k, v, cu, nr, mx, o)
+        want.append(o)
+    torch.cuda.synchronize()
+    outs = []
+    for i in range(70):
+        cu, nr, mx = sizes[i % n_req]
+        o = torch.zeros_like(q)
+        sx.full_attn(desc_of(w), q, k, v, cu, nr, mx, o)
+        outs.append(o)
+    torch.cuda.synchronize()
+    for i, o in enumerate(outs):
+        assert torch.equal(o, want[i % n_req]), f"full-attention launch {i}"
+    g = GpuLayer(w, t)
+    ratio = 0.3
+    g.realign()
+    g.scatter_nonreused()
+    g.score()
+    g.select(ratio)
+    g.scatter_rows(ratio)
+    m = g.plan.budget(ratio)[1]
+    n = g.n_rows.cpu().numpy()
+    counts = [torch.from_numpy(np.maximum(n // d, 1).astype(np.int32)).to("cuda") for d in (1, 2, 3)]
+    ref = []
+    for c in counts:
+        o = torch.zeros_like(g.out)
+        sx.sparse_attn(g.plan, g.t["q"], g.rows, c, m, g.k_cache, g.v_cache, o)
+        ref.append(o)
+    torch.cuda.synchronize()
+    outs = []
+    for i in range(30):
+        o = torch.zeros_like(g.out)
+        sx.sparse_attn(g.plan, g.t["q"], g.rows, counts[i % 3], m, g.k_cache, g.v_cache, o)
+        outs.append(o)
+    torch.cuda.synchronize()
+    for i, o in enumerate(outs):
+        assert torch.equal(o, ref[i % 3]), f"sparse-attention launch {i}"
